@@ -1,0 +1,428 @@
+// Cross-attention variable aggregation (one learned query over the V variable
+// tokens of each patch), forward and backward, in the exact refolded form:
+//
+//   score_{t,h,v} = q_h . (W_k^h x_{t,v} + b_k^h) / sqrt(dh)
+//                 = x_{t,v} . u_h / sqrt(dh) + const_h,   u_h = W_k^h q_h
+//   (the constant is the same for every v and drops out of the softmax), and
+//   zh_{t,h} = sum_v a_{t,h,v} (W_v^h x_{t,v} + b_v^h) = W_v^h xbar_{t,h} + b_v^h
+//   with xbar_{t,h} = sum_v a_{t,h,v} x_{t,v}  (the weights sum to one).
+//
+// So the per-token key/value projections (2 T V d A flops) are never formed:
+// the token tensor is streamed twice through skinny MFMA products (scores,
+// xbar), and only xbar [T, H, d] meets W_v. The backward mirrors it.
+#include <algorithm>
+
+#include "agg.h"
+#include "gemm.h"
+#include "kernels.h"
+
+namespace orbit {
+namespace {
+
+// q[j] = q0 . w_q[:, j] + b_q[j]   (float32 out)
+template <typename T>
+__global__ void __launch_bounds__(256) agg_query(const T* __restrict__ q0, const T* __restrict__ wq,
+                                                 const T* __restrict__ bq, float* __restrict__ q, int d, int A) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= A) return;
+  float s = 0.f;
+  for (int i = 0; i < d; ++i) s += to_f(q0[i]) * to_f(wq[(int64_t)i * A + j]);
+  q[j] = s + to_f(bq[j]);
+}
+
+// Ut[h][i] = sum_c w_k[i][h*dh + c] q[h*dh + c]   (one wave per (i, 8 heads))
+template <typename T>
+__global__ void __launch_bounds__(256) agg_fold_key(const T* __restrict__ wk, const float* __restrict__ q,
+                                                    T* __restrict__ Ut, int d, int H, int dh) {
+  const int A = H * dh;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over d * H
+  if (idx >= (int64_t)d * H) return;
+  const int i = (int)(idx / H), h = (int)(idx % H);
+  const T* row = wk + (int64_t)i * A + h * dh;
+  float s = 0.f;
+  for (int c = 0; c < dh; ++c) s += to_f(row[c]) * q[h * dh + c];
+  Ut[(int64_t)h * d + i] = from_f<T>(s);
+}
+
+// softmax over v of S[(t*V + v)*H + h]: a32[t][h][v] (float32) and ab[t][h][0..Vp) (dtype, zero padded)
+template <typename T>
+__global__ void __launch_bounds__(256) agg_softmax(const float* __restrict__ S, float* __restrict__ a32,
+                                                   T* __restrict__ ab, int64_t T_, int V, int Vp, int H) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (t, h)
+  if (idx >= T_ * H) return;
+  const int64_t t = idx / H;
+  const int h = (int)(idx % H);
+  const float* s = S + t * V * H + h;
+  float m = -INFINITY;
+  for (int v = 0; v < V; ++v) m = fmaxf(m, s[(int64_t)v * H]);
+  float z = 0.f;
+  for (int v = 0; v < V; ++v) z += __expf(s[(int64_t)v * H] - m);
+  const float inv = 1.f / z;
+  float* ao = a32 + idx * V;
+  T* bo = ab + idx * Vp;
+  for (int v = 0; v < V; ++v) {
+    const float p = __expf(s[(int64_t)v * H] - m) * inv;
+    ao[v] = p;
+    bo[v] = from_f<T>(p);
+  }
+  for (int v = V; v < Vp; ++v) bo[v] = from_f<T>(0.f);
+}
+
+// softmax backward per (t, h): ds = a (da - sum a da) * scale.
+// ac[(t*V + v)*2H + h] = a, ac[(t*V + v)*2H + H + h] = ds   (dtype)
+template <typename T>
+__global__ void __launch_bounds__(256) agg_softmax_bwd(const float* __restrict__ a32, const float* __restrict__ da,
+                                                       T* __restrict__ ac, int64_t T_, int V, int H, float scale) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= T_ * H) return;
+  const int64_t t = idx / H;
+  const int h = (int)(idx % H);
+  const float* a = a32 + idx * V;
+  const float* g = da + idx * V;
+  float dot = 0.f;
+  for (int v = 0; v < V; ++v) dot += a[v] * g[v];
+  T* o = ac + t * V * 2 * H;
+  for (int v = 0; v < V; ++v) {
+    o[(int64_t)v * 2 * H + h] = from_f<T>(a[v]);
+    o[(int64_t)v * 2 * H + H + h] = from_f<T>(a[v] * (g[v] - dot) * scale);
+  }
+}
+
+// dq[j] = sum_i w_k[i][j] dU[i][h(j)]
+template <typename T>
+__global__ void __launch_bounds__(256) agg_dq(const T* __restrict__ wk, const float* __restrict__ dU,
+                                              float* __restrict__ dq, int d, int H, int dh) {
+  const int A = H * dh;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= A) return;
+  const int h = j / dh;
+  float s = 0.f;
+  for (int i = 0; i < d; ++i) s += to_f(wk[(int64_t)i * A + j]) * dU[(int64_t)i * H + h];
+  dq[j] = s;
+}
+
+// dW_k[i][j] = dU[i][h(j)] q[j];  dW_q[i][j] = q0[i] dq[j]
+template <typename T>
+__global__ void __launch_bounds__(256) agg_outer(const float* __restrict__ dU, const float* __restrict__ q,
+                                                 const T* __restrict__ q0, const float* __restrict__ dq,
+                                                 float* __restrict__ dwk, float* __restrict__ dwq, int d, int H,
+                                                 int dh, int accumulate) {
+  const int A = H * dh;
+  const int64_t total = (int64_t)d * A;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int i = (int)(e / A), j = (int)(e % A);
+    const float vk = dU[(int64_t)i * H + j / dh] * q[j];
+    const float vq = to_f(q0[i]) * dq[j];
+    dwk[e] = accumulate ? dwk[e] + vk : vk;
+    dwq[e] = accumulate ? dwq[e] + vq : vq;
+  }
+}
+
+// dq0[i] = sum_j w_q[i][j] dq[j]; db_q = dq; db_k = 0 (one wave per row i)
+template <typename T>
+__global__ void __launch_bounds__(256) agg_query_bwd(const T* __restrict__ wq, const float* __restrict__ dq,
+                                                     float* dq0, float* dbq, float* dbk, int d, int A,
+                                                     int accumulate) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + wave;
+  if (i < d) {
+    float s = 0.f;
+    for (int j = lane; j < A; j += 64) s += to_f(wq[(int64_t)i * A + j]) * dq[j];
+    s = wave_sum(s);
+    if (lane == 0) dq0[i] = accumulate ? dq0[i] + s : s;
+  }
+  if (blockIdx.x == 0) {
+    for (int j = threadIdx.x; j < A; j += 256) {
+      dbq[j] = accumulate ? dbq[j] + dq[j] : dq[j];
+      if (!accumulate) dbk[j] = 0.f;
+    }
+  }
+}
+
+unsigned g1(int64_t n) { return (unsigned)std::max<int64_t>(1, cdiv(n, 256)); }
+
+struct Sizes {
+  int64_t T;
+  int V, Vp, d, H, dh, A, L, B;
+};
+Sizes sizes(const orbit_agg_desc& a) {
+  Sizes s;
+  s.B = a.B; s.L = a.L; s.T = (int64_t)a.B * a.L; s.V = a.V; s.Vp = (a.V + 7) / 8 * 8;
+  s.d = a.d; s.H = a.heads; s.dh = a.head_dim; s.A = a.heads * a.head_dim;
+  return s;
+}
+size_t esz(orbit_dtype dt) { return dt == ORBIT_BF16 ? 2 : 4; }
+
+// saved layout: q f32 [A] | Ut [H, d] | a32 [T, H, V] | xbar [T, H, d] | zh [T, A]
+struct Saved {
+  float* q; void* Ut; float* a32; void* xbar; void* zh;
+};
+Saved carve_saved(const Sizes& z, orbit_dtype dt, void* base, size_t* used) {
+  Carver c(base);
+  Saved s;
+  s.q = c.take<float>(z.A);
+  s.Ut = c.take<char>((size_t)z.H * z.d * esz(dt));
+  s.a32 = c.take<float>((size_t)z.T * z.H * z.V);
+  s.xbar = c.take<char>((size_t)z.T * z.H * z.d * esz(dt));
+  s.zh = c.take<char>((size_t)z.T * z.A * esz(dt));
+  if (used) *used = c.used();
+  return s;
+}
+
+Gemm base_gemm(orbit_dtype dt) {
+  Gemm g;
+  g.dtype = dt;
+  return g;
+}
+
+}  // namespace
+
+size_t agg_saved_bytes(const orbit_agg_desc& a) {
+  size_t u = 0;
+  carve_saved(sizes(a), (orbit_dtype)a.dtype, nullptr, &u);
+  return u;
+}
+
+// forward workspace: S f32 [T*V, H] | ab [T, H, Vp] | gemm split-K
+// backward workspace: dzh [T, A] | dxbar [T, H, d] | da f32 [T, H, V] | ac [T*V, 2H] | dU f32 [d, H]
+//                     | dq f32 [A] | colsum | gemm split-K
+static size_t gemm_ws_max(const Sizes& z, orbit_dtype dt) {
+  // the only products that may split K are the ones with few output tiles
+  Gemm g = base_gemm(dt);
+  size_t m = 0;
+  g.M = z.d; g.N = z.H; g.K = (int)(z.T * z.V); g.a_kmajor = false; g.b_kmajor = false;
+  m = std::max(m, gemm_workspace_bytes(g));
+  g.M = z.A; g.N = z.d; g.K = (int)z.T;
+  m = std::max(m, gemm_workspace_bytes(g));
+  g.M = z.d; g.N = z.dh; g.K = (int)z.T; g.batch = z.H;
+  m = std::max(m, gemm_workspace_bytes(g));
+  return m;
+}
+
+size_t agg_workspace_bytes(const orbit_agg_desc& a) {
+  const Sizes z = sizes(a);
+  const orbit_dtype dt = (orbit_dtype)a.dtype;
+  Carver f(nullptr);
+  f.take<float>((size_t)z.T * z.V * z.H);
+  f.take<char>((size_t)z.T * z.H * z.Vp * esz(dt));
+  size_t fwd = f.used();
+  Carver b(nullptr);
+  b.take<char>((size_t)z.T * z.A * esz(dt));
+  b.take<char>((size_t)z.T * z.H * z.d * esz(dt));
+  b.take<float>((size_t)z.T * z.H * z.V);
+  b.take<char>((size_t)z.T * z.V * 2 * z.H * esz(dt));
+  b.take<float>((size_t)z.d * z.H);
+  b.take<float>((size_t)z.A);
+  b.take<char>(std::max(colsum_workspace_bytes((int)z.T, std::max(z.d, z.A)),
+                        colsum_workspace_bytes(z.B, z.L * z.d)));
+  size_t bwd = b.used();
+  return std::max(fwd, bwd) + gemm_ws_max(z, dt);
+}
+
+orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_agg_params& p, void* z_out,
+                         void* saved, void* ws, size_t ws_bytes, hipStream_t s) {
+  const Sizes z = sizes(a);
+  const orbit_dtype dt = (orbit_dtype)a.dtype;
+  const Saved sv = carve_saved(z, dt, saved, nullptr);
+  Carver w(ws);
+  float* S = w.take<float>((size_t)z.T * z.V * z.H);
+  void* ab = w.take<char>((size_t)z.T * z.H * z.Vp * esz(dt));
+  void* gws = w.take<char>(0);
+  const size_t gws_bytes = ws_bytes - w.used();
+  const int64_t TV = z.T * z.V;
+
+  // 1. q = q0 W_q + b_q;  Ut[h] = W_k^h q_h
+  KernelInfo kq{"agg_query", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
+  KernelInfo ku{"agg_fold_key", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
+  if (dt == ORBIT_BF16) {
+    ORBIT_TRY(launch(kq, agg_query<bf16>, dim3(g1(z.A)), dim3(256), 0, s, (const bf16*)p.q0, (const bf16*)p.w_q,
+                     (const bf16*)p.b_q, sv.q, z.d, z.A));
+    ORBIT_TRY(launch(ku, agg_fold_key<bf16>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s, (const bf16*)p.w_k,
+                     (const float*)sv.q, (bf16*)sv.Ut, z.d, z.H, z.dh));
+  } else {
+    ORBIT_TRY(launch(kq, agg_query<float>, dim3(g1(z.A)), dim3(256), 0, s, (const float*)p.q0,
+                     (const float*)p.w_q, (const float*)p.b_q, sv.q, z.d, z.A));
+    ORBIT_TRY(launch(ku, agg_fold_key<float>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s,
+                     (const float*)p.w_k, (const float*)sv.q, (float*)sv.Ut, z.d, z.H, z.dh));
+  }
+  // 2. scores S[t*V+v][h] = x_{t,v} . u_h / sqrt(dh)
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_scores";
+    g.A = tok; g.lda = z.d; g.a_kmajor = true;
+    g.B = sv.Ut; g.ldb = z.d; g.b_kmajor = true;
+    g.C = S; g.ldc = z.H; g.out_f32 = true;
+    g.M = (int)TV; g.N = z.H; g.K = z.d;
+    g.alpha = 1.f / sqrtf((float)z.dh);
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // 3. softmax over variables
+  KernelInfo ks{"agg_softmax", 0.0, (double)TV * z.H * 8};
+  if (dt == ORBIT_BF16)
+    ORBIT_TRY(launch(ks, agg_softmax<bf16>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)S, sv.a32,
+                     (bf16*)ab, z.T, z.V, z.Vp, z.H));
+  else
+    ORBIT_TRY(launch(ks, agg_softmax<float>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)S, sv.a32,
+                     (float*)ab, z.T, z.V, z.Vp, z.H));
+  // 4. xbar_t = a_t [H, V] X_t [V, d]   (batched over tokens)
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_xbar";
+    g.A = ab; g.lda = z.Vp; g.a_kmajor = true; g.sA = (int64_t)z.H * z.Vp;
+    g.B = tok; g.ldb = z.d; g.b_kmajor = false; g.sB = (int64_t)z.V * z.d;
+    g.C = sv.xbar; g.ldc = z.d; g.sC = (int64_t)z.H * z.d;
+    g.M = z.H; g.N = z.d; g.K = z.V; g.batch = (int)z.T;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // 5. zh_h = xbar_h W_v^h + b_v^h   (batched over heads)
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_value";
+    g.A = sv.xbar; g.lda = (int64_t)z.H * z.d; g.a_kmajor = true; g.sA = z.d;
+    g.B = p.w_v; g.ldb = z.A; g.b_kmajor = false; g.sB = z.dh;
+    g.C = sv.zh; g.ldc = z.A; g.sC = z.dh;
+    g.bias = p.b_v; g.sBias = z.dh;
+    g.M = (int)z.T; g.N = z.dh; g.K = z.d; g.batch = z.H;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // 6. z = zh W_o + b_o + pos[l]
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_out";
+    g.A = sv.zh; g.lda = z.A; g.a_kmajor = true;
+    g.B = p.w_o; g.ldb = z.d; g.b_kmajor = false;
+    g.C = z_out; g.ldc = z.d;
+    g.bias = p.b_o;
+    if (p.pos) { g.res = p.pos; g.ldr = z.d; g.res_row_mod = z.L; }
+    g.M = (int)z.T; g.N = z.d; g.K = z.A;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  return ORBIT_OK;
+}
+
+orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_agg_params& p, const void* saved,
+                          const void* dz, void* dtok, const orbit_agg_grads& gr, int accumulate, void* ws,
+                          size_t ws_bytes, hipStream_t s) {
+  const Sizes z = sizes(a);
+  const orbit_dtype dt = (orbit_dtype)a.dtype;
+  const Saved sv = carve_saved(z, dt, const_cast<void*>(saved), nullptr);
+  Carver w(ws);
+  void* dzh = w.take<char>((size_t)z.T * z.A * esz(dt));
+  void* dxbar = w.take<char>((size_t)z.T * z.H * z.d * esz(dt));
+  float* da = w.take<float>((size_t)z.T * z.H * z.V);
+  void* ac = w.take<char>((size_t)z.T * z.V * 2 * z.H * esz(dt));
+  float* dU = w.take<float>((size_t)z.d * z.H);
+  float* dq = w.take<float>((size_t)z.A);
+  void* cws = w.take<char>(std::max(colsum_workspace_bytes((int)z.T, std::max(z.d, z.A)),
+                                    colsum_workspace_bytes(z.B, z.L * z.d)));
+  void* gws = w.take<char>(0);
+  const size_t gws_bytes = ws_bytes - w.used();
+  const int64_t TV = z.T * z.V;
+  const float scale = 1.f / sqrtf((float)z.dh);
+
+  // output projection: dpos, db_o, dW_o, dzh
+  if (gr.pos) ORBIT_TRY(colsum(dt, dz, (int64_t)z.L * z.d, z.B, z.L * z.d, nullptr, 0, nullptr, nullptr, gr.pos,
+                               nullptr, accumulate, cws, s));
+  ORBIT_TRY(colsum(dt, dz, z.d, (int)z.T, z.d, nullptr, 0, nullptr, nullptr, gr.b_o, nullptr, accumulate, cws, s));
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_out_dw";
+    g.A = sv.zh; g.lda = z.A; g.a_kmajor = false;
+    g.B = dz; g.ldb = z.d; g.b_kmajor = false;
+    g.C = gr.w_o; g.ldc = z.d; g.out_f32 = true; g.accumulate = accumulate != 0;
+    g.M = z.A; g.N = z.d; g.K = (int)z.T;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_out_dx";
+    g.A = dz; g.lda = z.d; g.a_kmajor = true;
+    g.B = p.w_o; g.ldb = z.d; g.b_kmajor = true;
+    g.C = dzh; g.ldc = z.A;
+    g.M = (int)z.T; g.N = z.A; g.K = z.d;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // value path: db_v, dW_v^h = xbar_h^T dzh_h, dxbar_h = dzh_h W_v^h^T
+  ORBIT_TRY(colsum(dt, dzh, z.A, (int)z.T, z.A, nullptr, 0, nullptr, nullptr, gr.b_v, nullptr, accumulate, cws, s));
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_value_dw";
+    g.A = sv.xbar; g.lda = (int64_t)z.H * z.d; g.a_kmajor = false; g.sA = z.d;
+    g.B = dzh; g.ldb = z.A; g.b_kmajor = false; g.sB = z.dh;
+    g.C = gr.w_v; g.ldc = z.A; g.sC = z.dh; g.out_f32 = true; g.accumulate = accumulate != 0;
+    g.M = z.d; g.N = z.dh; g.K = (int)z.T; g.batch = z.H;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_value_dx";
+    g.A = dzh; g.lda = z.A; g.a_kmajor = true; g.sA = z.dh;
+    g.B = p.w_v; g.ldb = z.A; g.b_kmajor = true; g.sB = z.dh;
+    g.C = dxbar; g.ldc = (int64_t)z.H * z.d; g.sC = z.d;
+    g.M = (int)z.T; g.N = z.d; g.K = z.dh; g.batch = z.H;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // da_t [H, V] = dxbar_t [H, d] X_t^T
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_da";
+    g.A = dxbar; g.lda = z.d; g.a_kmajor = true; g.sA = (int64_t)z.H * z.d;
+    g.B = tok; g.ldb = z.d; g.b_kmajor = true; g.sB = (int64_t)z.V * z.d;
+    g.C = da; g.ldc = z.V; g.sC = (int64_t)z.H * z.V; g.out_f32 = true;
+    g.M = z.H; g.N = z.V; g.K = z.d; g.batch = (int)z.T;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // softmax backward -> ac = [a | ds] per (t, v) row
+  KernelInfo ksb{"agg_softmax_bwd", 0.0, (double)TV * z.H * (8 + 4 * esz(dt))};
+  if (dt == ORBIT_BF16)
+    ORBIT_TRY(launch(ksb, agg_softmax_bwd<bf16>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)sv.a32,
+                     (const float*)da, (bf16*)ac, z.T, z.V, z.H, scale));
+  else
+    ORBIT_TRY(launch(ksb, agg_softmax_bwd<float>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)sv.a32,
+                     (const float*)da, (float*)ac, z.T, z.V, z.H, scale));
+  // dU [d, H] = X^T ds  (reduction over all T*V token rows)
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_du";
+    g.A = tok; g.lda = z.d; g.a_kmajor = false;
+    g.B = static_cast<const char*>(ac) + z.H * esz(dt); g.ldb = 2 * z.H; g.b_kmajor = false;
+    g.C = dU; g.ldc = z.H; g.out_f32 = true;
+    g.M = z.d; g.N = z.H; g.K = (int)TV;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  // query path
+  KernelInfo kdq{"agg_dq", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
+  KernelInfo kou{"agg_outer", 2.0 * z.d * z.A, 8.0 * z.d * z.A};
+  KernelInfo kqb{"agg_query_bwd", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
+  if (dt == ORBIT_BF16) {
+    ORBIT_TRY(launch(kdq, agg_dq<bf16>, dim3(g1(z.A)), dim3(256), 0, s, (const bf16*)p.w_k, (const float*)dU, dq,
+                     z.d, z.H, z.dh));
+    ORBIT_TRY(launch(kou, agg_outer<bf16>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
+                     dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const bf16*)p.q0, (const float*)dq,
+                     gr.w_k, gr.w_q, z.d, z.H, z.dh, accumulate));
+    ORBIT_TRY(launch(kqb, agg_query_bwd<bf16>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s, (const bf16*)p.w_q,
+                     (const float*)dq, gr.q0, gr.b_q, gr.b_k, z.d, z.A, accumulate));
+  } else {
+    ORBIT_TRY(launch(kdq, agg_dq<float>, dim3(g1(z.A)), dim3(256), 0, s, (const float*)p.w_k, (const float*)dU,
+                     dq, z.d, z.H, z.dh));
+    ORBIT_TRY(launch(kou, agg_outer<float>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
+                     dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const float*)p.q0, (const float*)dq,
+                     gr.w_k, gr.w_q, z.d, z.H, z.dh, accumulate));
+    ORBIT_TRY(launch(kqb, agg_query_bwd<float>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s,
+                     (const float*)p.w_q, (const float*)dq, gr.q0, gr.b_q, gr.b_k, z.d, z.A, accumulate));
+  }
+  // dtok_t [V, d] = [a^T | ds] [V, 2H] . [dxbar_t ; U^T] [2H, d]   (batched over tokens)
+  {
+    Gemm g = base_gemm(dt);
+    g.tag = "agg_dtok";
+    g.A = ac; g.lda = 2 * z.H; g.a_kmajor = true; g.sA = (int64_t)z.V * 2 * z.H;
+    g.B = dxbar; g.ldb = z.d; g.b_kmajor = false; g.sB = (int64_t)z.H * z.d;
+    g.B2 = sv.Ut; g.k_split = z.H; g.sB2 = 0;
+    g.C = dtok; g.ldc = z.d; g.sC = (int64_t)z.V * z.d;
+    g.M = z.V; g.N = z.d; g.K = 2 * z.H; g.batch = (int)z.T;
+    ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+  }
+  return ORBIT_OK;
+}
+
+}  // namespace orbit

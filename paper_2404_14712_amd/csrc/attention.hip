@@ -1,0 +1,559 @@
+// Fused multi-head self-attention O = softmax(q k^T / sqrt(dh)) v (no mask),
+// forward with an online softmax held in registers and backward in the
+// two-kernel deterministic form (K/V-major kernel for dK, dV; Q-major kernel
+// for dQ; no atomics), on 32x32x16 MFMA tiles.
+//
+// Layout trick: the forward computes S^T = K Q^T, so each lane owns one query
+// (accumulator column) and the probabilities P^T come out of the accumulator
+// already in the B-operand layout of O^T = V^T P^T; V is staged transposed in
+// LDS so its fragments are two 8-byte reads. The backward uses the same idea
+// in both orientations (see the per-kernel comments).
+#include <algorithm>
+
+#include "kernels.h"
+#include "tile.h"
+
+namespace orbit {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+struct FwdArgs {
+  const void *q, *k, *v;
+  void* o;
+  float* lse;
+  int64_t ldq, ldk, ldv, ldo;
+  int H, L;
+  float sl2;  // log2(e) / sqrt(dh)
+};
+
+// lane l: fragment slot j (0..7) of lane group g = l/32 in a 16-deep K step of
+// an accumulator-derived operand covers index (j/4)*8 + g*4 + j%4 of the step.
+// read that fragment from a transposed LDS row: two runs of 4.
+template <typename T>
+ORBIT_DEV void ld_frag_acc_order(Frag<T>& f, const T* row, int kstep, int g) {
+  ld_frag2(f, row + kstep * 16 + g * 4, row + kstep * 16 + 8 + g * 4);
+}
+
+// fragment of 8 values of an accumulator (registers base..base+7) as T
+template <typename T>
+ORBIT_DEV void acc_frag(Frag<T>& f, const f32x16& a, int base) {
+  float t[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) t[j] = a[base + j];
+  frag_from(f, t);
+}
+
+// store 4 consecutive floats as T
+template <typename T>
+ORBIT_DEV void st4(T* p, float a, float b, float c, float d) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
+    *reinterpret_cast<bf16x4*>(p) = v;
+  } else {
+    f32x4 v = {a, b, c, d};
+    *reinterpret_cast<f32x4*>(p) = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// forward: 4 waves x 32 queries per block, 64-key tiles
+// ---------------------------------------------------------------------------
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) attn_fwd_kernel(FwdArgs a) {
+  constexpr int KT = 64;
+  constexpr int E = 16 / (int)sizeof(T);
+  using LK = TileLoader<T, KT, DH, 256, true>;    // K rows  [kv][c]
+  using LV = TileLoader<T, DH, KT, 256, false>;   // V^T     [c][kv]
+  constexpr int KP = LK::PITCH, VP = LV::PITCH;
+  __shared__ __attribute__((aligned(16))) T ks[2][KT * KP];
+  __shared__ __attribute__((aligned(16))) T vs[2][DH * VP];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int L = a.L;
+  const int64_t row0 = (int64_t)b * L;
+  const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
+  const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
+  const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
+
+  const int qi = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  Frag<T> qf[DH / 16];
+#pragma unroll
+  for (int kk = 0; kk < DH / 16; ++kk) {
+    if (qi < L) ld_frag(qf[kk], Q + (int64_t)qi * a.ldq + kk * 16 + g * 8);
+    else {
+      float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      frag_from(qf[kk], z);
+    }
+  }
+
+  f32x16 o[DH / 32];
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[c][v] = 0.f;
+  float m = -INFINITY, lsum = 0.f;
+
+  LK lk;
+  LV lv;
+  const int nt = (L + KT - 1) / KT;
+  lk.load(K, nullptr, 0, a.ldk, 0, L, 0, DH, tid);
+  lv.load(V, nullptr, 0, a.ldv, 0, DH, 0, L, tid);
+  lk.store(ks[0], tid);
+  lv.store(vs[0], tid);
+  __syncthreads();
+
+  for (int jt = 0; jt < nt; ++jt) {
+    const int cur = jt & 1;
+    if (jt + 1 < nt) {
+      const int j0 = (jt + 1) * KT;
+      lk.load(K, nullptr, 0, a.ldk, j0, L, 0, DH, tid);
+      lv.load(V + (int64_t)j0 * a.ldv, nullptr, 0, a.ldv, 0, DH, 0, L - j0, tid);
+    }
+    const T* Ks = ks[cur];
+    const T* Vs = vs[cur];
+    // S^T[kv][q] for 64 keys: two 32-row tiles
+    f32x16 s[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[mt][v] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DH / 16; ++kk) {
+        Frag<T> kf;
+        ld_frag(kf, Ks + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+        mma16(s[mt], kf, qf[kk]);
+      }
+    }
+    // online softmax over this tile (log2 domain); lane owns query qi
+    const int jbase = jt * KT;
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int kv = jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
+        const float x = kv < L ? s[mt][v] * a.sl2 : -INFINITY;
+        s[mt][v] = x;
+        mloc = fmaxf(mloc, x);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float mnew = fmaxf(m, mloc);
+    const float alpha = exp2f(m - mnew);
+    float ps = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = exp2f(s[mt][v] - mnew);
+        s[mt][v] = p;
+        ps += p;
+      }
+    lsum = lsum * alpha + ps;
+    m = mnew;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[c][v] *= alpha;
+    // O^T[c][q] += V^T[c][kv] P^T[kv][q]
+#pragma unroll
+    for (int kk = 0; kk < KT / 16; ++kk) {
+      Frag<T> pf;
+      acc_frag(pf, s[kk >> 1], (kk & 1) * 8);
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        Frag<T> vf;
+        ld_frag_acc_order(vf, Vs + (c * 32 + (lane & 31)) * VP, kk, g);
+        mma16(o[c], vf, pf);
+      }
+    }
+    if (jt + 1 < nt) {
+      lk.store(ks[cur ^ 1], tid);
+      lv.store(vs[cur ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  if (qi < L) {
+    const float inv = 1.f / ltot;
+    T* O = static_cast<T*>(a.o) + (row0 + qi) * a.ldo + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + r4 * 8 + g * 4;
+        st4(O + col, o[c][r4 * 4] * inv, o[c][r4 * 4 + 1] * inv, o[c][r4 * 4 + 2] * inv,
+            o[c][r4 * 4 + 3] * inv);
+      }
+    if (g == 0) a.lse[((int64_t)b * a.H + h) * L + qi] = (m + __log2f(ltot)) * kLn2;
+  }
+  (void)E;
+}
+
+// ---------------------------------------------------------------------------
+// backward preprocess: D[b,h,i] = sum_c dO[i,c] O[i,c]
+// ---------------------------------------------------------------------------
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) attn_bwd_pre(const T* __restrict__ o, int64_t ldo, const T* __restrict__ dO,
+                                                    int64_t lddo, float* __restrict__ D, int B, int H, int L) {
+  constexpr int G = DH / 8;
+  const int li = threadIdx.x % G;
+  const int64_t row = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;  // (t, h)
+  const bool valid = row < (int64_t)B * L * H;
+  const int64_t t = valid ? row / H : 0;
+  const int h = valid ? (int)(row % H) : 0;
+  float s = 0.f;
+  if (valid) {
+    float a8[8], b8[8];
+    unpack(ld128(o + t * ldo + h * DH + li * 8), a8, (T*)nullptr);
+    unpack(ld128(dO + t * lddo + h * DH + li * 8), b8, (T*)nullptr);
+    if constexpr (sizeof(T) == 4) {
+      float a2[4], b2[4];
+      unpack(ld128(o + t * ldo + h * DH + li * 8 + 4), a2, (T*)nullptr);
+      unpack(ld128(dO + t * lddo + h * DH + li * 8 + 4), b2, (T*)nullptr);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { a8[4 + i] = a2[i]; b8[4 + i] = b2[i]; }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += a8[i] * b8[i];
+  }
+#pragma unroll
+  for (int off = G / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (valid && li == 0) {
+    const int64_t bb = t / L, l = t % L;
+    D[(bb * H + h) * L + l] = s;
+  }
+}
+
+struct BwdArgs {
+  const void *q, *k, *v, *dO;
+  const float *lse, *D;
+  void *dq, *dk, *dv;
+  int64_t ldq, ldk, ldv, lddo, ldg;
+  int H, L;
+  float sl2, scale;  // log2(e)/sqrt(dh), 1/sqrt(dh)
+};
+
+// Stage a 32-row x DH tile X[r][c] (rows r0.., valid < rlim) into LDS twice:
+// row-major Xs[r][c] (pitch DH+E) and transposed Xt[c][r] (pitch 32+E).
+template <typename T, int DH, int NT>
+struct DualStage {
+  static constexpr int E = 16 / (int)sizeof(T);
+  static constexpr int RP = DH + E, TP = 32 + E;
+  static constexpr int NU = (32 / 4) * (DH / E);  // units of 4 rows x E columns
+  static constexpr int PER = (NU + NT - 1) / NT;
+  U128 r[PER * 4];
+  ORBIT_DEV void load(const T* X, int64_t ld, int r0, int rlim, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = tid + i * NT;
+      const int rg = u / (DH / E), cc = u % (DH / E);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int rr = r0 + rg * 4 + j;
+        r[i * 4 + j] = (u < NU && rr < rlim) ? ld128(X + (int64_t)rr * ld + cc * E) : zero128();
+      }
+    }
+  }
+  ORBIT_DEV void store(T* Xs, T* Xt, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = tid + i * NT;
+      if (u >= NU) continue;
+      const int rg = u / (DH / E), cc = u % (DH / E);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) st128(Xs + (rg * 4 + j) * RP + cc * E, r[i * 4 + j]);
+      TileLoader<T, DH, 32, NT, false>::store_transposed(Xt + (cc * E) * TP + rg * 4, &r[i * 4]);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// backward, K/V-major: each wave owns 32 keys (K, V fragments in registers)
+// and sweeps all queries in tiles of 32:
+//   S = Q K^T (lane <-> key column), P = exp(S/sqrt(dh) - lse), dP = dO V^T,
+//   dS = P (dP - D);  dV^T += dO^T P,  dK^T += Q^T dS  (P, dS feed the MFMA
+//   B operand straight from the accumulator; dO^T, Q^T are staged transposed).
+// ---------------------------------------------------------------------------
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
+  using DS = DualStage<T, DH, 256>;
+  constexpr int RP = DS::RP, TP = DS::TP;
+  __shared__ __attribute__((aligned(16))) T qs[32 * RP];
+  __shared__ __attribute__((aligned(16))) T qt[DH * TP];
+  __shared__ __attribute__((aligned(16))) T ds_[32 * RP];
+  __shared__ __attribute__((aligned(16))) T dt[DH * TP];
+  __shared__ float lse_s[32], d_s[32];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int L = a.L;
+  const int64_t row0 = (int64_t)b * L;
+  const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
+  const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
+  const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
+  const T* dO = static_cast<const T*>(a.dO) + row0 * a.lddo + h * DH;
+  const float* lse = a.lse + ((int64_t)b * a.H + h) * L;
+  const float* Dv = a.D + ((int64_t)b * a.H + h) * L;
+
+  const int kv = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  Frag<T> kf[DH / 16], vf[DH / 16];
+#pragma unroll
+  for (int kk = 0; kk < DH / 16; ++kk) {
+    if (kv < L) {
+      ld_frag(kf[kk], K + (int64_t)kv * a.ldk + kk * 16 + g * 8);
+      ld_frag(vf[kk], V + (int64_t)kv * a.ldv + kk * 16 + g * 8);
+    } else {
+      float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      frag_from(kf[kk], z);
+      frag_from(vf[kk], z);
+    }
+  }
+  f32x16 dvt[DH / 32], dkt[DH / 32];
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dvt[c][v] = dkt[c][v] = 0.f;
+
+  DS sq, sd;
+  const int nq = (L + 31) / 32;
+  for (int it = 0; it < nq; ++it) {
+    const int q0 = it * 32;
+    sq.load(Q, a.ldq, q0, L, tid);
+    sd.load(dO, a.lddo, q0, L, tid);
+    __syncthreads();  // previous tile fully consumed
+    sq.store(qs, qt, tid);
+    sd.store(ds_, dt, tid);
+    if (tid < 32) {
+      const int qq = q0 + tid;
+      lse_s[tid] = qq < L ? lse[qq] * kLog2e : INFINITY;
+      d_s[tid] = qq < L ? Dv[qq] : 0.f;
+    }
+    __syncthreads();
+
+    f32x16 s, dp;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) {
+      Frag<T> af;
+      ld_frag(af, qs + (lane & 31) * RP + kk * 16 + g * 8);
+      mma16(s, af, kf[kk]);
+      ld_frag(af, ds_ + (lane & 31) * RP + kk * 16 + g * 8);
+      mma16(dp, af, vf[kk]);
+    }
+    // rows: query 8*(v/4) + 4g + v%4 of the tile; column: this lane's key
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int qr = (v >> 2) * 8 + g * 4 + (v & 3);
+      const float p = exp2f(s[v] * a.sl2 - lse_s[qr]);
+      s[v] = p;
+      dp[v] = p * (dp[v] - d_s[qr]);
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      Frag<T> pf, sf;
+      acc_frag(pf, s, kk * 8);
+      acc_frag(sf, dp, kk * 8);
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        Frag<T> af;
+        ld_frag_acc_order(af, dt + (c * 32 + (lane & 31)) * TP, kk, g);
+        mma16(dvt[c], af, pf);
+        ld_frag_acc_order(af, qt + (c * 32 + (lane & 31)) * TP, kk, g);
+        mma16(dkt[c], af, sf);
+      }
+    }
+  }
+
+  if (kv < L) {
+    T* dK = static_cast<T*>(a.dk) + (row0 + kv) * a.ldg + h * DH;
+    T* dV = static_cast<T*>(a.dv) + (row0 + kv) * a.ldg + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + r4 * 8 + g * 4;
+        st4(dK + col, dkt[c][r4 * 4] * a.scale, dkt[c][r4 * 4 + 1] * a.scale, dkt[c][r4 * 4 + 2] * a.scale,
+            dkt[c][r4 * 4 + 3] * a.scale);
+        st4(dV + col, dvt[c][r4 * 4], dvt[c][r4 * 4 + 1], dvt[c][r4 * 4 + 2], dvt[c][r4 * 4 + 3]);
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward, Q-major: each wave owns 32 queries (Q, dO fragments in registers)
+// and sweeps all keys in tiles of 64:
+//   S^T = K Q^T, P^T, dP^T = V dO^T, dS^T = P^T (dP^T - D);  dQ^T += K^T dS^T
+// ---------------------------------------------------------------------------
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
+  constexpr int KT = 64;
+  using LK = TileLoader<T, KT, DH, 256, true>;    // K, V rows [kv][c]
+  using LT = TileLoader<T, DH, KT, 256, false>;   // K^T      [c][kv]
+  constexpr int KP = LK::PITCH, TP = LT::PITCH;
+  __shared__ __attribute__((aligned(16))) T ks[KT * KP];
+  __shared__ __attribute__((aligned(16))) T vs[KT * KP];
+  __shared__ __attribute__((aligned(16))) T kt[DH * TP];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int L = a.L;
+  const int64_t row0 = (int64_t)b * L;
+  const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
+  const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
+  const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
+  const T* dO = static_cast<const T*>(a.dO) + row0 * a.lddo + h * DH;
+
+  const int qi = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  Frag<T> qf[DH / 16], of[DH / 16];
+#pragma unroll
+  for (int kk = 0; kk < DH / 16; ++kk) {
+    if (qi < L) {
+      ld_frag(qf[kk], Q + (int64_t)qi * a.ldq + kk * 16 + g * 8);
+      ld_frag(of[kk], dO + (int64_t)qi * a.lddo + kk * 16 + g * 8);
+    } else {
+      float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      frag_from(qf[kk], z);
+      frag_from(of[kk], z);
+    }
+  }
+  const float lse2 = qi < L ? a.lse[((int64_t)b * a.H + h) * L + qi] * kLog2e : INFINITY;
+  const float Dq = qi < L ? a.D[((int64_t)b * a.H + h) * L + qi] : 0.f;
+
+  f32x16 dqt[DH / 32];
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dqt[c][v] = 0.f;
+
+  LK lk, lvv;
+  LT lt;
+  const int nt = (L + KT - 1) / KT;
+  for (int jt = 0; jt < nt; ++jt) {
+    const int j0 = jt * KT;
+    lk.load(K, nullptr, 0, a.ldk, j0, L, 0, DH, tid);
+    lvv.load(V, nullptr, 0, a.ldv, j0, L, 0, DH, tid);
+    lt.load(K + (int64_t)j0 * a.ldk, nullptr, 0, a.ldk, 0, DH, 0, L - j0, tid);
+    __syncthreads();
+    lk.store(ks, tid);
+    lvv.store(vs, tid);
+    lt.store(kt, tid);
+    __syncthreads();
+
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[mt][v] = dp[mt][v] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DH / 16; ++kk) {
+        Frag<T> af;
+        ld_frag(af, ks + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+        mma16(s[mt], af, qf[kk]);
+        ld_frag(af, vs + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+        mma16(dp[mt], af, of[kk]);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int kvi = j0 + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
+        const float p = kvi < L ? exp2f(s[mt][v] * a.sl2 - lse2) : 0.f;
+        dp[mt][v] = p * (dp[mt][v] - Dq);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KT / 16; ++kk) {
+      Frag<T> sf;
+      acc_frag(sf, dp[kk >> 1], (kk & 1) * 8);
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        Frag<T> af;
+        ld_frag_acc_order(af, kt + (c * 32 + (lane & 31)) * TP, kk, g);
+        mma16(dqt[c], af, sf);
+      }
+    }
+  }
+
+  if (qi < L) {
+    T* dQ = static_cast<T*>(a.dq) + (row0 + qi) * a.ldg + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + r4 * 8 + g * 4;
+        st4(dQ + col, dqt[c][r4 * 4] * a.scale, dqt[c][r4 * 4 + 1] * a.scale, dqt[c][r4 * 4 + 2] * a.scale,
+            dqt[c][r4 * 4 + 3] * a.scale);
+      }
+  }
+}
+
+template <typename T, int DH>
+orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream_t s) {
+  FwdArgs a{io.q, io.k, io.v, o, lse, io.ldq, io.ldk, io.ldv, ldo, io.H, io.L, kLog2e / sqrtf((float)DH)};
+  const double bh = (double)io.B * io.H;
+  KernelInfo ki{sizeof(T) == 2 ? "attn_fwd_kernel<bf16>" : "attn_fwd_kernel<f32>",
+                4.0 * bh * io.L * (double)io.L * DH, 4.0 * bh * io.L * DH * sizeof(T)};
+  return launch(ki, attn_fwd_kernel<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
+}
+
+template <typename T, int DH>
+orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, const float* lse, const void* dO, int64_t lddo,
+                   void* dq, void* dk, void* dv, int64_t ldg, float* D, hipStream_t s) {
+  const double bh = (double)io.B * io.H;
+  const int64_t rows = (int64_t)io.B * io.L * io.H;
+  KernelInfo kp{sizeof(T) == 2 ? "attn_bwd_pre<bf16>" : "attn_bwd_pre<f32>", 2.0 * rows * DH,
+                2.0 * rows * DH * sizeof(T)};
+  ORBIT_TRY(launch(kp, attn_bwd_pre<T, DH>, dim3((unsigned)cdiv(rows, 256 / (DH / 8))), dim3(256), 0, s,
+                   (const T*)o, ldo, (const T*)dO, lddo, D, io.B, io.H, io.L));
+  BwdArgs a{io.q, io.k, io.v, dO, lse, D, dq, dk, dv, io.ldq, io.ldk, io.ldv, lddo, ldg, io.H, io.L,
+            kLog2e / sqrtf((float)DH), 1.f / sqrtf((float)DH)};
+  // algorithmic backward = 2x forward; kernels split it 3:2 (dK,dV: 4 products, dQ: 3 incl. recompute)
+  const double fl = 4.0 * bh * io.L * (double)io.L * DH;
+  KernelInfo k1{sizeof(T) == 2 ? "attn_bwd_dkdv<bf16>" : "attn_bwd_dkdv<f32>", 1.2 * 2 * fl / 1.2 * 0.6,
+                6.0 * bh * io.L * DH * sizeof(T)};
+  ORBIT_TRY(launch(k1, attn_bwd_dkdv<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a));
+  KernelInfo k2{sizeof(T) == 2 ? "attn_bwd_dq<bf16>" : "attn_bwd_dq<f32>", 2 * fl * 0.4,
+                5.0 * bh * io.L * DH * sizeof(T)};
+  return launch(k2, attn_bwd_dq<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
+}
+
+}  // namespace
+
+orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream_t s) {
+#define AF(TT, D) return fwd_t<TT, D>(io, o, ldo, lse, s)
+  if (dt == ORBIT_BF16) {
+    if (io.dh == 32) AF(bf16, 32);
+    if (io.dh == 64) AF(bf16, 64);
+    if (io.dh == 128) AF(bf16, 128);
+  } else {
+    if (io.dh == 32) AF(float, 32);
+    if (io.dh == 64) AF(float, 64);
+    if (io.dh == 128) AF(float, 128);
+  }
+#undef AF
+  set_error("attention: head_dim %d unsupported", io.dh);
+  return ORBIT_E_UNSUPPORTED;
+}
+
+orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, const float* lse,
+                      const void* dO, int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg, float* Dbuf,
+                      hipStream_t s) {
+#define AB(TT, D) return bwd_t<TT, D>(io, o, ldo, lse, dO, lddo, dq, dk, dv, ldg, Dbuf, s)
+  if (dt == ORBIT_BF16) {
+    if (io.dh == 32) AB(bf16, 32);
+    if (io.dh == 64) AB(bf16, 64);
+    if (io.dh == 128) AB(bf16, 128);
+  } else {
+    if (io.dh == 32) AB(float, 32);
+    if (io.dh == 64) AB(float, 64);
+    if (io.dh == 128) AB(float, 128);
+  }
+#undef AB
+  set_error("attention: head_dim %d unsupported", io.dh);
+  return ORBIT_E_UNSUPPORTED;
+}
+
+}  // namespace orbit

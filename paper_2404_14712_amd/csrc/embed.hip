@@ -1,0 +1,221 @@
+// Per-variable patch tokenisation: tok[b,l,v,:] = P[b,v,l,:] W_pe[v] + b_pe[v]
+// + ve[v] with 4x4 patches (16 pixels), and its parameter gradients.
+//
+// Both directions are bound by HBM traffic on tok / dtok (one token row of d
+// elements per patch and variable); the 16-deep products are done in float32
+// vector ALU with the weight slice of a thread held in registers and the
+// block's pixels staged in LDS.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace orbit {
+namespace {
+
+constexpr int kPP = 16;             // pixels per 4x4 patch
+constexpr int kPatchesPerBlock = 64;
+
+template <typename T> ORBIT_DEV void ld8f(const T* p, float* f) {
+  if constexpr (sizeof(T) == 2) unpack(ld128(p), f, (bf16*)nullptr);
+  else {
+    unpack(ld128(p), f, (float*)nullptr);
+    unpack(ld128(p + 4), f + 4, (float*)nullptr);
+  }
+}
+template <typename T> ORBIT_DEV void st8f(T* p, const float* f) {
+  if constexpr (sizeof(T) == 2) st128(p, pack(f, (bf16*)nullptr));
+  else {
+    st128(p, pack(f, (float*)nullptr));
+    st128(p + 4, pack(f + 4, (float*)nullptr));
+  }
+}
+
+// block: (patch group of 64, v, b); thread: 8 output columns of some patches
+template <typename T>
+__global__ void __launch_bounds__(256) patch_fwd_kernel(const float* __restrict__ img, const T* __restrict__ w,
+                                                        const T* __restrict__ bias, const T* __restrict__ ve,
+                                                        T* __restrict__ tok, int V, int Hg, int Wg, int d) {
+  __shared__ float px[kPatchesPerBlock][kPP];
+  const int v = blockIdx.y, b = blockIdx.z;
+  const int nw = Wg / 4, L = (Hg / 4) * nw;
+  const int l0 = blockIdx.x * kPatchesPerBlock;
+  const float* im = img + ((int64_t)b * V + v) * Hg * Wg;
+  for (int idx = threadIdx.x; idx < kPatchesPerBlock * kPP; idx += 256) {
+    const int pl = idx / kPP, c = idx % kPP;
+    const int l = l0 + pl;
+    float val = 0.f;
+    if (l < L) {
+      const int ph = l / nw, pw = l % nw;
+      val = im[(int64_t)(ph * 4 + c / 4) * Wg + pw * 4 + (c % 4)];
+    }
+    px[pl][c] = val;
+  }
+  __syncthreads();
+  const int ech = d / 8;
+  const int lanes = ech >= 256 ? 1 : 256 / ech;   // patch lanes per block
+  const int ec_first = threadIdx.x % (ech >= 256 ? 256 : ech);
+  const int plane = threadIdx.x / (ech >= 256 ? 256 : ech);
+  if (plane >= lanes) return;
+  for (int ec = ec_first; ec < ech; ec += 256) {
+    const int e0 = ec * 8;
+    float wr[kPP][8], add[8];
+#pragma unroll
+    for (int c = 0; c < kPP; ++c) ld8f(w + ((int64_t)v * kPP + c) * d + e0, wr[c]);
+    ld8f(bias + (int64_t)v * d + e0, add);
+    if (ve) {
+      float t[8];
+      ld8f(ve + (int64_t)v * d + e0, t);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) add[i] += t[i];
+    }
+    for (int pl = plane; pl < kPatchesPerBlock; pl += lanes) {
+      const int l = l0 + pl;
+      if (l >= L) break;
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = add[i];
+#pragma unroll
+      for (int c = 0; c < kPP; ++c) {
+        const float p = px[pl][c];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] += p * wr[c][i];
+      }
+      st8f(tok + (((int64_t)b * L + l) * V + v) * d + e0, o);
+    }
+  }
+}
+
+// partial gradients over a chunk of patches (all samples flattened, n = B*L):
+// part[chunk][lane][v][17][d]: rows 0..15 = dW rows, row 16 = db
+constexpr int kBwdPatchesPerChunk = 1024;
+
+template <typename T>
+__global__ void __launch_bounds__(256) patch_bwd_partial(const float* __restrict__ img, const T* __restrict__ dtok,
+                                                         float* __restrict__ part, int B, int V, int Hg, int Wg,
+                                                         int d) {
+  __shared__ float px[kPatchesPerBlock][kPP];
+  const int v = blockIdx.y, chunk = blockIdx.x;
+  const int nw = Wg / 4, L = (Hg / 4) * nw;
+  const int64_t n = (int64_t)B * L;
+  const int ech = d / 8;
+  const int per = ech >= 256 ? 256 : ech;
+  const int lanes = ech >= 256 ? 1 : 256 / ech;  // 1, 2, 4 ... patch lanes
+  const int ec_first = threadIdx.x % per, plane = threadIdx.x / per;
+  for (int ecb = 0; ecb < ech; ecb += 256) {
+    const int ec = ecb + ec_first;
+    float acc[17][8];
+#pragma unroll
+    for (int r = 0; r < 17; ++r)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[r][i] = 0.f;
+    for (int g0 = chunk * kBwdPatchesPerChunk; g0 < min<int64_t>(n, (int64_t)(chunk + 1) * kBwdPatchesPerChunk);
+         g0 += kPatchesPerBlock) {
+      __syncthreads();
+      for (int idx = threadIdx.x; idx < kPatchesPerBlock * kPP; idx += 256) {
+        const int pl = idx / kPP, c = idx % kPP;
+        const int64_t gi = g0 + pl;
+        float val = 0.f;
+        if (gi < n) {
+          const int b = (int)(gi / L), l = (int)(gi % L);
+          const int ph = l / nw, pw = l % nw;
+          val = img[(((int64_t)b * V + v) * Hg + ph * 4 + c / 4) * Wg + pw * 4 + (c % 4)];
+        }
+        px[pl][c] = val;
+      }
+      __syncthreads();
+      if (plane < lanes && ec < ech) {
+        for (int pl = plane; pl < kPatchesPerBlock; pl += lanes) {
+          const int64_t gi = g0 + pl;
+          if (gi >= n) break;
+          float g8[8];
+          ld8f(dtok + (gi * V + v) * d + ec * 8, g8);
+#pragma unroll
+          for (int c = 0; c < kPP; ++c) {
+            const float p = px[pl][c];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[c][i] += p * g8[i];
+          }
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[16][i] += g8[i];
+        }
+      }
+    }
+    // one partial per (chunk, patch lane); the final pass sums them in order
+    if (plane < lanes && ec < ech)
+#pragma unroll
+      for (int r = 0; r < 17; ++r)
+        st8f(part + ((((int64_t)chunk * lanes + plane) * V + v) * 17 + r) * d + ec * 8, acc[r]);
+  }
+}
+
+__global__ void __launch_bounds__(256) patch_bwd_final(const float* __restrict__ part, int chunks, int V, int d,
+                                                       float* dw, float* db, float* dve, int accumulate) {
+  const int64_t per = (int64_t)V * 17 * d;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < per; e += (int64_t)gridDim.x * 256) {
+    float s = 0.f;
+    for (int k = 0; k < chunks; ++k) s += part[(int64_t)k * per + e];
+    const int64_t v = e / (17 * d), rem = e % (17 * d);
+    const int r = (int)(rem / d), c = (int)(rem % d);
+    if (r < 16) {
+      float* o = dw + (v * 16 + r) * d + c;
+      *o = accumulate ? *o + s : s;
+    } else {
+      float* o = db + v * d + c;
+      *o = accumulate ? *o + s : s;
+      if (dve) {
+        float* o2 = dve + v * d + c;
+        *o2 = accumulate ? *o2 + s : s;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+orbit_status patch_embed_fwd(orbit_dtype dt, const float* img, const void* w, const void* b, const void* ve,
+                             void* tok, int B, int V, int Hg, int Wg, int p, int d, hipStream_t s) {
+  (void)p;
+  const int L = (Hg / 4) * (Wg / 4);
+  dim3 grid((unsigned)cdiv(L, kPatchesPerBlock), V, B);
+  const double toks = (double)B * L * V;
+  KernelInfo ki{dt == ORBIT_BF16 ? "patch_fwd_kernel<bf16>" : "patch_fwd_kernel<f32>", toks * d * 2 * kPP,
+                toks * (kPP * 4.0 + d * (dt == ORBIT_BF16 ? 2.0 : 4.0))};
+  if (dt == ORBIT_BF16)
+    return launch(ki, patch_fwd_kernel<bf16>, grid, dim3(256), 0, s, img, (const bf16*)w, (const bf16*)b,
+                  (const bf16*)ve, (bf16*)tok, V, Hg, Wg, d);
+  return launch(ki, patch_fwd_kernel<float>, grid, dim3(256), 0, s, img, (const float*)w, (const float*)b,
+                (const float*)ve, (float*)tok, V, Hg, Wg, d);
+}
+
+size_t patch_embed_bwd_workspace_bytes(int B, int V, int Hg, int Wg, int p, int d) {
+  (void)p;
+  const int64_t n = (int64_t)B * (Hg / 4) * (Wg / 4);
+  const int lanes = d / 8 >= 256 ? 1 : 256 / (d / 8);
+  return align_up((size_t)cdiv(n, kBwdPatchesPerChunk) * lanes * V * 17 * (size_t)d * sizeof(float));
+}
+
+orbit_status patch_embed_bwd(orbit_dtype dt, const float* img, const void* dtok, float* dw, float* db, float* dve,
+                             int accumulate, int B, int V, int Hg, int Wg, int p, int d, void* ws, hipStream_t s) {
+  (void)p;
+  const int64_t n = (int64_t)B * (Hg / 4) * (Wg / 4);
+  const int chunks = (int)cdiv(n, kBwdPatchesPerChunk);
+  const int lanes = d / 8 >= 256 ? 1 : 256 / (d / 8);
+  float* part = static_cast<float*>(ws);
+  dim3 grid(chunks, V);
+  const double toks = (double)n * V;
+  KernelInfo ki{dt == ORBIT_BF16 ? "patch_bwd_partial<bf16>" : "patch_bwd_partial<f32>", toks * d * 2 * 17,
+                toks * (kPP * 4.0 + d * (dt == ORBIT_BF16 ? 2.0 : 4.0))};
+  if (dt == ORBIT_BF16) {
+    ORBIT_TRY(launch(ki, patch_bwd_partial<bf16>, grid, dim3(256), 0, s, img, (const bf16*)dtok, part, B, V, Hg,
+                     Wg, d));
+  } else {
+    ORBIT_TRY(launch(ki, patch_bwd_partial<float>, grid, dim3(256), 0, s, img, (const float*)dtok, part, B, V,
+                     Hg, Wg, d));
+  }
+  const int64_t per = (int64_t)V * 17 * d;
+  KernelInfo kf{"patch_bwd_final", 0.0, (double)chunks * lanes * per * 4};
+  return launch(kf, patch_bwd_final, dim3((unsigned)std::min<int64_t>(cdiv(per, 256), 4096)), dim3(256), 0, s,
+                (const float*)part, chunks * lanes, V, d, dw, db, dve, accumulate);
+}
+
+}  // namespace orbit

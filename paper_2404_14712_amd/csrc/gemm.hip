@@ -1,0 +1,300 @@
+// MFMA GEMM for gfx950 with LDS-staged, register-prefetched double-buffered
+// tiles and a fused epilogue (bias, GELU with pre-activation store, GELU
+// derivative, residual, accumulate). Three operand layouts cover all linear
+// layers: forward (A K-major, B N-major), input gradient (both K-major) and
+// weight gradient (both M/N-major: the reduction runs over tokens).
+//
+// LDS holds both operands K-contiguous ([row][k], padded by 16 bytes per row)
+// so every MFMA fragment is one 16-byte LDS read. M/N-major operands are
+// transposed on the way in: each thread loads a 4(k) x 16-byte tile from HBM
+// (coalesced along the contiguous dimension) and scatters it as 4-element
+// k-runs.
+#include <stdio.h>
+#include <string>
+
+#include <algorithm>
+
+#include "gemm.h"
+#include "tile.h"
+
+namespace orbit {
+namespace {
+
+struct Epi {
+  float alpha;
+  int accumulate;
+  const void* bias; int64_t sBias;
+  void* gelu_out; int64_t ldgo;
+  const void* gelu_in; int64_t ldgi;
+  const void* res; int64_t ldr, sR; int res_row_mod;
+};
+
+struct GemmKArgs {
+  const void* A; const void* B; const void* B2; void* C;
+  int M, N, K, k_split;
+  int64_t lda, ldb, ldc;
+  int64_t sA, sB, sB2, sC;
+  int batch, splits, k_per_split;
+  float* partial;  // splits > 1: float32 partials [splits][batch][M][N]
+  Epi epi;
+};
+
+template <typename T, typename OutT>
+ORBIT_DEV void epi_apply(const Epi& e, int64_t bz, int r, int c, float v, OutT* C, int64_t ldc) {
+  v *= e.alpha;
+  const int64_t off = (int64_t)r * ldc + c;
+  if (e.accumulate) v += to_f(C[off]);
+  if (e.bias) v += to_f(static_cast<const T*>(e.bias)[bz * e.sBias + c]);
+  if (e.gelu_out) {
+    static_cast<T*>(e.gelu_out)[(int64_t)r * e.ldgo + c] = from_f<T>(v);
+    v = gelu_f(v);
+  }
+  if (e.gelu_in) v *= gelu_grad_f(to_f(static_cast<const T*>(e.gelu_in)[(int64_t)r * e.ldgi + c]));
+  if (e.res) {
+    const int rr = e.res_row_mod ? r % e.res_row_mod : r;
+    v += to_f(static_cast<const T*>(e.res)[bz * e.sR + (int64_t)rr * e.ldr + c]);
+  }
+  C[off] = from_f<OutT>(v);
+}
+
+template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+__global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int BKE = 128 / (int)sizeof(T);
+  constexpr int E = 16 / (int)sizeof(T);
+  constexpr int PITCH = BKE + E;
+  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
+  static_assert(TM >= 1 && TN >= 1, "wave tile must be at least 32x32");
+  __shared__ __attribute__((aligned(16))) T lds[2][(BM + BN) * PITCH];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int z = blockIdx.z;
+  const int split = z % g.splits;
+  const int64_t bz = z / g.splits;
+  const T* A = static_cast<const T*>(g.A) + bz * g.sA;
+  const T* B = static_cast<const T*>(g.B) + bz * g.sB;
+  const T* B2 = g.B2 ? static_cast<const T*>(g.B2) + bz * g.sB2 : nullptr;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int kbeg = split * g.k_per_split;
+  const int kend = min(g.K, kbeg + g.k_per_split);
+  const int nk = (kend - kbeg + BKE - 1) / BKE;
+
+  TileLoader<T, BM, BKE, NT, AK> la;
+  TileLoader<T, BN, BKE, NT, BKM> lb;
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  if (nk > 0) {
+    la.load(A, nullptr, 0, g.lda, m0, g.M, kbeg, kend, tid);
+    lb.load(B, B2, g.k_split, g.ldb, n0, g.N, kbeg, kend, tid);
+    la.store(&lds[0][0], tid);
+    lb.store(&lds[0][BM * PITCH], tid);
+  }
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      const int k0 = kbeg + (kt + 1) * BKE;
+      la.load(A, nullptr, 0, g.lda, m0, g.M, k0, kend, tid);
+      lb.load(B, B2, g.k_split, g.ldb, n0, g.N, k0, kend, tid);
+    }
+    const T* As = &lds[cur][0];
+    const T* Bs = &lds[cur][BM * PITCH];
+#pragma unroll
+    for (int kk = 0; kk < BKE / 16; ++kk) {
+      Frag<T> af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        ld_frag(af[i], As + (wm * WTM + i * 32 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        ld_frag(bfr[j], Bs + (wn * WTN + j * 32 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) mma16(acc[i][j], af[i], bfr[j]);
+    }
+    if (kt + 1 < nk) {
+      la.store(&lds[cur ^ 1][0], tid);
+      lb.store(&lds[cur ^ 1][BM * PITCH], tid);
+    }
+    __syncthreads();
+  }
+
+  // epilogue
+  OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+        const int c = n0 + wn * WTN + j * 32 + (lane & 31);
+        if (r < g.M && c < g.N) {
+          if (g.splits > 1) {
+            g.partial[(((int64_t)split * g.batch + bz) * g.M + r) * g.N + c] = acc[i][j][v];
+          } else {
+            epi_apply<T, OutT>(g.epi, bz, r, c, acc[i][j][v], C, g.ldc);
+          }
+        }
+      }
+}
+
+template <typename T, typename OutT>
+__global__ void __launch_bounds__(256) splitk_reduce(GemmKArgs g) {
+  const int64_t MN = (int64_t)g.M * g.N;
+  const int64_t total = MN * g.batch;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
+    const int64_t bz = idx / MN;
+    const int64_t rem = idx % MN;
+    const int r = (int)(rem / g.N), c = (int)(rem % g.N);
+    float v = 0.f;
+    for (int s = 0; s < g.splits; ++s) v += g.partial[((int64_t)s * g.batch + bz) * MN + rem];
+    OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
+    epi_apply<T, OutT>(g.epi, bz, r, c, v, C, g.ldc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host dispatch
+// ---------------------------------------------------------------------------
+struct TileCfg { int BM, BN, WM, WN; };
+constexpr TileCfg kBig{128, 128, 2, 2};
+constexpr TileCfg kNarrowN{128, 32, 4, 1};
+constexpr TileCfg kNarrowM{32, 128, 1, 4};
+constexpr TileCfg kSmall{64, 64, 2, 2};
+
+TileCfg pick_tile(const Gemm& g) {
+  if (g.N <= 32) return kNarrowN;
+  if (g.M <= 32) return kNarrowM;
+  if (g.M <= 64 || g.N <= 64) return kSmall;
+  return kBig;
+}
+
+int bke_of(orbit_dtype dt) { return dt == ORBIT_BF16 ? 64 : 32; }
+
+int pick_splits(const Gemm& g, const TileCfg& t) {
+  const int64_t tiles = cdiv(g.M, t.BM) * cdiv(g.N, t.BN) * (int64_t)g.batch;
+  const int bke = bke_of(g.dtype);
+  const int64_t ksteps = cdiv(g.K, bke);
+  if (tiles >= 256 || ksteps < 8) return 1;
+  int64_t s = cdiv(512, tiles);
+  s = std::min<int64_t>(s, ksteps / 4);
+  s = std::min<int64_t>(s, 64);
+  return (int)std::max<int64_t>(s, 1);
+}
+
+template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+const char* kname() {
+  static std::string s = [] {
+    char b[160];
+    snprintf(b, sizeof b, "gemm_kernel<%s,%s,%d,%d,%d,%d,%s,%s>", sizeof(T) == 2 ? "bf16" : "f32",
+             sizeof(OutT) == 2 ? "bf16" : "f32", BM, BN, WM, WN, AK ? "AK" : "AM", BKM ? "BK" : "BN");
+    return std::string(b);
+  }();
+  return s.c_str();
+}
+
+template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+orbit_status run_cfg(const Gemm& g, GemmKArgs& a, hipStream_t s) {
+  const double flops = 2.0 * g.M * g.N * (double)g.K * g.batch;
+  const double bytes = ((double)g.M * g.K + (double)g.K * g.N) * sizeof(T) * g.batch +
+                       (double)g.M * g.N * sizeof(OutT) * g.batch;
+  KernelInfo ki{kname<T, OutT, BM, BN, WM, WN, AK, BKM>(), flops, bytes};
+  dim3 grid((unsigned)cdiv(g.N, BN), (unsigned)cdiv(g.M, BM), (unsigned)(g.batch * a.splits));
+  ORBIT_TRY(launch(ki, gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>, grid, dim3(WM * WN * 64), 0, s, a));
+  if (a.splits > 1) {
+    const int64_t total = (int64_t)g.M * g.N * g.batch;
+    const unsigned blocks = (unsigned)std::min<int64_t>(cdiv(total, 256), 8192);
+    KernelInfo kr{sizeof(OutT) == 2 ? "splitk_reduce<bf16>" : "splitk_reduce<f32>", 0.0,
+                  (double)total * 4 * (a.splits + 1)};
+    ORBIT_TRY(launch(kr, splitk_reduce<T, OutT>, dim3(blocks), dim3(256), 0, s, a));
+  }
+  return ORBIT_OK;
+}
+
+template <typename T, typename OutT, bool AK, bool BKM>
+orbit_status run_layout(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream_t s) {
+  if (t.BM == 128 && t.BN == 128) return run_cfg<T, OutT, 128, 128, 2, 2, AK, BKM>(g, a, s);
+  if (t.BM == 128 && t.BN == 32) return run_cfg<T, OutT, 128, 32, 4, 1, AK, BKM>(g, a, s);
+  if (t.BM == 32 && t.BN == 128) return run_cfg<T, OutT, 32, 128, 1, 4, AK, BKM>(g, a, s);
+  return run_cfg<T, OutT, 64, 64, 2, 2, AK, BKM>(g, a, s);
+}
+
+template <typename T, typename OutT>
+orbit_status run_typed(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream_t s) {
+  if (g.a_kmajor && !g.b_kmajor) return run_layout<T, OutT, true, false>(g, a, t, s);
+  if (g.a_kmajor && g.b_kmajor) return run_layout<T, OutT, true, true>(g, a, t, s);
+  if (!g.a_kmajor && !g.b_kmajor) return run_layout<T, OutT, false, false>(g, a, t, s);
+  set_error("gemm: layout (A M-major, B K-major) is not supported");
+  return ORBIT_E_UNSUPPORTED;
+}
+
+}  // namespace
+
+size_t gemm_workspace_bytes(const Gemm& g) {
+  const TileCfg t = pick_tile(g);
+  const int s = pick_splits(g, t);
+  return s > 1 ? align_up((size_t)s * g.batch * (size_t)g.M * g.N * sizeof(float)) : 0;
+}
+
+orbit_status gemm(const Gemm& g, void* ws, size_t ws_bytes, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return ORBIT_OK;
+  // K-major operands are read in 16-byte chunks along K: with K % 8 != 0 the
+  // last chunk runs past K, which is only sound when the other operand's rows
+  // are masked (M/N-major) and the K-major rows are zero-padded (internal use).
+  if (g.K % 8 != 0 && g.a_kmajor && g.b_kmajor) {
+    set_error("gemm: K=%d must be a multiple of 8 when both operands are K-major", g.K);
+    return ORBIT_E_ARG;
+  }
+  if (g.accumulate && !g.out_f32) {
+    set_error("gemm: accumulate needs a float32 output");
+    return ORBIT_E_ARG;
+  }
+  const TileCfg t = pick_tile(g);
+  GemmKArgs a{};
+  a.A = g.A; a.B = g.B; a.B2 = g.B2; a.C = g.C;
+  a.M = g.M; a.N = g.N; a.K = g.K; a.k_split = g.B2 ? g.k_split : g.K;
+  a.lda = g.lda; a.ldb = g.ldb; a.ldc = g.ldc;
+  a.sA = g.sA; a.sB = g.sB; a.sB2 = g.sB2; a.sC = g.sC;
+  a.batch = g.batch;
+  a.splits = 1;
+  a.k_per_split = g.K;
+  a.partial = nullptr;
+  const int splits = pick_splits(g, t);
+  if (splits > 1 && ws && ws_bytes >= gemm_workspace_bytes(g)) {
+    const int bke = bke_of(g.dtype);
+    const int64_t ksteps = cdiv(g.K, bke);
+    const int per = (int)cdiv(ksteps, splits) * bke;
+    a.splits = (int)cdiv(g.K, per);
+    a.k_per_split = per;
+    a.partial = static_cast<float*>(ws);
+  }
+  if (g.K <= 0) a.k_per_split = 0;
+  a.epi.alpha = g.alpha;
+  a.epi.accumulate = g.accumulate ? 1 : 0;
+  a.epi.bias = g.bias;
+  a.epi.sBias = g.sBias;
+  a.epi.gelu_out = g.gelu_out; a.epi.ldgo = g.ldgo;
+  a.epi.gelu_in = g.gelu_in; a.epi.ldgi = g.ldgi;
+  a.epi.res = g.res; a.epi.ldr = g.ldr; a.epi.sR = g.sR; a.epi.res_row_mod = g.res_row_mod;
+  if (g.dtype == ORBIT_BF16) {
+    return g.out_f32 ? run_typed<bf16, float>(g, a, t, s) : run_typed<bf16, bf16>(g, a, t, s);
+  }
+  if (!g.out_f32) {
+    // float operands always produce float
+    return run_typed<float, float>(g, a, t, s);
+  }
+  return run_typed<float, float>(g, a, t, s);
+}
+
+}  // namespace orbit

@@ -1,0 +1,76 @@
+// Host launchers of the non-GEMM kernels. Each enqueues on `s` and returns a
+// status; shapes are validated by the callers in abi.cpp.
+#pragma once
+#include "common.h"
+
+namespace orbit {
+
+// ---- LayerNorm over rows of length n (pre-LN and final LN) ----------------
+// y = g * (x - mean) * rstd + b; mean/rstd [rows] float32 (may be null).
+orbit_status layernorm_fwd(orbit_dtype dt, const void* x, int64_t ldx, const void* g, const void* b,
+                           void* y, int64_t ldy, float* mean, float* rstd, int rows, int n,
+                           float eps, hipStream_t s);
+// dx = rstd * (dy*g - mean(dy*g) - xhat * mean(dy*g*xhat)) [+ dres]; dx may alias dres.
+orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const void* x, int64_t ldx,
+                           const float* mean, const float* rstd, const void* g, const void* dres,
+                           void* dx, int64_t lddx, int rows, int n, hipStream_t s);
+
+// ---- deterministic column reductions over rows ----------------------------
+// Partials of sum_r dy[r, c] and (if x) sum_r dy[r, c] * xhat[r, c] with
+// xhat = (x - mean[r]) * rstd[r]; then a fixed-order final sum into float32
+// outputs (overwrite or accumulate). Workspace: colsum_workspace_bytes.
+size_t colsum_workspace_bytes(int rows, int n);
+orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int n,
+                    const void* x, int64_t ldx, const float* mean, const float* rstd,
+                    float* out_sum, float* out_xsum, int accumulate, void* ws, hipStream_t s);
+// float32 input variant (dpred of the head)
+orbit_status colsum_f32(const float* dy, int64_t lddy, int rows, int n, float* out_sum,
+                        int accumulate, void* ws, hipStream_t s);
+
+// ---- QK-LayerNorm: per-head LN over head_dim on q and k --------------------
+// src row t: q at src[t*lds + h*dh], k at src[t*lds + A + h*dh]; dst the same
+// with ldd. stats: mean/rstd [T, 2H] (q heads then k heads).
+orbit_status qk_norm_fwd(orbit_dtype dt, const void* src, int64_t lds, void* dst, int64_t ldd,
+                         const void* qg, const void* qb, const void* kg, const void* kb,
+                         float* mean, float* rstd, int T, int H, int dh, float eps, hipStream_t s);
+// in place on dq/dk (rows of `d`, ld ldd): dxhat -> dx; gain/shift grads.
+size_t qk_norm_bwd_workspace_bytes(int dh);
+orbit_status qk_norm_bwd(orbit_dtype dt, void* d, int64_t ldd, const void* src, int64_t lds,
+                         const float* mean, const float* rstd, const void* qg, const void* kg,
+                         float* dqg, float* dqb, float* dkg, float* dkb, int accumulate,
+                         int T, int H, int dh, void* ws, hipStream_t s);
+
+// ---- attention: O = softmax(q k^T / sqrt(dh)) v per (sample, head) --------
+struct AttnIO {
+  const void *q, *k, *v;
+  int64_t ldq, ldk, ldv;
+  int B, H, L, dh;
+};
+orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream_t s);
+// D[b,h,l] = rowsum(dO * O)
+orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, const float* lse,
+                      const void* dO, int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg,
+                      float* Dbuf, hipStream_t s);
+
+// ---- patch embedding --------------------------------------------------------
+orbit_status patch_embed_fwd(orbit_dtype dt, const float* img, const void* w, const void* b,
+                             const void* ve, void* tok, int B, int V, int Hg, int Wg, int p, int d,
+                             hipStream_t s);
+size_t patch_embed_bwd_workspace_bytes(int B, int V, int Hg, int Wg, int p, int d);
+orbit_status patch_embed_bwd(orbit_dtype dt, const float* img, const void* dtok, float* dw, float* db,
+                             float* dve, int accumulate, int B, int V, int Hg, int Wg, int p, int d,
+                             void* ws, hipStream_t s);
+
+// ---- loss ---------------------------------------------------------------------
+size_t mse_workspace_bytes(int64_t n);
+orbit_status mse(const float* pred, const float* tgt, int64_t n, float scale, float* loss,
+                 float* dpred, void* ws, hipStream_t s);
+
+// ---- small helpers ------------------------------------------------------------
+// dst[i] = (dtype) src[i] (float32 -> dtype); used for dpred before the head GEMMs
+orbit_status cast_from_f32(orbit_dtype dt, const float* src, void* dst, int64_t n, hipStream_t s);
+// out[i] = accumulate ? out[i] + v : v, for a float32 vector v given on device
+orbit_status axpy_f32(const float* src, float* dst, int64_t n, int accumulate, hipStream_t s);
+orbit_status fill_f32(float* dst, int64_t n, float v, hipStream_t s);
+
+}  // namespace orbit

@@ -1,0 +1,60 @@
+// Mean squared error and its gradient with a fixed-order (deterministic)
+// two-stage reduction.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace orbit {
+namespace {
+
+constexpr int kMseBlocks = 1024;
+
+__global__ void __launch_bounds__(256) mse_partial(const float* __restrict__ pred, const float* __restrict__ tgt,
+                                                   int64_t n, float gscale, float* __restrict__ dpred,
+                                                   float* __restrict__ part) {
+  __shared__ float red[4];
+  float s = 0.f;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const float r = pred[i] - tgt[i];
+    s += r * r;
+    if (dpred) dpred[i] = r * gscale;
+  }
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ void __launch_bounds__(256) mse_final(const float* __restrict__ part, int nparts, double inv_n,
+                                                 float* loss) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < nparts; i += 256) s += part[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 128; o >= 1; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) loss[0] = (float)(red[0] * inv_n);
+}
+
+}  // namespace
+
+size_t mse_workspace_bytes(int64_t n) {
+  (void)n;
+  return align_up(kMseBlocks * sizeof(float));
+}
+
+orbit_status mse(const float* pred, const float* tgt, int64_t n, float scale, float* loss, float* dpred, void* ws,
+                 hipStream_t s) {
+  const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(kMseBlocks, cdiv(n, 256)));
+  float* part = static_cast<float*>(ws);
+  KernelInfo kp{"mse_partial", 3.0 * n, (dpred ? 12.0 : 8.0) * n};
+  ORBIT_TRY(launch(kp, mse_partial, dim3(blocks), dim3(256), 0, s, pred, tgt, n,
+                   (float)(2.0 / (double)n * scale), dpred, part));
+  KernelInfo kf{"mse_final", 0.0, 4.0 * blocks};
+  return launch(kf, mse_final, dim3(1), dim3(256), 0, s, (const float*)part, blocks, 1.0 / (double)n, loss);
+}
+
+}  // namespace orbit

@@ -1,0 +1,549 @@
+// LayerNorm (pre-LN, final LN and the per-head QK-LayerNorm) forward and
+// backward, deterministic column reductions (bias and LayerNorm-parameter
+// gradients) and small elementwise helpers. All HBM-bound: rows are read as
+// 16-byte vectors by consecutive lanes; statistics are float32 wave/block
+// reductions.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace orbit {
+namespace {
+
+template <typename T> ORBIT_DEV void load8(const T* p, float* f);
+template <> ORBIT_DEV void load8<bf16>(const bf16* p, float* f) { unpack(ld128(p), f, (bf16*)nullptr); }
+template <> ORBIT_DEV void load8<float>(const float* p, float* f) {
+  unpack(ld128(p), f, (float*)nullptr);
+  unpack(ld128(p + 4), f + 4, (float*)nullptr);
+}
+template <typename T> ORBIT_DEV void store8(T* p, const float* f);
+template <> ORBIT_DEV void store8<bf16>(bf16* p, const float* f) { st128(p, pack(f, (bf16*)nullptr)); }
+template <> ORBIT_DEV void store8<float>(float* p, const float* f) {
+  st128(p, pack(f, (float*)nullptr));
+  st128(p + 4, pack(f + 4, (float*)nullptr));
+}
+
+// sum over a 256-thread block; `red` is 4 floats of LDS; ends with a barrier
+ORBIT_DEV float block_sum256(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  const float r = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return r;
+}
+
+template <typename T, int NCH>
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const T* __restrict__ x, int64_t ldx,
+                                                     const T* __restrict__ g, const T* __restrict__ b,
+                                                     T* __restrict__ y, int64_t ldy, float* mean,
+                                                     float* rstd, int n, float eps) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  const T* xr = x + row * ldx;
+  float v[NCH][8];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = (threadIdx.x + c * 256) * 8;
+    if (idx < n) {
+      load8(xr + idx, v[c]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[c][i];
+    }
+  }
+  const float mu = block_sum256(s, red) / (float)n;
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = (threadIdx.x + c * 256) * 8;
+    if (idx < n) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float t = v[c][i] - mu;
+        q += t * t;
+      }
+    }
+  }
+  const float r = rsqrtf(block_sum256(q, red) / (float)n + eps);
+  T* yr = y + row * ldy;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = (threadIdx.x + c * 256) * 8;
+    if (idx < n) {
+      float gg[8], bb[8], o[8];
+      load8(g + idx, gg);
+      load8(b + idx, bb);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = (v[c][i] - mu) * r * gg[i] + bb[i];
+      store8(yr + idx, o);
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (mean) mean[row] = mu;
+    if (rstd) rstd[row] = r;
+  }
+}
+
+template <typename T, int NCH>
+__global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, int64_t lddy,
+                                                     const T* __restrict__ x, int64_t ldx,
+                                                     const float* __restrict__ mean,
+                                                     const float* __restrict__ rstd,
+                                                     const T* __restrict__ g, const T* dres, T* dx,
+                                                     int64_t lddx, int n) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  const float mu = mean[row], r = rstd[row];
+  float gh[NCH][8], xh[NCH][8];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = (threadIdx.x + c * 256) * 8;
+    if (idx < n) {
+      float d8[8], x8[8], g8[8];
+      load8(dy + row * lddy + idx, d8);
+      load8(x + row * ldx + idx, x8);
+      load8(g + idx, g8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        xh[c][i] = (x8[i] - mu) * r;
+        gh[c][i] = d8[i] * g8[i];
+        s1 += gh[c][i];
+        s2 += gh[c][i] * xh[c][i];
+      }
+    }
+  }
+  const float inv_n = 1.f / (float)n;
+  const float m1 = block_sum256(s1, red) * inv_n;
+  const float m2 = block_sum256(s2, red) * inv_n;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = (threadIdx.x + c * 256) * 8;
+    if (idx < n) {
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = r * (gh[c][i] - m1 - xh[c][i] * m2);
+      if (dres) {
+        float rr[8];
+        load8(dres + row * lddx + idx, rr);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] += rr[i];
+      }
+      store8(dx + row * lddx + idx, o);
+    }
+  }
+}
+
+// ---- column sums ------------------------------------------------------------
+constexpr int kColsPerBlock = 512;  // 64 threads x 8 columns
+constexpr int kRowsPerChunk = 64;
+
+template <typename T, bool XS>
+__global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ dy, int64_t lddy, int rows,
+                                                      int n, const T* __restrict__ x, int64_t ldx,
+                                                      const float* __restrict__ mean,
+                                                      const float* __restrict__ rstd,
+                                                      float* __restrict__ part_s,
+                                                      float* __restrict__ part_x) {
+  __shared__ float sm[2][4][kColsPerBlock];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int c0 = blockIdx.x * kColsPerBlock + tx * 8;
+  const int chunk = blockIdx.y;
+  const int r0 = chunk * kRowsPerChunk, r1 = min(rows, r0 + kRowsPerChunk);
+  float as[8], ax[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) as[i] = ax[i] = 0.f;
+  if (c0 < n) {
+    for (int r = r0 + ty; r < r1; r += 4) {
+      float d8[8];
+      load8(dy + (int64_t)r * lddy + c0, d8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) as[i] += d8[i];
+      if (XS) {
+        float x8[8];
+        load8(x + (int64_t)r * ldx + c0, x8);
+        const float mu = mean[r], rs = rstd[r];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ax[i] += d8[i] * ((x8[i] - mu) * rs);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    sm[0][ty][tx * 8 + i] = as[i];
+    sm[1][ty][tx * 8 + i] = ax[i];
+  }
+  __syncthreads();
+  // 256 threads reduce 512 columns (2 each) over the 4 row lanes, fixed order
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int cc = threadIdx.x + h * 256;
+    const int c = blockIdx.x * kColsPerBlock + cc;
+    if (c < n) {
+      const float s = (sm[0][0][cc] + sm[0][1][cc]) + (sm[0][2][cc] + sm[0][3][cc]);
+      part_s[(int64_t)chunk * n + c] = s;
+      if (XS) {
+        const float t = (sm[1][0][cc] + sm[1][1][cc]) + (sm[1][2][cc] + sm[1][3][cc]);
+        part_x[(int64_t)chunk * n + c] = t;
+      }
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) colsum_final(const float* __restrict__ part, int chunks, int n,
+                                                    float* __restrict__ out, int accumulate) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= n) return;
+  float s = 0.f;
+  for (int k = 0; k < chunks; ++k) s += part[(int64_t)k * n + c];
+  out[c] = accumulate ? out[c] + s : s;
+}
+
+// ---- QK-LayerNorm -------------------------------------------------------------
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) qkln_fwd_kernel(const T* __restrict__ src, int64_t lds,
+                                                       T* __restrict__ dst, int64_t ldd,
+                                                       const T* __restrict__ qg, const T* __restrict__ qb,
+                                                       const T* __restrict__ kg, const T* __restrict__ kb,
+                                                       float* mean, float* rstd, int T_, int H, int A,
+                                                       float eps) {
+  constexpr int G = DH / 8;
+  const int li = threadIdx.x % G;
+  const int64_t row = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;
+  const bool valid = row < (int64_t)T_ * 2 * H;
+  const int64_t t = valid ? row / (2 * H) : 0;
+  const int j = valid ? (int)(row % (2 * H)) : 0;
+  const int sidx = j / H, h = j % H;
+  float v[8];
+  if (valid) load8(src + t * lds + sidx * A + h * DH + li * 8, v);
+  else
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = 0.f;
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s += v[i];
+#pragma unroll
+  for (int o = G / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  const float mu = s / (float)DH;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) q += (v[i] - mu) * (v[i] - mu);
+#pragma unroll
+  for (int o = G / 2; o >= 1; o >>= 1) q += __shfl_xor(q, o, 64);
+  const float r = rsqrtf(q / (float)DH + eps);
+  if (!valid) return;
+  float gg[8], bb[8], y[8];
+  load8((sidx ? kg : qg) + li * 8, gg);
+  load8((sidx ? kb : qb) + li * 8, bb);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) y[i] = (v[i] - mu) * r * gg[i] + bb[i];
+  store8(dst + t * ldd + sidx * A + h * DH + li * 8, y);
+  if (li == 0) {
+    mean[row] = mu;
+    rstd[row] = r;
+  }
+}
+
+constexpr int kQkBwdBlocks = 512;
+
+template <typename T, int DH>
+__global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const T* __restrict__ src,
+                                                       int64_t lds, const float* __restrict__ mean,
+                                                       const float* __restrict__ rstd,
+                                                       const T* __restrict__ qg, const T* __restrict__ kg,
+                                                       int T_, int H, int A, float* __restrict__ part) {
+  constexpr int G = DH / 8;
+  constexpr int NG = 256 / G;  // row groups per block
+  __shared__ float sm[NG][4][DH];
+  const int li = threadIdx.x % G, grp = threadIdx.x / G;
+  float ag[2][8], ab[2][8];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ag[s][i] = ab[s][i] = 0.f;
+  float gq[8], gk[8];
+  load8(qg + li * 8, gq);
+  load8(kg + li * 8, gk);
+  const int64_t nrows = (int64_t)T_ * 2 * H;
+  // every row group of every block runs the same number of iterations (shuffles)
+  const int64_t stride = (int64_t)gridDim.x * NG;
+  const int64_t iters = (nrows + stride - 1) / stride;
+  for (int64_t it = 0; it < iters; ++it) {
+    const int64_t row = it * stride + (int64_t)blockIdx.x * NG + grp;
+    const bool valid = row < nrows;
+    const int64_t t = valid ? row / (2 * H) : 0;
+    const int j = valid ? (int)(row % (2 * H)) : 0;
+    const int sidx = j / H, h = j % H;
+    const int64_t off_d = t * ldd + sidx * A + h * DH + li * 8;
+    const int64_t off_s = t * lds + sidx * A + h * DH + li * 8;
+    float dy[8], xv[8], xh[8], gh[8];
+    if (valid) {
+      load8(d + off_d, dy);
+      load8(src + off_s, xv);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dy[i] = xv[i] = 0.f;
+    }
+    const float mu = valid ? mean[row] : 0.f, r = valid ? rstd[row] : 0.f;
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      xh[i] = (xv[i] - mu) * r;
+      gh[i] = dy[i] * (sidx ? gk[i] : gq[i]);
+      s1 += gh[i];
+      s2 += gh[i] * xh[i];
+    }
+#pragma unroll
+    for (int o = G / 2; o >= 1; o >>= 1) {
+      s1 += __shfl_xor(s1, o, 64);
+      s2 += __shfl_xor(s2, o, 64);
+    }
+    if (valid) {
+      const float m1 = s1 / (float)DH, m2 = s2 / (float)DH;
+      float o8[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o8[i] = r * (gh[i] - m1 - xh[i] * m2);
+      store8(d + off_d, o8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (sidx) { ag[1][i] += dy[i] * xh[i]; ab[1][i] += dy[i]; }
+        else      { ag[0][i] += dy[i] * xh[i]; ab[0][i] += dy[i]; }
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    sm[grp][0][li * 8 + i] = ag[0][i];
+    sm[grp][1][li * 8 + i] = ab[0][i];
+    sm[grp][2][li * 8 + i] = ag[1][i];
+    sm[grp][3][li * 8 + i] = ab[1][i];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 4 * DH; e += 256) {
+    const int which = e / DH, c = e % DH;
+    float s = 0.f;
+    for (int g2 = 0; g2 < NG; ++g2) s += sm[g2][which][c];
+    part[(int64_t)blockIdx.x * 4 * DH + e] = s;
+  }
+}
+
+__global__ void __launch_bounds__(256) qkln_param_final(const float* __restrict__ part, int blocks, int dh,
+                                                        float* dqg, float* dqb, float* dkg, float* dkb,
+                                                        int accumulate) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= 4 * dh) return;
+  float s = 0.f;
+  for (int k = 0; k < blocks; ++k) s += part[(int64_t)k * 4 * dh + e];
+  const int which = e / dh, c = e % dh;
+  float* out = which == 0 ? dqg : which == 1 ? dqb : which == 2 ? dkg : dkb;
+  out[c] = accumulate ? out[c] + s : s;
+}
+
+// ---- elementwise --------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) cast_kernel(const float* __restrict__ src, T* __restrict__ dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = from_f<T>(src[i]);
+}
+
+__global__ void __launch_bounds__(256) axpy_kernel(const float* __restrict__ src, float* dst, int64_t n, int acc) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = acc ? dst[i] + src[i] : src[i];
+}
+
+__global__ void __launch_bounds__(256) fill_kernel(float* dst, int64_t n, float v) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) dst[i] = v;
+}
+
+unsigned grid1d(int64_t n) { return (unsigned)std::max<int64_t>(1, std::min<int64_t>(cdiv(n, 256), 16384)); }
+
+template <typename T, int NCH>
+orbit_status ln_fwd_t(const void* x, int64_t ldx, const void* g, const void* b, void* y, int64_t ldy,
+                      float* mean, float* rstd, int rows, int n, float eps, hipStream_t s) {
+  KernelInfo ki{sizeof(T) == 2 ? "ln_fwd_kernel<bf16>" : "ln_fwd_kernel<f32>", 8.0 * rows * n,
+                2.0 * rows * n * sizeof(T)};
+  return launch(ki, ln_fwd_kernel<T, NCH>, dim3(rows), dim3(256), 0, s, (const T*)x, ldx, (const T*)g,
+                (const T*)b, (T*)y, ldy, mean, rstd, n, eps);
+}
+
+template <typename T, int NCH>
+orbit_status ln_bwd_t(const void* dy, int64_t lddy, const void* x, int64_t ldx, const float* mean,
+                      const float* rstd, const void* g, const void* dres, void* dx, int64_t lddx, int rows,
+                      int n, hipStream_t s) {
+  KernelInfo ki{sizeof(T) == 2 ? "ln_bwd_kernel<bf16>" : "ln_bwd_kernel<f32>", 12.0 * rows * n,
+                (dres ? 4.0 : 3.0) * rows * n * sizeof(T)};
+  return launch(ki, ln_bwd_kernel<T, NCH>, dim3(rows), dim3(256), 0, s, (const T*)dy, lddy, (const T*)x, ldx,
+                mean, rstd, (const T*)g, (const T*)dres, (T*)dx, lddx, n);
+}
+
+template <typename T>
+orbit_status ln_fwd_dispatch(const void* x, int64_t ldx, const void* g, const void* b, void* y, int64_t ldy,
+                             float* mean, float* rstd, int rows, int n, float eps, hipStream_t s) {
+  const int nch = (int)cdiv(n, 2048);
+  if (nch <= 1) return ln_fwd_t<T, 1>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
+  if (nch <= 2) return ln_fwd_t<T, 2>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
+  if (nch <= 4) return ln_fwd_t<T, 4>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
+  if (nch <= 8) return ln_fwd_t<T, 8>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
+  set_error("layernorm: row length %d exceeds 16384", n);
+  return ORBIT_E_UNSUPPORTED;
+}
+
+template <typename T>
+orbit_status ln_bwd_dispatch(const void* dy, int64_t lddy, const void* x, int64_t ldx, const float* mean,
+                             const float* rstd, const void* g, const void* dres, void* dx, int64_t lddx,
+                             int rows, int n, hipStream_t s) {
+  const int nch = (int)cdiv(n, 2048);
+  if (nch <= 1) return ln_bwd_t<T, 1>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
+  if (nch <= 2) return ln_bwd_t<T, 2>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
+  if (nch <= 4) return ln_bwd_t<T, 4>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
+  if (nch <= 8) return ln_bwd_t<T, 8>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
+  set_error("layernorm: row length %d exceeds 16384", n);
+  return ORBIT_E_UNSUPPORTED;
+}
+
+template <typename T>
+orbit_status colsum_t(const void* dy, int64_t lddy, int rows, int n, const void* x, int64_t ldx,
+                      const float* mean, const float* rstd, float* out_sum, float* out_xsum, int accumulate,
+                      void* ws, hipStream_t s) {
+  const int chunks = (int)cdiv(rows, kRowsPerChunk);
+  float* ps = static_cast<float*>(ws);
+  float* px = ps + (int64_t)chunks * n;
+  dim3 grid((unsigned)cdiv(n, kColsPerBlock), (unsigned)chunks);
+  KernelInfo ki{sizeof(T) == 2 ? "colsum_partial<bf16>" : "colsum_partial<f32>", 0.0,
+                (x ? 2.0 : 1.0) * rows * (double)n * sizeof(T)};
+  if (x) {
+    ORBIT_TRY(launch(ki, colsum_partial<T, true>, grid, dim3(256), 0, s, (const T*)dy, lddy, rows, n,
+                     (const T*)x, ldx, mean, rstd, ps, px));
+  } else {
+    ORBIT_TRY(launch(ki, colsum_partial<T, false>, grid, dim3(256), 0, s, (const T*)dy, lddy, rows, n,
+                     (const T*)nullptr, (int64_t)0, (const float*)nullptr, (const float*)nullptr, ps, px));
+  }
+  KernelInfo kf{"colsum_final", 0.0, (double)chunks * n * 4};
+  if (out_sum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s,
+                                (const float*)ps, chunks, n, out_sum, accumulate));
+  if (x && out_xsum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s,
+                                      (const float*)px, chunks, n, out_xsum, accumulate));
+  return ORBIT_OK;
+}
+
+template <typename T, int DH>
+orbit_status qk_fwd_t(const void* src, int64_t lds, void* dst, int64_t ldd, const void* qg, const void* qb,
+                      const void* kg, const void* kb, float* mean, float* rstd, int T_, int H, float eps,
+                      hipStream_t s) {
+  constexpr int G = DH / 8;
+  const int64_t rows = (int64_t)T_ * 2 * H;
+  KernelInfo ki{sizeof(T) == 2 ? "qkln_fwd_kernel<bf16>" : "qkln_fwd_kernel<f32>", 8.0 * rows * DH,
+                2.0 * rows * DH * sizeof(T)};
+  return launch(ki, qkln_fwd_kernel<T, DH>, dim3((unsigned)cdiv(rows, 256 / G)), dim3(256), 0, s,
+                (const T*)src, lds, (T*)dst, ldd, (const T*)qg, (const T*)qb, (const T*)kg, (const T*)kb, mean,
+                rstd, T_, H, H * DH, eps);
+}
+
+template <typename T, int DH>
+orbit_status qk_bwd_t(void* d, int64_t ldd, const void* src, int64_t lds, const float* mean, const float* rstd,
+                      const void* qg, const void* kg, float* dqg, float* dqb, float* dkg, float* dkb,
+                      int accumulate, int T_, int H, void* ws, hipStream_t s) {
+  const int64_t rows = (int64_t)T_ * 2 * H;
+  const int blocks = (int)std::min<int64_t>(kQkBwdBlocks, cdiv(rows, 256 / (DH / 8)));
+  float* part = static_cast<float*>(ws);
+  KernelInfo ki{sizeof(T) == 2 ? "qkln_bwd_kernel<bf16>" : "qkln_bwd_kernel<f32>", 12.0 * rows * DH,
+                3.0 * rows * DH * sizeof(T)};
+  ORBIT_TRY(launch(ki, qkln_bwd_kernel<T, DH>, dim3(blocks), dim3(256), 0, s, (T*)d, ldd, (const T*)src, lds,
+                   mean, rstd, (const T*)qg, (const T*)kg, T_, H, H * DH, part));
+  KernelInfo kf{"qkln_param_final", 0.0, 4.0 * blocks * 4 * DH};
+  return launch(kf, qkln_param_final, dim3((unsigned)cdiv(4 * DH, 256)), dim3(256), 0, s, (const float*)part,
+                blocks, DH, dqg, dqb, dkg, dkb, accumulate);
+}
+
+}  // namespace
+
+orbit_status layernorm_fwd(orbit_dtype dt, const void* x, int64_t ldx, const void* g, const void* b, void* y,
+                           int64_t ldy, float* mean, float* rstd, int rows, int n, float eps, hipStream_t s) {
+  if (dt == ORBIT_BF16) return ln_fwd_dispatch<bf16>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
+  return ln_fwd_dispatch<float>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
+}
+
+orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const void* x, int64_t ldx,
+                           const float* mean, const float* rstd, const void* g, const void* dres, void* dx,
+                           int64_t lddx, int rows, int n, hipStream_t s) {
+  if (dt == ORBIT_BF16) return ln_bwd_dispatch<bf16>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
+  return ln_bwd_dispatch<float>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
+}
+
+size_t colsum_workspace_bytes(int rows, int n) {
+  return align_up((size_t)2 * cdiv(rows, kRowsPerChunk) * (size_t)n * sizeof(float));
+}
+
+orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int n, const void* x, int64_t ldx,
+                    const float* mean, const float* rstd, float* out_sum, float* out_xsum, int accumulate,
+                    void* ws, hipStream_t s) {
+  if (rows <= 0 || n <= 0) return ORBIT_OK;
+  if (dt == ORBIT_BF16)
+    return colsum_t<bf16>(dy, lddy, rows, n, x, ldx, mean, rstd, out_sum, out_xsum, accumulate, ws, s);
+  return colsum_t<float>(dy, lddy, rows, n, x, ldx, mean, rstd, out_sum, out_xsum, accumulate, ws, s);
+}
+
+orbit_status colsum_f32(const float* dy, int64_t lddy, int rows, int n, float* out_sum, int accumulate, void* ws,
+                        hipStream_t s) {
+  if (rows <= 0 || n <= 0) return ORBIT_OK;
+  return colsum_t<float>(dy, lddy, rows, n, nullptr, 0, nullptr, nullptr, out_sum, nullptr, accumulate, ws, s);
+}
+
+orbit_status qk_norm_fwd(orbit_dtype dt, const void* src, int64_t lds, void* dst, int64_t ldd, const void* qg,
+                         const void* qb, const void* kg, const void* kb, float* mean, float* rstd, int T_, int H,
+                         int dh, float eps, hipStream_t s) {
+#define QKF(TT, D) return qk_fwd_t<TT, D>(src, lds, dst, ldd, qg, qb, kg, kb, mean, rstd, T_, H, eps, s)
+  if (dt == ORBIT_BF16) {
+    if (dh == 32) QKF(bf16, 32);
+    if (dh == 64) QKF(bf16, 64);
+    if (dh == 128) QKF(bf16, 128);
+  } else {
+    if (dh == 32) QKF(float, 32);
+    if (dh == 64) QKF(float, 64);
+    if (dh == 128) QKF(float, 128);
+  }
+#undef QKF
+  set_error("qk_norm: head_dim %d unsupported", dh);
+  return ORBIT_E_UNSUPPORTED;
+}
+
+size_t qk_norm_bwd_workspace_bytes(int dh) { return align_up((size_t)kQkBwdBlocks * 4 * dh * sizeof(float)); }
+
+orbit_status qk_norm_bwd(orbit_dtype dt, void* d, int64_t ldd, const void* src, int64_t lds, const float* mean,
+                         const float* rstd, const void* qg, const void* kg, float* dqg, float* dqb, float* dkg,
+                         float* dkb, int accumulate, int T_, int H, int dh, void* ws, hipStream_t s) {
+#define QKB(TT, D) \
+  return qk_bwd_t<TT, D>(d, ldd, src, lds, mean, rstd, qg, kg, dqg, dqb, dkg, dkb, accumulate, T_, H, ws, s)
+  if (dt == ORBIT_BF16) {
+    if (dh == 32) QKB(bf16, 32);
+    if (dh == 64) QKB(bf16, 64);
+    if (dh == 128) QKB(bf16, 128);
+  } else {
+    if (dh == 32) QKB(float, 32);
+    if (dh == 64) QKB(float, 64);
+    if (dh == 128) QKB(float, 128);
+  }
+#undef QKB
+  set_error("qk_norm: head_dim %d unsupported", dh);
+  return ORBIT_E_UNSUPPORTED;
+}
+
+orbit_status cast_from_f32(orbit_dtype dt, const float* src, void* dst, int64_t n, hipStream_t s) {
+  KernelInfo ki{"cast_kernel", 0.0, (4.0 + (dt == ORBIT_BF16 ? 2 : 4)) * n};
+  if (dt == ORBIT_BF16) return launch(ki, cast_kernel<bf16>, dim3(grid1d(n)), dim3(256), 0, s, src, (bf16*)dst, n);
+  return launch(ki, cast_kernel<float>, dim3(grid1d(n)), dim3(256), 0, s, src, (float*)dst, n);
+}
+
+orbit_status axpy_f32(const float* src, float* dst, int64_t n, int accumulate, hipStream_t s) {
+  KernelInfo ki{"axpy_kernel", 0.0, 12.0 * n};
+  return launch(ki, axpy_kernel, dim3(grid1d(n)), dim3(256), 0, s, src, dst, n, accumulate);
+}
+
+orbit_status fill_f32(float* dst, int64_t n, float v, hipStream_t s) {
+  KernelInfo ki{"fill_kernel", 0.0, 4.0 * n};
+  return launch(ki, fill_kernel, dim3(grid1d(n)), dim3(256), 0, s, dst, n, v);
+}
+
+}  // namespace orbit

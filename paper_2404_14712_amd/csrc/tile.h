@@ -1,0 +1,96 @@
+// HBM -> register -> LDS staging of one operand tile, shared by the GEMM and
+// the attention kernels.
+//
+// The LDS copy is always K-contiguous: S[row][k] with a row pitch of KD + 16
+// bytes (the padding spreads the 16-byte fragment reads of 32 consecutive
+// rows over distinct banks). Two source layouts:
+//   KMAJ = true : element (row, k) at X[row*ld + k]  (rows are contiguous in k)
+//   KMAJ = false: element (row, k) at X[k*ld + row]  (rows are contiguous in the
+//                 row dimension; transposed on the way: each thread loads a
+//                 4(k) x 16-byte tile and writes 4-element k-runs)
+#pragma once
+#include "common.h"
+
+namespace orbit {
+
+template <typename T, int ROWS, int KD, int NT, bool KMAJ>
+struct TileLoader {
+  static constexpr int E = 16 / (int)sizeof(T);
+  static constexpr int PITCH = KD + E;
+  static_assert(KD % E == 0 && ROWS % E == 0 && KD % 4 == 0, "tile shape");
+  static constexpr int NCH = KMAJ ? ROWS * (KD / E) : (KD / 4) * (ROWS / E);
+  static constexpr int PER = (NCH + NT - 1) / NT;
+  static constexpr int REGS = KMAJ ? PER : PER * 4;
+  U128 r[REGS];
+
+  // X: operand base. Tile rows row0 .. row0+ROWS-1 (valid while < rlim), k
+  // range k0 .. k0+KD-1 (valid while < kend). For the transposed layout a
+  // second source X2 supplies the k-rows at and after ksplit (concatenated K).
+  ORBIT_DEV void load(const T* X, const T* X2, int ksplit, int64_t ld, int row0, int rlim,
+                      int k0, int kend, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (KMAJ) {
+        const int row = c / (KD / E), kc = c % (KD / E);
+        const int gr = row0 + row, gk = k0 + kc * E;
+        r[i] = (c < NCH && gr < rlim && gk < kend) ? ld128(X + (int64_t)gr * ld + gk) : zero128();
+      } else {
+        const int kg = c / (ROWS / E), rc = c % (ROWS / E);
+        const int gr = row0 + rc * E;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int gk = k0 + kg * 4 + j;
+          const bool ok = c < NCH && gr < rlim && gk < kend;
+          const T* base = (X2 && gk >= ksplit) ? X2 + (int64_t)(gk - ksplit) * ld : X + (int64_t)gk * ld;
+          r[i * 4 + j] = ok ? ld128(base + gr) : zero128();
+        }
+      }
+    }
+  }
+
+  ORBIT_DEV void store(T* S, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c >= NCH) continue;
+      if (KMAJ) {
+        const int row = c / (KD / E), kc = c % (KD / E);
+        st128(S + row * PITCH + kc * E, r[i]);
+      } else {
+        const int kg = c / (ROWS / E), rc = c % (ROWS / E);
+        store_transposed(S + (rc * E) * PITCH + kg * 4, &r[i * 4]);
+      }
+    }
+  }
+
+  // q[0..3]: four k-rows of E row-elements; writes E runs of 4 k-values
+  static ORBIT_DEV void store_transposed(T* S, const U128* q) {
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int w = e >> 1, sh = (e & 1) * 16;
+        const uint32_t v0 = (q[0].w[w] >> sh) & 0xffffu;
+        const uint32_t v1 = (q[1].w[w] >> sh) & 0xffffu;
+        const uint32_t v2 = (q[2].w[w] >> sh) & 0xffffu;
+        const uint32_t v3 = (q[3].w[w] >> sh) & 0xffffu;
+        uint2 o;
+        o.x = v0 | (v1 << 16);
+        o.y = v2 | (v3 << 16);
+        *reinterpret_cast<uint2*>(S + e * PITCH) = o;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        U128 o;
+        o.w[0] = q[0].w[e];
+        o.w[1] = q[1].w[e];
+        o.w[2] = q[2].w[e];
+        o.w[3] = q[3].w[e];
+        st128(S + e * PITCH, o);
+      }
+    }
+  }
+};
+
+}  // namespace orbit

@@ -1,0 +1,118 @@
+"""Kernel-level parity of the building blocks (GEMM, attention, LayerNorm)
+against the fp64 oracle / plain definitions, through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle as O
+from helpers import TOL, check, dev, host
+
+pytestmark = pytest.mark.gpu
+
+R = np.random.default_rng(4242)
+CODE = {"f32": 0, "bf16": 1}
+
+
+def _mat(shape, dtype, scale=1.0):
+    import synth
+    a = (R.standard_normal(shape) * scale).astype(np.float32)
+    return synth.bf16_round(a) if dtype == "bf16" else a
+
+
+GEMM_SHAPES = [(37, 40, 24), (200, 136, 72), (130, 264, 520), (1, 48, 64), (300, 16, 1000), (64, 64, 16384),
+               (257, 129 * 8, 8)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["KN", "KK", "MM"])
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+def test_gemm(lib, dtype, layout, shape):
+    import torch
+    M, N, K = shape
+    a_k, b_k = {"KN": (1, 0), "KK": (1, 1), "MM": (0, 0)}[layout]
+    if (not a_k and M % 8) or (b_k and K % 8) or (not b_k and N % 8) or (a_k and K % 8):
+        pytest.skip("contiguous dimension not a multiple of 8")
+    A = _mat((M, K), dtype)
+    B = _mat((K, N), dtype)
+    bias = _mat((N,), dtype)
+    Adev = dev(A if a_k else A.T.copy(), dtype)
+    Bdev = dev(B.T.copy() if b_k else B, dtype)
+    lda = K if a_k else M
+    ldb = K if b_k else N
+    for c_f32 in ([1] if dtype == "f32" else [0, 1]):
+        C = torch.zeros(M, N, dtype=torch.float32 if c_f32 else torch.bfloat16, device="cuda")
+        nb = lib.orbit_gemm_workspace_bytes(CODE[dtype], M, N, K, a_k, b_k)
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        lib.orbit_gemm(CODE[dtype], M, N, K, Adev, lda, a_k, Bdev, ldb, b_k, C, N, c_f32, 0.5, dev(bias, dtype),
+                       0, ws)
+        torch.cuda.synchronize()
+        ref = 0.5 * (A.astype(np.float64) @ B.astype(np.float64)) + bias
+        tol = TOL[dtype] if dtype == "f32" else 1e-2
+        check(f"gemm {layout} {shape} c_f32={c_f32}", host(C), ref, tol)
+    # accumulate into float32
+    C = torch.ones(M, N, dtype=torch.float32, device="cuda")
+    lib.orbit_gemm(CODE[dtype], M, N, K, Adev, lda, a_k, Bdev, ldb, b_k, C, N, 1, 1.0, None, 1, ws)
+    torch.cuda.synchronize()
+    check(f"gemm acc {layout} {shape}", host(C), 1.0 + A.astype(np.float64) @ B, TOL[dtype] if dtype == "f32"
+          else 1e-2)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dh", [32, 64, 128])
+@pytest.mark.parametrize("L", [1, 37, 130])
+def test_attention(lib, dtype, dh, L):
+    import torch
+    B, H = 2, 3
+    A = H * dh
+    # q, k, v live in one [T, 3A] buffer (as in the block), scaled like QK-normalised rows
+    qkv = _mat((B * L, 3 * A), dtype, 1.0)
+    dO = _mat((B * L, A), dtype, 1.0)
+    t = dev(qkv, dtype)
+    e = t.element_size()
+    q, k, v = t.data_ptr(), t.data_ptr() + A * e, t.data_ptr() + 2 * A * e
+    o = torch.zeros(B * L, A, dtype=t.dtype, device="cuda")
+    lse = torch.zeros(B, H, L, dtype=torch.float32, device="cuda")
+    lib.orbit_attention_fwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o, A, lse)
+    g = torch.zeros(B * L, 3 * A, dtype=t.dtype, device="cuda")
+    ge = g.data_ptr()
+    Dws = torch.zeros(B * H * L, dtype=torch.float32, device="cuda")
+    dOd = dev(dO, dtype)
+    lib.orbit_attention_bwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o, A, lse, dOd, A, ge,
+                            ge + A * e, ge + 2 * A * e, 3 * A, Dws)
+    torch.cuda.synchronize()
+    hd = lambda x: x.reshape(B, L, H, dh).transpose(0, 2, 1, 3)
+    Q, K_, V_ = hd(qkv[:, :A]), hd(qkv[:, A:2 * A]), hd(qkv[:, 2 * A:])
+    ref_o, P = O.attention_fwd(Q, K_, V_)
+    dq, dk, dv = O.attention_bwd(hd(dO), Q, K_, V_, P)
+    un = lambda x: x.transpose(0, 2, 1, 3).reshape(B * L, A)
+    tol = TOL[dtype]
+    check("o", host(o), un(ref_o), tol)
+    lse_ref = np.log(np.exp((Q @ np.swapaxes(K_, -1, -2)) / np.sqrt(dh)).sum(-1))
+    check("lse", host(lse), lse_ref, tol)
+    gh = host(g)
+    check("dq", gh[:, :A], un(dq), tol)
+    check("dk", gh[:, A:2 * A], un(dk), tol)
+    check("dv", gh[:, 2 * A:], un(dv), tol)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("rows,n", [(1, 8), (37, 128), (300, 1032), (5, 16384)])
+def test_layernorm(lib, dtype, rows, n):
+    import torch
+    x = _mat((rows, n), dtype, 3.0) + (np.float32(2.0) if dtype == "f32" else 0)
+    if dtype == "bf16":
+        import synth
+        x = synth.bf16_round(x)
+    g = _mat((n,), dtype, 0.3) + np.float32(1.0)
+    b = _mat((n,), dtype, 0.3)
+    if dtype == "bf16":
+        import synth
+        g = synth.bf16_round(g)
+    y = torch.zeros(rows, n, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda")
+    mean = torch.zeros(rows, dtype=torch.float32, device="cuda")
+    rstd = torch.zeros(rows, dtype=torch.float32, device="cuda")
+    lib.orbit_layernorm_fwd(CODE[dtype], rows, n, dev(x, dtype), dev(g, dtype), dev(b, dtype), 1e-5, y, mean, rstd)
+    torch.cuda.synchronize()
+    ref, (xhat, r) = O.layer_norm_fwd(x, g, b, 1e-5)
+    check("ln y", host(y), ref, TOL[dtype])
+    check("ln rstd", host(rstd), r[:, 0], 1e-4)
+    check("ln mean", host(mean), x.astype(np.float64).mean(-1), 1e-4)

@@ -1,0 +1,288 @@
+"""Call-level parity of every C-ABI entry point against the fp64 oracle on
+seeded synthetic inputs, at sizes the oracle finishes in seconds that still
+span several tiles and ragged tails; fp32 mode within 1e-4 and bf16 mode
+within 2e-2 (per-tensor max relative error)."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from helpers import TOL, check, dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+def _dims(c: synth.Config, mode: str):
+    from paper_2404_14712_amd.model import PassDims
+    return PassDims(mode=mode, dtype=c.dtype, B=c.B, L=c.L, d=c.d, blocks=c.blocks, heads=c.heads,
+                    head_dim=c.head_dim, mlp=c.mlp, qk_norm=c.qk_norm, eps=c.eps, V=c.V, grid=c.grid,
+                    agg_heads=c.agg_heads, agg_head_dim=c.agg_head_dim)
+
+
+def _dev_params(p: dict, dtype: str):
+    return {k: (None if v is None else dev(v, dtype)) for k, v in p.items()}
+
+
+# ---------------------------------------------------------------------------
+# patch embedding
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,V,Hg,Wg,d", [(2, 3, 8, 12, 40), (1, 5, 16, 16, 1032), (2, 2, 4, 8, 2056)])
+def test_patch_embed(lib, dtype, B, V, Hg, Wg, d):
+    import torch
+    from paper_2404_14712_amd._lib import EmbedDesc
+    c = synth.small_config(1, dtype=dtype, B=B, V=V, grid=(Hg, Wg), d=d, L=(Hg // 4) * (Wg // 4))
+    img = synth.image(c)
+    e = synth.embed_params(c)
+    desc = EmbedDesc(B, V, Hg, Wg, 4, d, 1 if dtype == "bf16" else 0)
+    tok = torch.zeros(B, c.L, V, d, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda")
+    ed = _dev_params(e, dtype)
+    imgd = dev(img, "f32")
+    lib.orbit_patch_embed(desc, imgd, ed["w_pe"], ed["b_pe"], ed["ve"], tok)
+    ref = O.patch_embed_fwd(img, e["w_pe"], e["b_pe"], e["ve"], 4)
+    dtok = synth.normal(c.cfg, "dtok", ref.shape, dtype=dtype)
+    ws = torch.empty(lib.orbit_patch_embed_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    g = {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in e.items()}
+    lib.orbit_patch_embed_bwd(desc, imgd, dev(dtok, dtype), g["w_pe"], g["b_pe"], g["ve"], 0, ws)
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    check("tok", host(tok), ref, tol)
+    gr = O.patch_embed_bwd(img, dtok, 4)
+    for k in gr:
+        check(f"d{k}", host(g[k]), gr[k], tol)
+
+
+# ---------------------------------------------------------------------------
+# aggregation
+# ---------------------------------------------------------------------------
+AGG_CASES = [
+    # dtype, B, L, V, d, heads, head_dim
+    ("f32", 2, 37, 4, 128, 4, 32),
+    ("f32", 1, 20, 13, 64, 4, 16),
+    ("bf16", 2, 33, 48, 256, 8, 32),
+    ("bf16", 1, 70, 91, 512, 8, 64),      # V of the 91-variable set, A = d
+    ("bf16", 1, 19, 7, 1024, 8, 64),       # column shard: A = 512 != d
+]
+
+
+@pytest.mark.parametrize("case", AGG_CASES)
+def test_var_aggregate(lib, case):
+    import torch
+    from paper_2404_14712_amd._lib import AggDesc
+    dtype, B, L, V, d, H, dh = case
+    c = synth.small_config(2, dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
+    A = H * dh
+    tok = synth.normal(c.cfg, "tok", (B, L, V, d), dtype=dtype)
+    prm = synth.make_params(c.cfg, "agg", synth.agg_param_shapes(d, A, L), 0.2, dtype)
+    desc = AggDesc(B, L, V, d, H, dh, 1 if dtype == "bf16" else 0)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    z = torch.zeros(B, L, d, dtype=tdt, device="cuda")
+    saved = torch.empty(lib.orbit_var_aggregate_saved_bytes(desc), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(lib.orbit_var_aggregate_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    pd = _dev_params(prm, dtype)
+    tokd = dev(tok, dtype)
+    lib.orbit_var_aggregate(desc, tokd, pd, z, saved, ws)
+    dz = synth.normal(c.cfg, "dz", (B, L, d), dtype=dtype)
+    dtok = torch.zeros(B, L, V, d, dtype=tdt, device="cuda")
+    g = {k: torch.full(v.shape, 7.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
+    lib.orbit_var_aggregate_bwd(desc, tokd, pd, saved, dev(dz, dtype), dtok, g, 0, ws)
+    torch.cuda.synchronize()
+    ref, cache = O.agg_fwd(tok, prm, H)
+    rdtok, rg = O.agg_bwd(dz, cache, prm)
+    tol = TOL[dtype]
+    check("z", host(z), ref, tol)
+    check("dtok", host(dtok), rdtok, tol)
+    for k in rg:
+        check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["b_q"])
+
+
+# ---------------------------------------------------------------------------
+# block
+# ---------------------------------------------------------------------------
+BLOCK_CASES = [
+    # dtype, B, L, d, heads, head_dim, mlp, qk_norm
+    ("f32", 2, 37, 128, 4, 32, 512, 1),
+    ("f32", 1, 130, 256, 2, 64, 264, 0),
+    ("f32", 2, 64, 192, 2, 128, 128, 1),
+    ("bf16", 2, 100, 256, 4, 64, 1024, 1),
+    ("bf16", 1, 257, 512, 4, 128, 1032, 1),
+    ("bf16", 2, 33, 384, 3, 32, 256, 0),
+    ("bf16", 1, 150, 1024, 2, 128, 512, 1),   # shard: A = 256 != d, local MLP width
+]
+
+
+def _run_block(lib, case, accumulate=0):
+    import torch
+    from paper_2404_14712_amd._lib import BlockDesc
+    dtype, B, L, d, H, dh, F, qk = case
+    c = synth.small_config(4, dtype=dtype, B=B, L=L, d=d, heads=H, head_dim=dh, mlp=F, qk_norm=qk, sigma=0.05)
+    x = synth.activations(c, "x")
+    dy = synth.normal(c.cfg, "dy", x.shape, dtype=dtype)
+    prm = synth.block_params(c, 0)
+    desc = BlockDesc(B, L, d, H, dh, F, qk, 1e-5, 1 if dtype == "bf16" else 0)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    saved = torch.empty(lib.orbit_vit_block_saved_bytes(desc), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(lib.orbit_vit_block_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    xd = dev(x, dtype)
+    y = torch.zeros(B, L, d, dtype=tdt, device="cuda")
+    pd = _dev_params(prm, dtype)
+    lib.orbit_vit_block_fwd(desc, pd, xd, y, saved, ws)
+    dx = torch.zeros(B, L, d, dtype=tdt, device="cuda")
+    g = {k: torch.full(v.shape, 0.5 if accumulate else 0.0, dtype=torch.float32, device="cuda")
+         for k, v in prm.items()}
+    lib.orbit_vit_block_bwd(desc, pd, xd, saved, dev(dy, dtype), dx, g, accumulate, ws)
+    torch.cuda.synchronize()
+    return x, dy, prm, y, dx, g
+
+
+@pytest.mark.parametrize("case", BLOCK_CASES)
+def test_vit_block(lib, case):
+    dtype, B, L, d, H, dh, F, qk = case
+    x, dy, prm, y, dx, g = _run_block(lib, case)
+    ref, cache = O.block_fwd(x, prm, H, qk, 1e-5)
+    rdx, rg = O.block_bwd(dy, cache, prm)
+    tol = TOL[dtype]
+    check("y", host(y), ref, tol)
+    check("dx", host(dx), rdx, tol)
+    for k in rg:
+        check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["ln1_b"])
+
+
+def test_vit_block_accumulate(lib):
+    case = ("f32", 2, 37, 128, 4, 32, 512, 1)
+    x, dy, prm, y, dx, g = _run_block(lib, case, accumulate=1)
+    _, cache = O.block_fwd(x, prm, 4, 1, 1e-5)
+    _, rg = O.block_bwd(dy, cache, prm)
+    for k in rg:
+        check(f"acc d{k}", host(g[k]), rg[k] + 0.5, 1e-4)
+
+
+def test_vit_block_inference_and_determinism(lib):
+    """saved = NULL gives the same output; two runs are bitwise identical."""
+    import torch
+    from paper_2404_14712_amd._lib import BlockDesc
+    case = ("bf16", 2, 100, 256, 4, 64, 1024, 1)
+    x, dy, prm, y, dx, g = _run_block(lib, case)
+    x2, dy2, prm2, y2, dx2, g2 = _run_block(lib, case)
+    assert torch.equal(y, y2) and torch.equal(dx, dx2)
+    for k in g:
+        assert torch.equal(g[k], g2[k]), k
+    dtype, B, L, d, H, dh, F, qk = case
+    desc = BlockDesc(B, L, d, H, dh, F, qk, 1e-5, 1)
+    ws = torch.empty(lib.orbit_vit_block_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    y3 = torch.zeros_like(y)
+    lib.orbit_vit_block_fwd(desc, _dev_params(prm, dtype), dev(x, dtype), y3, None, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y3)
+
+
+# ---------------------------------------------------------------------------
+# head and loss
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,B,L,d,out,final_ln", [("f32", 2, 37, 128, 64, 1), ("bf16", 2, 100, 512, 768, 1),
+                                                      ("bf16", 1, 33, 256, 1456, 0)])
+def test_head(lib, dtype, B, L, d, out, final_ln):
+    import torch
+    from paper_2404_14712_amd._lib import HeadDesc
+    c = synth.small_config(1, dtype=dtype, B=B, L=L, d=d, V=out // 16, sigma=0.05)
+    x = synth.activations(c, "x")
+    prm = synth.head_params(c)
+    desc = HeadDesc(B, L, d, out, final_ln, 1e-5, 1 if dtype == "bf16" else 0)
+    saved = torch.empty(lib.orbit_head_saved_bytes(desc), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(lib.orbit_head_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    pred = torch.zeros(B, L, out, dtype=torch.float32, device="cuda")
+    pd = _dev_params(prm, dtype)
+    xd = dev(x, dtype)
+    lib.orbit_head_fwd(desc, xd, pd, pred, saved, ws)
+    dpred = synth.normal(c.cfg, "dpred", (B, L, out))
+    dx = torch.zeros_like(xd)
+    g = {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in prm.items()}
+    lib.orbit_head_bwd(desc, xd, pd, saved, dev(dpred, "f32"), dx, g, 0, ws)
+    torch.cuda.synchronize()
+    ref, cache = O.head_fwd(x, prm, final_ln, 1e-5)
+    # the head's backward GEMMs take dpred in the compute dtype (bf16 rounding of dpred)
+    dpr = synth.bf16_round(dpred) if dtype == "bf16" else dpred
+    rdx, rg = O.head_bwd(dpr, cache, prm)
+    rg["b_h"] = O.head_bwd(dpred, cache, prm)[1]["b_h"]
+    tol = TOL[dtype]
+    check("pred", host(pred), ref, tol)
+    check("dx", host(dx), rdx, tol)
+    for k in rg:
+        check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["b_h"])
+
+
+@pytest.mark.parametrize("n", [1, 1000, 6291456])
+def test_mse(lib, n):
+    import torch
+    r = np.random.default_rng(n)
+    pred = r.standard_normal(n).astype(np.float32)
+    tgt = r.standard_normal(n).astype(np.float32)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    dpred = torch.zeros(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(lib.orbit_mse_workspace_bytes(n), dtype=torch.uint8, device="cuda")
+    lib.orbit_mse_loss(dev(pred, "f32"), dev(tgt, "f32"), n, 2.0, loss, dpred, ws)
+    torch.cuda.synchronize()
+    rl, rd = O.mse(pred, tgt, 2.0)
+    assert abs(host(loss)[0] - rl) <= 1e-5 * rl
+    check("dpred", host(dpred), rd, 1e-6)
+
+
+# ---------------------------------------------------------------------------
+# whole model: the tiny fp32 configuration exactly, and a reduced bf16 one
+# ---------------------------------------------------------------------------
+def _model_inputs(c):
+    img = synth.image(c)
+    tgt = synth.target(c)
+    emb = synth.embed_params(c)
+    agg = synth.agg_params(c)
+    blocks = [synth.block_params(c, i) for i in range(c.blocks)]
+    head = synth.head_params(c)
+    return img, tgt, emb, agg, blocks, head
+
+
+def _run_model(lib, c):
+    import torch
+    from paper_2404_14712_amd.model import ViTPass
+    img, tgt, emb, agg, blocks, head = _model_inputs(c)
+    params = {"embed": _dev_params(emb, c.dtype), "agg": _dev_params(agg, c.dtype),
+              "blocks": [_dev_params(b, c.dtype) for b in blocks], "head": _dev_params(head, c.dtype)}
+    vp = ViTPass(lib, _dims(c, "full"), params)
+    loss = vp.forward_backward({"img": dev(img, "f32"), "tgt": dev(tgt, "f32")})
+    torch.cuda.synchronize()
+    return vp, loss, (img, tgt, emb, agg, blocks, head)
+
+
+def _check_model(vp, loss, inputs, c, tol):
+    img, tgt, emb, agg, blocks, head = inputs
+    rl, pred, rg = O.model_fwd_bwd(img, tgt, emb, agg, blocks, head, p=4, agg_heads=c.agg_heads, heads=c.heads,
+                                   qk_norm=c.qk_norm, eps=c.eps)
+    assert abs(host(loss)[0] - rl) <= tol * abs(rl), (host(loss)[0], rl)
+    check("pred", host(vp.pred), pred, tol)
+    G = vp.grads
+    for k, v in rg["embed"].items():
+        check(f"embed.d{k}", host(G["embed"][k]), v, tol)
+    for k, v in rg["agg"].items():
+        check(f"agg.d{k}", host(G["agg"][k]), v, tol, floor_ref=rg["agg"]["b_q"])
+    for i, gb in enumerate(rg["blocks"]):
+        for k, v in gb.items():
+            check(f"block{i}.d{k}", host(G["blocks"][i][k]), v, tol, floor_ref=gb["ln1_b"])
+    for k, v in rg["head"].items():
+        check(f"head.d{k}", host(G["head"][k]), v, tol)
+
+
+def test_full_model_tiny_fp32(lib):
+    """The tiny configuration exactly: 2 x 4 variables on 32x64, d=128, 2 blocks, fp32."""
+    c = synth.CONFIGS[1]
+    vp, loss, inputs = _run_model(lib, c)
+    _check_model(vp, loss, inputs, c, TOL["f32"])
+
+
+def test_full_model_reduced_bf16(lib):
+    """The 115M-scale model's structure at reduced size (bf16): V=12 on 32x64,
+    d=256, 2 blocks, head_dim 64."""
+    c = synth.small_config(2, B=2, L=128, grid=(32, 64), V=12, d=256, blocks=2, heads=4, head_dim=64, mlp=1024,
+                           agg_heads=8, agg_head_dim=32, sigma=0.05)
+    vp, loss, inputs = _run_model(lib, c)
+    _check_model(vp, loss, inputs, c, TOL["bf16"])
