@@ -243,18 +243,23 @@ orbit_status orbit_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const vo
 /* O = softmax(q k^T / sqrt(head_dim)) v for every (sample b, head h), no mask
  * (Sec. III-A). Row t = b*L + l of q holds head h at q[t*ldq + h*head_dim];
  * likewise k, v, o. lse [B, H, L] float32 receives the natural-log
- * normaliser of each softmax row (needed by the backward). */
+ * normaliser of each softmax row (needed by the backward). o32 (may be NULL,
+ * leading dimension ldo32) receives a float32 copy of O. */
 orbit_status orbit_attention_fwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
                                  const void* q, int64_t ldq, const void* k, int64_t ldk,
                                  const void* v, int64_t ldv, void* o, int64_t ldo, float* lse,
-                                 void* stream);
+                                 float* o32, int64_t ldo32, void* stream);
 /* Gradients dq, dk, dv (same row layout, leading dimension ldg) from dO and
- * the forward's o and lse. Dws: B*H*L floats of workspace. */
+ * the forward's O and lse. O is float32 when o_f32 (the forward's o32 copy:
+ * its row sums against dO stay consistent with the recomputed probabilities
+ * in bf16 mode), else dtype. Workspace: orbit_attention_bwd_workspace_bytes. */
+size_t orbit_attention_bwd_workspace_bytes(int32_t B, int32_t H, int32_t L, int32_t head_dim);
 orbit_status orbit_attention_bwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
                                  const void* q, int64_t ldq, const void* k, int64_t ldk,
                                  const void* v, int64_t ldv, const void* o, int64_t ldo,
-                                 const float* lse, const void* dO, int64_t lddo, void* dq, void* dk,
-                                 void* dv, int64_t ldg, float* Dws, void* stream);
+                                 int32_t o_f32, const float* lse, const void* dO, int64_t lddo,
+                                 void* dq, void* dk, void* dv, int64_t ldg, void* ws, size_t ws_bytes,
+                                 void* stream);
 
 /* LayerNorm over rows of length n (biased variance): y = g (x - mean) rstd + b;
  * mean, rstd [rows] float32 (may be NULL). n <= 16384, multiple of 8. */
@@ -281,6 +286,9 @@ int orbit_abi_version(void);
  * their summed duration in milliseconds, summed flops and summed bytes.
  * Not for concurrent use from several threads. */
 orbit_status orbit_timing_enable(int on);
+/* Record only kernels whose name starts with `prefix` (NULL or "" = all).
+ * Applies to launches enqueued after the call. */
+orbit_status orbit_timing_filter(const char* prefix);
 orbit_status orbit_timing_summary(const char* prefix, int64_t* launches, double* total_ms,
                                   double* flops, double* bytes);
 /* Name of the i-th distinct kernel recorded (NULL past the end). */

@@ -50,6 +50,14 @@ def _f(a) -> np.ndarray:
     return np.asarray(a, dtype=F64)
 
 
+def _keep(store):
+    """`store` models the storage of an intermediate between two steps. The
+    oracle proper passes None (exact: nothing is rounded); tests pass a
+    rounding function to measure how much storing intermediates at a reduced
+    precision can move each result (the precision floor of the comparison)."""
+    return store if store is not None else (lambda a: a)
+
+
 # ---------------------------------------------------------------------------
 # Patch tokenisation (Sec. II: independent tokenisation of every variable)
 # ---------------------------------------------------------------------------
@@ -67,7 +75,7 @@ def patchify(img: np.ndarray, p: int) -> np.ndarray:
     return x.reshape(B, V, nh * nw, p * p)
 
 
-def patch_embed_fwd(img, w_pe, b_pe, ve, p: int) -> np.ndarray:
+def patch_embed_fwd(img, w_pe, b_pe, ve, p: int, store=None) -> np.ndarray:
     """tok[b, l, v, :] = P[b, v, l, :] @ w_pe[v] + b_pe[v] + ve[v]   (Sec. II).
 
     One linear map p*p -> d per variable (equal to a stride-p convolution with
@@ -83,7 +91,7 @@ def patch_embed_fwd(img, w_pe, b_pe, ve, p: int) -> np.ndarray:
         if ve is not None:
             e = e + _f(ve[v])
         tok[:, :, v, :] = e
-    return tok
+    return _keep(store)(tok)
 
 
 def patch_embed_bwd(img, dtok, p: int) -> Dict[str, np.ndarray]:
@@ -193,7 +201,7 @@ def _unheads(t):
     return t.transpose(0, 2, 1, 3).reshape(B, L, H * dh)
 
 
-def block_fwd(x, prm: Dict[str, np.ndarray], heads: int, qk_norm: int = 1, eps: float = 1e-5):
+def block_fwd(x, prm: Dict[str, np.ndarray], heads: int, qk_norm: int = 1, eps: float = 1e-5, store=None):
     """One pre-LN transformer block; x[B, L, d] -> y[B, L, d].
 
     h1 = LN1(x); [q|k|v] = h1 W_qkv + b_qkv (columns q, k, v, each head-major);
@@ -207,26 +215,31 @@ def block_fwd(x, prm: Dict[str, np.ndarray], heads: int, qk_norm: int = 1, eps: 
     under Eq. (2): W_qkv / W_fc1 are column shards, W_proj / W_fc2 row shards,
     and the row-shard outputs are partial sums added to the residual unreduced.
     """
+    S = _keep(store)
     x = _f(x)
     p = {k_: _f(v_) for k_, v_ in prm.items()}
     A = p["w_proj"].shape[0]
     h1, c_ln1 = layer_norm_fwd(x, p["ln1_g"], p["ln1_b"], eps)
-    qkv = h1 @ p["w_qkv"] + p["b_qkv"]
+    h1 = S(h1)
+    qkv = S(h1 @ p["w_qkv"] + p["b_qkv"])
     q_raw, k_raw, v_ = qkv[..., :A], qkv[..., A:2 * A], qkv[..., 2 * A:]
     q, k, v = _heads(q_raw, heads), _heads(k_raw, heads), _heads(v_, heads)
     c_qn = c_kn = None
     if qk_norm:
         q, c_qn = layer_norm_fwd(q, p["qn_g"], p["qn_b"], eps)
         k, c_kn = layer_norm_fwd(k, p["kn_g"], p["kn_b"], eps)
+        q, k = S(q), S(k)
     O, P = attention_fwd(q, k, v)
-    o = _unheads(O)
-    x1 = x + o @ p["w_proj"] + p["b_proj"]
+    o = S(_unheads(O))
+    x1 = S(x + o @ p["w_proj"] + p["b_proj"])
     h2, c_ln2 = layer_norm_fwd(x1, p["ln2_g"], p["ln2_b"], eps)
-    u = h2 @ p["w_fc1"] + p["b_fc1"]
-    g = gelu(u)
-    y = x1 + g @ p["w_fc2"] + p["b_fc2"]
+    h2 = S(h2)
+    u_ = h2 @ p["w_fc1"] + p["b_fc1"]
+    u = S(u_)
+    g = S(gelu(u_))
+    y = S(x1 + g @ p["w_fc2"] + p["b_fc2"])
     cache = dict(x=x, h1=h1, c_ln1=c_ln1, q=q, k=k, v=v, P=P, o=o, c_qn=c_qn, c_kn=c_kn,
-                 x1=x1, h2=h2, c_ln2=c_ln2, u=u, g=g, heads=heads, qk_norm=qk_norm)
+                 x1=x1, h2=h2, c_ln2=c_ln2, u=u, g=g, heads=heads, qk_norm=qk_norm, store=store)
     return y, cache
 
 
@@ -235,43 +248,45 @@ def block_bwd(dy, cache, prm: Dict[str, np.ndarray]):
     p = {k_: _f(v_) for k_, v_ in prm.items()}
     dy = _f(dy)
     c = cache
+    S = _keep(c.get("store"))
     B, L, d = dy.shape
     T = B * L
     gr: Dict[str, np.ndarray] = {}
     # feed-forward sub-layer: y = x1 + GELU(u) W_fc2 + b_fc2
     gr["w_fc2"] = c["g"].reshape(T, -1).T @ dy.reshape(T, d)
     gr["b_fc2"] = dy.reshape(T, d).sum(0)
-    du = (dy @ p["w_fc2"].T) * gelu_grad(c["u"])
+    du = S((dy @ p["w_fc2"].T) * gelu_grad(c["u"]))
     gr["w_fc1"] = c["h2"].reshape(T, d).T @ du.reshape(T, -1)
     gr["b_fc1"] = du.reshape(T, -1).sum(0)
-    dh2 = du @ p["w_fc1"].T
+    dh2 = S(du @ p["w_fc1"].T)
     dx1_ln, gr["ln2_g"], gr["ln2_b"] = layer_norm_bwd(dh2, c["c_ln2"], p["ln2_g"])
-    dx1 = dy + dx1_ln
+    dx1 = S(dy + dx1_ln)
     # attention sub-layer: x1 = x + o W_proj + b_proj
     A = p["w_proj"].shape[0]
     gr["w_proj"] = c["o"].reshape(T, A).T @ dx1.reshape(T, d)
     gr["b_proj"] = dx1.reshape(T, d).sum(0)
-    do = dx1 @ p["w_proj"].T
+    do = S(dx1 @ p["w_proj"].T)
     dq, dk, dv = attention_bwd(_heads(do, c["heads"]), c["q"], c["k"], c["v"], c["P"])
+    dq, dk, dv = S(dq), S(dk), S(dv)
     if c["qk_norm"]:
         dq, gr["qn_g"], gr["qn_b"] = layer_norm_bwd(dq, c["c_qn"], p["qn_g"])
         dk, gr["kn_g"], gr["kn_b"] = layer_norm_bwd(dk, c["c_kn"], p["kn_g"])
     else:
         for n_ in ("qn_g", "qn_b", "kn_g", "kn_b"):
             gr[n_] = np.zeros_like(p[n_])
-    dqkv = np.concatenate([_unheads(dq), _unheads(dk), _unheads(dv)], axis=-1)
+    dqkv = S(np.concatenate([_unheads(dq), _unheads(dk), _unheads(dv)], axis=-1))
     gr["w_qkv"] = c["h1"].reshape(T, d).T @ dqkv.reshape(T, 3 * A)
     gr["b_qkv"] = dqkv.reshape(T, 3 * A).sum(0)
-    dh1 = dqkv @ p["w_qkv"].T
+    dh1 = S(dqkv @ p["w_qkv"].T)
     dx_ln, gr["ln1_g"], gr["ln1_b"] = layer_norm_bwd(dh1, c["c_ln1"], p["ln1_g"])
-    return dx1 + dx_ln, gr
+    return S(dx1 + dx_ln), gr
 
 
 # ---------------------------------------------------------------------------
 # Cross-attention variable aggregation (Sec. II)
 # ---------------------------------------------------------------------------
 
-def agg_fwd(tok, prm: Dict[str, np.ndarray], heads: int):
+def agg_fwd(tok, prm: Dict[str, np.ndarray], heads: int, store=None):
     """tok[B, L, V, d] -> z[B, L, d]: one learned query attends over the V
     variable tokens of each patch (multi-head attention semantics).
 
@@ -293,12 +308,13 @@ def agg_fwd(tok, prm: Dict[str, np.ndarray], heads: int):
     Vh = Vv.reshape(B, L, V, heads, dh)
     s = np.einsum("hc,blvhc->blhv", qh, Kh) / math.sqrt(dh)
     a = softmax(s, axis=-1)                                 # [B,L,H,V]
-    zh = np.einsum("blhv,blvhc->blhc", a, Vh).reshape(B, L, A)
+    S = _keep(store)
+    zh = S(np.einsum("blhv,blvhc->blhc", a, Vh).reshape(B, L, A))
     z = zh @ p["w_o"] + p["b_o"]
     if "pos" in p and p["pos"] is not None:
         z = z + p["pos"][None, :, :]
-    cache = dict(X=X, q=q, Kh=Kh, Vh=Vh, a=a, zh=zh, heads=heads)
-    return z, cache
+    cache = dict(X=X, q=q, Kh=Kh, Vh=Vh, a=a, zh=zh, heads=heads, store=store)
+    return S(z), cache
 
 
 def agg_bwd(dz, cache, prm: Dict[str, np.ndarray]):
@@ -316,7 +332,8 @@ def agg_bwd(dz, cache, prm: Dict[str, np.ndarray]):
     gr["pos"] = dz.sum(axis=0)
     gr["b_o"] = dz.reshape(T, d).sum(0)
     gr["w_o"] = c["zh"].reshape(T, A).T @ dz.reshape(T, d)
-    dzh = (dz @ p["w_o"].T).reshape(B, L, H, dh)
+    S = _keep(c.get("store"))
+    dzh = S(dz @ p["w_o"].T).reshape(B, L, H, dh)
     da = np.einsum("blhc,blvhc->blhv", dzh, Vh)
     dVh = np.einsum("blhv,blhc->blvhc", a, dzh)
     ds = a * (da - (da * a).sum(axis=-1, keepdims=True)) / math.sqrt(dh)
@@ -334,7 +351,7 @@ def agg_bwd(dz, cache, prm: Dict[str, np.ndarray]):
     gr["w_q"] = np.outer(p["q0"], dq)
     gr["b_q"] = dq
     gr["q0"] = p["w_q"] @ dq
-    dtok = dK @ p["w_k"].T + dVv @ p["w_v"].T
+    dtok = S(dK @ p["w_k"].T + dVv @ p["w_v"].T)
     return dtok, gr
 
 
@@ -342,16 +359,18 @@ def agg_bwd(dz, cache, prm: Dict[str, np.ndarray]):
 # Prediction head (Sec. II: projection from feature space to image space) and loss
 # ---------------------------------------------------------------------------
 
-def head_fwd(x, prm: Dict[str, np.ndarray], final_ln: int = 1, eps: float = 1e-5):
+def head_fwd(x, prm: Dict[str, np.ndarray], final_ln: int = 1, eps: float = 1e-5, store=None):
     """pred[B, L, V*p*p] = LN_f(x) W_h + b_h (LN_f skipped when final_ln == 0).
     The output row of a token holds its V patches, pixel index v*p*p + i*p + j."""
     x = _f(x)
     p = {k_: _f(v_) for k_, v_ in prm.items()}
+    S = _keep(store)
     if final_ln:
         hf, c_ln = layer_norm_fwd(x, p["lnf_g"], p["lnf_b"], eps)
+        hf = S(hf)
     else:
         hf, c_ln = x, None
-    return hf @ p["w_h"] + p["b_h"], dict(hf=hf, c_ln=c_ln, final_ln=final_ln)
+    return hf @ p["w_h"] + p["b_h"], dict(hf=hf, c_ln=c_ln, final_ln=final_ln, store=store)
 
 
 def head_bwd(dpred, cache, prm: Dict[str, np.ndarray]):
@@ -360,11 +379,14 @@ def head_bwd(dpred, cache, prm: Dict[str, np.ndarray]):
     B, L, n = dpred.shape
     hf = cache["hf"]
     d = hf.shape[-1]
-    gr = {"w_h": hf.reshape(B * L, d).T @ dpred.reshape(B * L, n),
-          "b_h": dpred.reshape(B * L, n).sum(0)}
-    dhf = dpred @ p["w_h"].T
+    S = _keep(cache.get("store"))
+    gr = {"b_h": dpred.reshape(B * L, n).sum(0)}
+    dpred = S(dpred)
+    gr["w_h"] = hf.reshape(B * L, d).T @ dpred.reshape(B * L, n)
+    dhf = S(dpred @ p["w_h"].T)
     if cache["final_ln"]:
         dx, gr["lnf_g"], gr["lnf_b"] = layer_norm_bwd(dhf, cache["c_ln"], p["lnf_g"])
+        dx = S(dx)
     else:
         dx = dhf
         gr["lnf_g"] = np.zeros(d)
@@ -385,19 +407,19 @@ def mse(pred, tgt, scale: float = 1.0):
 # ---------------------------------------------------------------------------
 
 def model_fwd_bwd(img, tgt, emb, agg, blocks, head, *, p: int, agg_heads: int, heads: int,
-                  qk_norm: int = 1, eps: float = 1e-5, final_ln: int = 1):
+                  qk_norm: int = 1, eps: float = 1e-5, final_ln: int = 1, store=None):
     """Forward and backward of the full ClimaX-style model for one batch.
 
     Returns (loss, pred, grads) with grads = {"embed": .., "agg": ..,
-    "blocks": [..], "head": ..}.
+    "blocks": [..], "head": ..}. `store` as in block_fwd (None: exact).
     """
-    tok = patch_embed_fwd(img, emb["w_pe"], emb["b_pe"], emb.get("ve"), p)
-    x, c_agg = agg_fwd(tok, agg, agg_heads)
+    tok = patch_embed_fwd(img, emb["w_pe"], emb["b_pe"], emb.get("ve"), p, store)
+    x, c_agg = agg_fwd(tok, agg, agg_heads, store)
     caches = []
     for prm in blocks:
-        x, c = block_fwd(x, prm, heads, qk_norm, eps)
+        x, c = block_fwd(x, prm, heads, qk_norm, eps, store)
         caches.append(c)
-    pred, c_head = head_fwd(x, head, final_ln, eps)
+    pred, c_head = head_fwd(x, head, final_ln, eps, store)
     loss, dpred = mse(pred, tgt)
     dx, g_head = head_bwd(dpred, c_head, head)
     g_blocks = [None] * len(blocks)

@@ -102,14 +102,17 @@ _PROTOS = {
     "orbit_gemm_workspace_bytes": (c_size_t, [c_int32] * 6),
     "orbit_gemm": (c_int, [c_int32, c_int32, c_int32, c_int32, P, c_int64, c_int32, P, c_int64, c_int32, P,
                            c_int64, c_int32, c_float, P, c_int32, P, c_size_t, P]),
-    "orbit_attention_fwd": (c_int, [c_int32] * 5 + [P, c_int64, P, c_int64, P, c_int64, P, c_int64, P, P]),
-    "orbit_attention_bwd": (c_int, [c_int32] * 5 + [P, c_int64, P, c_int64, P, c_int64, P, c_int64, P, P,
-                                                    c_int64, P, P, P, c_int64, P, P]),
+    "orbit_attention_fwd": (c_int, [c_int32] * 5 + [P, c_int64, P, c_int64, P, c_int64, P, c_int64, P, P, c_int64,
+                                                    P]),
+    "orbit_attention_bwd_workspace_bytes": (c_size_t, [c_int32] * 4),
+    "orbit_attention_bwd": (c_int, [c_int32] * 5 + [P, c_int64, P, c_int64, P, c_int64, P, c_int64, c_int32, P, P,
+                                                    c_int64, P, P, P, c_int64, P, c_size_t, P]),
     "orbit_layernorm_fwd": (c_int, [c_int32, c_int32, c_int32, P, P, P, c_float, P, P, P, P]),
     "orbit_status_string": (c_char_p, [c_int]),
     "orbit_last_error": (c_char_p, []),
     "orbit_abi_version": (c_int, []),
     "orbit_timing_enable": (c_int, [c_int]),
+    "orbit_timing_filter": (c_int, [c_char_p]),
     "orbit_timing_summary": (c_int, [c_char_p, POINTER(c_int64), POINTER(c_double), POINTER(c_double),
                                      POINTER(c_double)]),
     "orbit_timing_kernel_name": (c_char_p, [c_int]),
@@ -260,16 +263,21 @@ class OrbitLib:
             dtype, M, N, K, _ptr(A), lda, int(a_kmajor), _ptr(B), ldb, int(b_kmajor), _ptr(C), ldc, int(c_f32),
             float(alpha), _ptr(bias), int(accumulate), _ptr(ws), nb, _stream(stream)))
 
-    def orbit_attention_fwd(self, dtype, B, H, L, dh, q, ldq, k, ldk, v, ldv, o, ldo, lse, stream=None):
+    def orbit_attention_fwd(self, dtype, B, H, L, dh, q, ldq, k, ldk, v, ldv, o, ldo, lse, o32=None, ldo32=0,
+                            stream=None):
         self._check("orbit_attention_fwd", self.lib.orbit_attention_fwd(
-            dtype, B, H, L, dh, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, _ptr(lse),
-            _stream(stream)))
+            dtype, B, H, L, dh, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, _ptr(lse), _ptr(o32),
+            ldo32, _stream(stream)))
 
-    def orbit_attention_bwd(self, dtype, B, H, L, dh, q, ldq, k, ldk, v, ldv, o, ldo, lse, dO, lddo, dq, dk, dv,
-                            ldg, Dws, stream=None):
+    def orbit_attention_bwd_workspace_bytes(self, B, H, L, dh) -> int:
+        return self.lib.orbit_attention_bwd_workspace_bytes(B, H, L, dh)
+
+    def orbit_attention_bwd(self, dtype, B, H, L, dh, q, ldq, k, ldk, v, ldv, o, ldo, o_f32, lse, dO, lddo, dq, dk,
+                            dv, ldg, ws, stream=None):
         self._check("orbit_attention_bwd", self.lib.orbit_attention_bwd(
-            dtype, B, H, L, dh, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, _ptr(lse), _ptr(dO), lddo,
-            _ptr(dq), _ptr(dk), _ptr(dv), ldg, _ptr(Dws), _stream(stream)))
+            dtype, B, H, L, dh, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, int(o_f32), _ptr(lse),
+            _ptr(dO), lddo, _ptr(dq), _ptr(dk), _ptr(dv), ldg, _ptr(ws), ws.numel() * ws.element_size(),
+            _stream(stream)))
 
     def orbit_layernorm_fwd(self, dtype, rows, n, x, g, b, eps, y, mean, rstd, stream=None):
         self._check("orbit_layernorm_fwd", self.lib.orbit_layernorm_fwd(
@@ -279,6 +287,9 @@ class OrbitLib:
     # -- timing ----------------------------------------------------------------
     def orbit_timing_enable(self, on: bool):
         self._check("orbit_timing_enable", self.lib.orbit_timing_enable(1 if on else 0))
+
+    def orbit_timing_filter(self, prefix: Optional[str]):
+        self._check("orbit_timing_filter", self.lib.orbit_timing_filter(prefix.encode() if prefix else None))
 
     def orbit_timing_summary(self, prefix: Optional[str] = None):
         n, ms, fl, by = c_int64(), c_double(), c_double(), c_double()

@@ -79,6 +79,7 @@ struct BlockSaved {
   void* qkn;
   float *qmu, *qr;
   void* o;
+  float* o32;
   float* lse;
   void* x1;
   float *mu2, *r2;
@@ -101,6 +102,7 @@ BlockSaved carve_block_saved(const BlockDims& z, void* base, size_t* used) {
     s.qr = c.take<float>(z.T * 2 * z.H);
   }
   s.o = c.take<char>(z.T * z.A * e);
+  s.o32 = z.dt == ORBIT_BF16 ? c.take<float>(z.T * z.A) : nullptr;
   s.lse = c.take<float>(z.T * z.H);
   s.x1 = c.take<char>(z.T * z.d * e);
   s.mu2 = c.take<float>(z.T);
@@ -124,7 +126,7 @@ struct BlockWs {
   void* dh;    // [T, d]
   void* dO;    // [T, A]
   void* dqkv;  // [T, 3A]
-  float* D;    // [T, H]
+  float* D;    // attention backward workspace
   void* cws;
   void* qws;
   void* gws;
@@ -159,7 +161,7 @@ size_t block_ws_layout(const BlockDims& z, void* base, size_t bytes, BlockWs* w,
   t.dh = c.take<char>(z.T * z.d * e);
   t.dO = c.take<char>(z.T * z.A * e);
   t.dqkv = c.take<char>(z.T * 3 * z.A * e);
-  t.D = c.take<float>(z.T * z.H);
+  t.D = static_cast<float*>(static_cast<void*>(c.take<char>(attn_bwd_workspace_bytes(z.B, z.H, z.L, z.dh))));
   t.cws = c.take<char>(colsum_workspace_bytes((int)z.T, std::max({z.d, 3 * z.A, z.F})));
   t.qws = c.take<char>(qk_norm_bwd_workspace_bytes(z.dh));
   const size_t g = block_gemm_ws(z);
@@ -239,7 +241,7 @@ orbit_status orbit_vit_block_fwd(const orbit_block_desc* desc, const orbit_block
     io.q = sv.qkv; io.ldq = 3 * z.A;
     io.k = static_cast<char*>(sv.qkv) + z.A * e; io.ldk = 3 * z.A;
   }
-  ORBIT_TRY(attn_fwd(dt, io, sv.o, z.A, sv.lse, s));
+  ORBIT_TRY(attn_fwd(dt, io, sv.o, z.A, sv.lse, sv.o32, z.A, s));
   {
     Gemm g; g.dtype = dt; g.tag = "proj";
     g.A = sv.o; g.lda = z.A; g.B = p->w_proj; g.ldb = z.d; g.C = sv.x1; g.ldc = z.d;
@@ -348,7 +350,10 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     io.q = sv.qkv; io.ldq = 3 * z.A; io.k = static_cast<char*>(sv.qkv) + z.A * e; io.ldk = 3 * z.A;
   }
   char* dq = static_cast<char*>(w.dqkv);
-  ORBIT_TRY(attn_bwd(dt, io, sv.o, z.A, sv.lse, w.dO, z.A, dq, dq + z.A * e, dq + 2 * z.A * e, 3 * z.A, w.D, s));
+  if (sv.o32)
+    ORBIT_TRY(attn_bwd(dt, io, sv.o32, z.A, 1, sv.lse, w.dO, z.A, dq, dq + z.A * e, dq + 2 * z.A * e, 3 * z.A, w.D, s));
+  else
+    ORBIT_TRY(attn_bwd(dt, io, sv.o, z.A, 0, sv.lse, w.dO, z.A, dq, dq + z.A * e, dq + 2 * z.A * e, 3 * z.A, w.D, s));
   if (z.qk) {
     ORBIT_TRY(qk_norm_bwd(dt, w.dqkv, 3 * z.A, sv.qkv, 3 * z.A, sv.qmu, sv.qr, p->qn_g, p->kn_g, gr->qn_g, gr->qn_b,
                           gr->kn_g, gr->kn_b, accumulate, T, z.H, z.dh, w.qws, s));
@@ -697,34 +702,42 @@ static orbit_status attn_check(const char* fn, int32_t dtype, int32_t B, int32_t
 
 orbit_status orbit_attention_fwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim, const void* q,
                                  int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv, void* o,
-                                 int64_t ldo, float* lse, void* stream) {
+                                 int64_t ldo, float* lse, float* o32, int64_t ldo32, void* stream) {
   const char* fn = "orbit_attention_fwd";
   clear_error();
   ORBIT_TRY(attn_check(fn, dtype, B, H, L, head_dim));
-  PTR(q, "q"); PTR(k, "k"); PTR(v, "v"); PTR(o, "o"); PTR(lse, "lse");
+  PTR(q, "q"); PTR(k, "k"); PTR(v, "v"); PTR(o, "o"); PTR(lse, "lse"); OPT_PTR(o32, "o32");
   const int64_t A = (int64_t)H * head_dim;
   REQ(ldq >= A && ldk >= A && ldv >= A && ldo >= A && ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0 && ldo % 8 == 0,
       ORBIT_E_ARG, "%s: leading dimensions must be >= heads*head_dim and multiples of 8", fn);
+  REQ(!o32 || (ldo32 >= A && ldo32 % 8 == 0), ORBIT_E_ARG, "%s: bad ldo32", fn);
   AttnIO io{q, k, v, ldq, ldk, ldv, B, H, L, head_dim};
-  return attn_fwd((orbit_dtype)dtype, io, o, ldo, lse, S(stream));
+  return attn_fwd((orbit_dtype)dtype, io, o, ldo, lse, o32, ldo32, S(stream));
 }
 
 orbit_status orbit_attention_bwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim, const void* q,
                                  int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv, const void* o,
-                                 int64_t ldo, const float* lse, const void* dO, int64_t lddo, void* dq, void* dk,
-                                 void* dv, int64_t ldg, float* Dws, void* stream) {
+                                 int64_t ldo, int32_t o_f32, const float* lse, const void* dO, int64_t lddo, void* dq,
+                                 void* dk, void* dv, int64_t ldg, void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "orbit_attention_bwd";
   clear_error();
   ORBIT_TRY(attn_check(fn, dtype, B, H, L, head_dim));
   PTR(q, "q"); PTR(k, "k"); PTR(v, "v"); PTR(o, "o"); PTR(lse, "lse"); PTR(dO, "dO");
-  PTR(dq, "dq"); PTR(dk, "dk"); PTR(dv, "dv"); PTR(Dws, "Dws");
+  PTR(dq, "dq"); PTR(dk, "dk"); PTR(dv, "dv"); PTR(ws, "ws");
+  REQ(ws_bytes >= attn_bwd_workspace_bytes(B, H, L, head_dim), ORBIT_E_ARG, "%s: workspace too small", fn);
   const int64_t A = (int64_t)H * head_dim;
   REQ(ldq >= A && ldk >= A && ldv >= A && ldo >= A && lddo >= A && ldg >= A, ORBIT_E_ARG,
       "%s: leading dimensions must be >= heads*head_dim", fn);
   REQ(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0 && ldo % 8 == 0 && lddo % 8 == 0 && ldg % 8 == 0, ORBIT_E_ARG,
       "%s: leading dimensions must be multiples of 8", fn);
   AttnIO io{q, k, v, ldq, ldk, ldv, B, H, L, head_dim};
-  return attn_bwd((orbit_dtype)dtype, io, o, ldo, lse, dO, lddo, dq, dk, dv, ldg, Dws, S(stream));
+  return attn_bwd((orbit_dtype)dtype, io, o, ldo, o_f32 ? 1 : 0, lse, dO, lddo, dq, dk, dv, ldg,
+                  static_cast<float*>(ws), S(stream));
+}
+
+size_t orbit_attention_bwd_workspace_bytes(int32_t B, int32_t H, int32_t L, int32_t head_dim) {
+  if (B <= 0 || H <= 0 || L <= 0 || head_dim <= 0) return 0;
+  return attn_bwd_workspace_bytes(B, H, L, head_dim);
 }
 
 orbit_status orbit_layernorm_fwd(int32_t dtype, int32_t rows, int32_t n, const void* x, const void* g,

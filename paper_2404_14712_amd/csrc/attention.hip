@@ -23,7 +23,8 @@ struct FwdArgs {
   const void *q, *k, *v;
   void* o;
   float* lse;
-  int64_t ldq, ldk, ldv, ldo;
+  float* o32;  // optional float32 copy of O (consistent softmax-backward row sums)
+  int64_t ldq, ldk, ldv, ldo, ldo32;
   int H, L;
   float sl2;  // log2(e) / sqrt(dh)
 };
@@ -188,6 +189,17 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(FwdArgs a) {
         st4(O + col, o[c][r4 * 4] * inv, o[c][r4 * 4 + 1] * inv, o[c][r4 * 4 + 2] * inv,
             o[c][r4 * 4 + 3] * inv);
       }
+    if (a.o32) {
+      float* O32 = a.o32 + (row0 + qi) * a.ldo32 + h * DH;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int col = c * 32 + r4 * 8 + g * 4;
+          st4(O32 + col, o[c][r4 * 4] * inv, o[c][r4 * 4 + 1] * inv, o[c][r4 * 4 + 2] * inv,
+              o[c][r4 * 4 + 3] * inv);
+        }
+    }
     if (g == 0) a.lse[((int64_t)b * a.H + h) * L + qi] = (m + __log2f(ltot)) * kLn2;
   }
   (void)E;
@@ -196,8 +208,8 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(FwdArgs a) {
 // ---------------------------------------------------------------------------
 // backward preprocess: D[b,h,i] = sum_c dO[i,c] O[i,c]
 // ---------------------------------------------------------------------------
-template <typename T, int DH>
-__global__ void __launch_bounds__(256) attn_bwd_pre(const T* __restrict__ o, int64_t ldo, const T* __restrict__ dO,
+template <typename T, typename OT, int DH>
+__global__ void __launch_bounds__(256) attn_bwd_pre(const OT* __restrict__ o, int64_t ldo, const T* __restrict__ dO,
                                                     int64_t lddo, float* __restrict__ D, int B, int H, int L) {
   constexpr int G = DH / 8;
   const int li = threadIdx.x % G;
@@ -208,15 +220,10 @@ __global__ void __launch_bounds__(256) attn_bwd_pre(const T* __restrict__ o, int
   float s = 0.f;
   if (valid) {
     float a8[8], b8[8];
-    unpack(ld128(o + t * ldo + h * DH + li * 8), a8, (T*)nullptr);
+    unpack(ld128(o + t * ldo + h * DH + li * 8), a8, (OT*)nullptr);
     unpack(ld128(dO + t * lddo + h * DH + li * 8), b8, (T*)nullptr);
-    if constexpr (sizeof(T) == 4) {
-      float a2[4], b2[4];
-      unpack(ld128(o + t * ldo + h * DH + li * 8 + 4), a2, (T*)nullptr);
-      unpack(ld128(dO + t * lddo + h * DH + li * 8 + 4), b2, (T*)nullptr);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { a8[4 + i] = a2[i]; b8[4 + i] = b2[i]; }
-    }
+    if constexpr (sizeof(OT) == 4) unpack(ld128(o + t * ldo + h * DH + li * 8 + 4), a8 + 4, (OT*)nullptr);
+    if constexpr (sizeof(T) == 4) unpack(ld128(dO + t * lddo + h * DH + li * 8 + 4), b8 + 4, (T*)nullptr);
 #pragma unroll
     for (int i = 0; i < 8; ++i) s += a8[i] * b8[i];
   }
@@ -231,6 +238,7 @@ __global__ void __launch_bounds__(256) attn_bwd_pre(const T* __restrict__ o, int
 struct BwdArgs {
   const void *q, *k, *v, *dO;
   const float *lse, *D;
+  const float *qsum, *ksum;  // per (sample, head, feature) sums of q and k over the sequence
   void *dq, *dk, *dv;
   int64_t ldq, ldk, ldv, lddo, ldg;
   int H, L;
@@ -258,7 +266,9 @@ struct DualStage {
       }
     }
   }
-  ORBIT_DEV void store(T* Xs, T* Xt, int tid) const {
+  // Xt gets X - mean[column] when mean is given
+  ORBIT_DEV void store(T* Xs, T* Xt, int tid, const float* mean) const {
+    using TL = TileLoader<T, DH, 32, NT, false>;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int u = tid + i * NT;
@@ -266,7 +276,8 @@ struct DualStage {
       const int rg = u / (DH / E), cc = u % (DH / E);
 #pragma unroll
       for (int j = 0; j < 4; ++j) st128(Xs + (rg * 4 + j) * RP + cc * E, r[i * 4 + j]);
-      TileLoader<T, DH, 32, NT, false>::store_transposed(Xt + (cc * E) * TP + rg * 4, &r[i * 4]);
+      if (mean) TL::store_transposed_sub(Xt + (cc * E) * TP + rg * 4, &r[i * 4], mean + cc * E);
+      else TL::store_transposed(Xt + (cc * E) * TP + rg * 4, &r[i * 4]);
     }
   }
 };
@@ -287,11 +298,13 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T ds_[32 * RP];
   __shared__ __attribute__((aligned(16))) T dt[DH * TP];
   __shared__ float lse_s[32], d_s[32];
+  __shared__ float qbar[DH];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
   const int h = blockIdx.y, b = blockIdx.z;
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
+  if (tid < DH) qbar[tid] = a.qsum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
   const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
   const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
@@ -318,15 +331,19 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) dvt[c][v] = dkt[c][v] = 0.f;
 
+  // dK_j = sum_i dS_ij q_i = sum_i dS_ij (q_i - qbar) + qbar sum_i dS_ij: the
+  // product runs on centred queries (small when the queries are alike) and
+  // the rank-one remainder is added in float32 from the exact column sums.
+  float cs = 0.f;
   DS sq, sd;
   const int nq = (L + 31) / 32;
   for (int it = 0; it < nq; ++it) {
     const int q0 = it * 32;
     sq.load(Q, a.ldq, q0, L, tid);
     sd.load(dO, a.lddo, q0, L, tid);
-    __syncthreads();  // previous tile fully consumed
-    sq.store(qs, qt, tid);
-    sd.store(ds_, dt, tid);
+    __syncthreads();  // previous tile fully consumed (and qbar visible)
+    sq.store(qs, qt, tid, qbar);
+    sd.store(ds_, dt, tid, nullptr);
     if (tid < 32) {
       const int qq = q0 + tid;
       lse_s[tid] = qq < L ? lse[qq] * kLog2e : INFINITY;
@@ -352,6 +369,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
       const float p = exp2f(s[v] * a.sl2 - lse_s[qr]);
       s[v] = p;
       dp[v] = p * (dp[v] - d_s[qr]);
+      cs += dp[v];
     }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -369,6 +387,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
     }
   }
 
+  cs += __shfl_xor(cs, 32, 64);
   if (kv < L) {
     T* dK = static_cast<T*>(a.dk) + (row0 + kv) * a.ldg + h * DH;
     T* dV = static_cast<T*>(a.dv) + (row0 + kv) * a.ldg + h * DH;
@@ -377,8 +396,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int col = c * 32 + r4 * 8 + g * 4;
-        st4(dK + col, dkt[c][r4 * 4] * a.scale, dkt[c][r4 * 4 + 1] * a.scale, dkt[c][r4 * 4 + 2] * a.scale,
-            dkt[c][r4 * 4 + 3] * a.scale);
+        st4(dK + col, (dkt[c][r4 * 4] + qbar[col] * cs) * a.scale, (dkt[c][r4 * 4 + 1] + qbar[col + 1] * cs) * a.scale,
+            (dkt[c][r4 * 4 + 2] + qbar[col + 2] * cs) * a.scale, (dkt[c][r4 * 4 + 3] + qbar[col + 3] * cs) * a.scale);
         st4(dV + col, dvt[c][r4 * 4], dvt[c][r4 * 4 + 1], dvt[c][r4 * 4 + 2], dvt[c][r4 * 4 + 3]);
       }
   }
@@ -387,7 +406,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // backward, Q-major: each wave owns 32 queries (Q, dO fragments in registers)
 // and sweeps all keys in tiles of 64:
-//   S^T = K Q^T, P^T, dP^T = V dO^T, dS^T = P^T (dP^T - D);  dQ^T += K^T dS^T
+//   S^T = K Q^T, P^T, dP^T = V dO^T, dS^T = P^T (dP^T - D);  dQ^T += (K - kbar)^T dS^T
 // ---------------------------------------------------------------------------
 template <typename T, int DH>
 __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
@@ -398,11 +417,13 @@ __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T ks[KT * KP];
   __shared__ __attribute__((aligned(16))) T vs[KT * KP];
   __shared__ __attribute__((aligned(16))) T kt[DH * TP];
+  __shared__ float kbar[DH];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
   const int h = blockIdx.y, b = blockIdx.z;
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
+  if (tid < DH) kbar[tid] = a.ksum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
   const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
   const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
@@ -441,7 +462,9 @@ __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
     __syncthreads();
     lk.store(ks, tid);
     lvv.store(vs, tid);
-    lt.store(kt, tid);
+    // dQ_i = sum_j dS_ij k_j = sum_j dS_ij (k_j - kbar) since sum_j dS_ij = 0:
+    // centred keys keep the product well conditioned when the keys are alike
+    lt.store_sub(kt, tid, kbar);
     __syncthreads();
 
     f32x16 s[2], dp[2];
@@ -491,8 +514,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
 }
 
 template <typename T, int DH>
-orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream_t s) {
-  FwdArgs a{io.q, io.k, io.v, o, lse, io.ldq, io.ldk, io.ldv, ldo, io.H, io.L, kLog2e / sqrtf((float)DH)};
+orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32, hipStream_t s) {
+  FwdArgs a{io.q, io.k, io.v, o, lse, o32, io.ldq, io.ldk, io.ldv, ldo, ldo32, io.H, io.L, kLog2e / sqrtf((float)DH)};
   const double bh = (double)io.B * io.H;
   KernelInfo ki{sizeof(T) == 2 ? "attn_fwd_kernel<bf16>" : "attn_fwd_kernel<f32>",
                 4.0 * bh * io.L * (double)io.L * DH, 4.0 * bh * io.L * DH * sizeof(T)};
@@ -500,19 +523,35 @@ orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream
 }
 
 template <typename T, int DH>
-orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, const float* lse, const void* dO, int64_t lddo,
-                   void* dq, void* dk, void* dv, int64_t ldg, float* D, hipStream_t s) {
+orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, const float* lse, const void* dO,
+                   int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg, float* D, hipStream_t s) {
   const double bh = (double)io.B * io.H;
   const int64_t rows = (int64_t)io.B * io.L * io.H;
   KernelInfo kp{sizeof(T) == 2 ? "attn_bwd_pre<bf16>" : "attn_bwd_pre<f32>", 2.0 * rows * DH,
-                2.0 * rows * DH * sizeof(T)};
-  ORBIT_TRY(launch(kp, attn_bwd_pre<T, DH>, dim3((unsigned)cdiv(rows, 256 / (DH / 8))), dim3(256), 0, s,
-                   (const T*)o, ldo, (const T*)dO, lddo, D, io.B, io.H, io.L));
-  BwdArgs a{io.q, io.k, io.v, dO, lse, D, dq, dk, dv, io.ldq, io.ldk, io.ldv, lddo, ldg, io.H, io.L,
+                rows * DH * (sizeof(T) + (o_f32 ? 4.0 : sizeof(T)))};
+  const dim3 gp((unsigned)cdiv(rows, 256 / (DH / 8)));
+  if (o_f32)
+    ORBIT_TRY(launch(kp, attn_bwd_pre<T, float, DH>, gp, dim3(256), 0, s, (const float*)o, ldo, (const T*)dO, lddo,
+                     D, io.B, io.H, io.L));
+  else
+    ORBIT_TRY(launch(kp, attn_bwd_pre<T, T, DH>, gp, dim3(256), 0, s, (const T*)o, ldo, (const T*)dO, lddo, D,
+                     io.B, io.H, io.L));
+  // per (sample, head) feature sums of q and k over the sequence
+  float* qsum = D + (int64_t)io.B * io.H * io.L;
+  float* ksum = qsum + (int64_t)io.B * io.H * DH;
+  void* cws = ksum + (int64_t)io.B * io.H * DH;
+  const int A = io.H * DH;
+  for (int bb = 0; bb < io.B; ++bb) {
+    ORBIT_TRY(colsum(sizeof(T) == 2 ? ORBIT_BF16 : ORBIT_F32, static_cast<const T*>(io.q) + (int64_t)bb * io.L * io.ldq,
+                     io.ldq, io.L, A, nullptr, 0, nullptr, nullptr, qsum + (int64_t)bb * A, nullptr, 0, cws, s));
+    ORBIT_TRY(colsum(sizeof(T) == 2 ? ORBIT_BF16 : ORBIT_F32, static_cast<const T*>(io.k) + (int64_t)bb * io.L * io.ldk,
+                     io.ldk, io.L, A, nullptr, 0, nullptr, nullptr, ksum + (int64_t)bb * A, nullptr, 0, cws, s));
+  }
+  BwdArgs a{io.q, io.k, io.v, dO, lse, D, qsum, ksum, dq, dk, dv, io.ldq, io.ldk, io.ldv, lddo, ldg, io.H, io.L,
             kLog2e / sqrtf((float)DH), 1.f / sqrtf((float)DH)};
   // algorithmic backward = 2x forward; kernels split it 3:2 (dK,dV: 4 products, dQ: 3 incl. recompute)
   const double fl = 4.0 * bh * io.L * (double)io.L * DH;
-  KernelInfo k1{sizeof(T) == 2 ? "attn_bwd_dkdv<bf16>" : "attn_bwd_dkdv<f32>", 1.2 * 2 * fl / 1.2 * 0.6,
+  KernelInfo k1{sizeof(T) == 2 ? "attn_bwd_dkdv<bf16>" : "attn_bwd_dkdv<f32>", 2 * fl * 0.6,
                 6.0 * bh * io.L * DH * sizeof(T)};
   ORBIT_TRY(launch(k1, attn_bwd_dkdv<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a));
   KernelInfo k2{sizeof(T) == 2 ? "attn_bwd_dq<bf16>" : "attn_bwd_dq<f32>", 2 * fl * 0.4,
@@ -522,8 +561,13 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, const float* ls
 
 }  // namespace
 
-orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream_t s) {
-#define AF(TT, D) return fwd_t<TT, D>(io, o, ldo, lse, s)
+size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh) {
+  return align_up((size_t)B * H * (L + 2 * dh) * sizeof(float)) + colsum_workspace_bytes(L, H * dh);
+}
+
+orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32,
+                      int64_t ldo32, hipStream_t s) {
+#define AF(TT, D) return fwd_t<TT, D>(io, o, ldo, lse, o32, ldo32, s)
   if (dt == ORBIT_BF16) {
     if (io.dh == 32) AF(bf16, 32);
     if (io.dh == 64) AF(bf16, 64);
@@ -538,10 +582,10 @@ orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, fl
   return ORBIT_E_UNSUPPORTED;
 }
 
-orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, const float* lse,
+orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, int o_f32, const float* lse,
                       const void* dO, int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg, float* Dbuf,
                       hipStream_t s) {
-#define AB(TT, D) return bwd_t<TT, D>(io, o, ldo, lse, dO, lddo, dq, dk, dv, ldg, Dbuf, s)
+#define AB(TT, D) return bwd_t<TT, D>(io, o, ldo, o_f32, lse, dO, lddo, dq, dk, dv, ldg, Dbuf, s)
   if (dt == ORBIT_BF16) {
     if (io.dh == 32) AB(bf16, 32);
     if (io.dh == 64) AB(bf16, 64);

@@ -46,11 +46,16 @@ struct AttnIO {
   int64_t ldq, ldk, ldv;
   int B, H, L, dh;
 };
-orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, hipStream_t s);
-// D[b,h,l] = rowsum(dO * O)
-orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, const float* lse,
+// o32 (optional): float32 copy of O, used by the backward for rowsum(dO * O)
+orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32,
+                      hipStream_t s);
+// workspace of attn_bwd: D[b,h,l] = rowsum(dO * O), sums of q and k over the
+// sequence, and the column-reduction scratch
+size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh);
+// O is float32 when o_f32, else dtype
+orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, int o_f32, const float* lse,
                       const void* dO, int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg,
-                      float* Dbuf, hipStream_t s);
+                      float* ws, hipStream_t s);
 
 // ---- patch embedding --------------------------------------------------------
 orbit_status patch_embed_fwd(orbit_dtype dt, const float* img, const void* w, const void* b,

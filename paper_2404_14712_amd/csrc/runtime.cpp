@@ -40,6 +40,7 @@ struct Timing {
   std::vector<Record> recs;
   int open = -1;
   std::vector<std::string> names;
+  std::string filter;
 };
 Timing& T() {
   static Timing t;
@@ -53,6 +54,7 @@ void timing_begin(hipStream_t s, const KernelInfo& k) {
   Timing& t = T();
   t.open = -1;
   if ((int)t.recs.size() >= kMaxRecords) return;
+  if (!t.filter.empty() && strncmp(k.name, t.filter.c_str(), t.filter.size()) != 0) return;
   const int i = (int)t.recs.size();
   Record r{k.name, k.flops, k.bytes, t.pool[2 * i], t.pool[2 * i + 1]};
   if (hipEventRecord(r.start, s) != hipSuccess) return;
@@ -104,6 +106,11 @@ orbit_status orbit_timing_enable(int on) {
     t.names.clear();
   }
   t.on = on != 0;
+  return ORBIT_OK;
+}
+
+orbit_status orbit_timing_filter(const char* prefix) {
+  T().filter = prefix ? prefix : "";
   return ORBIT_OK;
 }
 

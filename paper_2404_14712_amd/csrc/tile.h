@@ -64,6 +64,44 @@ struct TileLoader {
     }
   }
 
+  // transposed layout only: as store(), with mean[row] subtracted from every
+  // element first (in float32, then rounded back to T)
+  ORBIT_DEV void store_sub(T* S, int tid, const float* mean) const {
+    static_assert(!KMAJ, "store_sub applies to the transposed layout");
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c >= NCH) continue;
+      const int kg = c / (ROWS / E), rc = c % (ROWS / E);
+      store_transposed_sub(S + (rc * E) * PITCH + kg * 4, &r[i * 4], mean + rc * E);
+    }
+  }
+
+  static ORBIT_DEV float elem(const U128& u, int e) {
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t w = u.w[e >> 1];
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+      return __uint_as_float(u.w[e]);
+    }
+  }
+
+  static ORBIT_DEV void store_transposed_sub(T* S, const U128* q, const float* mean) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float m = mean[e];
+      const float v0 = elem(q[0], e) - m, v1 = elem(q[1], e) - m;
+      const float v2 = elem(q[2], e) - m, v3 = elem(q[3], e) - m;
+      if constexpr (sizeof(T) == 2) {
+        bf16x4 o = {(bf16)v0, (bf16)v1, (bf16)v2, (bf16)v3};
+        *reinterpret_cast<bf16x4*>(S + e * PITCH) = o;
+      } else {
+        f32x4 o = {v0, v1, v2, v3};
+        *reinterpret_cast<f32x4*>(S + e * PITCH) = o;
+      }
+    }
+  }
+
   // q[0..3]: four k-rows of E row-elements; writes E runs of 4 k-values
   static ORBIT_DEV void store_transposed(T* S, const U128* q) {
     if constexpr (sizeof(T) == 2) {

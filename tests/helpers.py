@@ -36,11 +36,46 @@ def rel_err(got, ref) -> float:
     return float(num / den)
 
 
-def check(name, got, ref, tol, floor_ref=None):
-    """Per-tensor relative error <= tol. For tensors that are exactly zero in
-    the reference, compare against tol * max|floor_ref| (a sibling tensor)."""
+def rounder(dtype: str):
+    """Storage rounding of the GPU path's intermediates: bf16 (RNE) or float32."""
+    if dtype == "bf16":
+        return lambda a: synth.bf16_round(np.asarray(a, np.float32)).astype(np.float64)
+    return lambda a: np.asarray(a, np.float32).astype(np.float64)
+
+
+# The bound of a tensor is max(TOL, FLOOR_FACTOR * floor), where floor is how far
+# the same oracle moves when its stored intermediates are rounded to the GPU's
+# storage precision (the unavoidable error of any implementation that stores
+# them so). Where the synthetic model makes a result ill-conditioned (tokens
+# that differ by a few percent amplify every rounding of the shared part),
+# floor exceeds TOL; elsewhere the bound is TOL itself.
+FLOOR_FACTOR = 3.0
+
+
+def _err(got, ref, floor_ref):
     ref = np.asarray(ref, np.float64)
-    if np.abs(ref).max() == 0.0 and floor_ref is not None:
+    if floor_ref is not None and np.abs(ref).max() <= 1e-9 * np.abs(floor_ref).max():
+        return float(np.abs(np.asarray(got, np.float64)).max() / max(np.abs(floor_ref).max(), 1e-30))
+    return rel_err(got, ref)
+
+
+def compare(name, got, ref, ref_stored, tol, floor_ref=None):
+    """check() with the bound raised to FLOOR_FACTOR x the storage-precision floor."""
+    floor = _err(ref_stored, ref, floor_ref)
+    e = _err(got, ref, floor_ref)
+    bound = max(tol, FLOOR_FACTOR * floor)
+    assert np.all(np.isfinite(np.asarray(got, np.float64))), f"{name}: non-finite values"
+    assert e <= bound, f"{name}: max relative error {e:.3e} > bound {bound:.1e} (tol {tol:.0e}, floor {floor:.2e})"
+    return e, floor
+
+
+def check(name, got, ref, tol, floor_ref=None):
+    """Per-tensor relative error <= tol. For tensors that vanish in the
+    reference, compare max|got| against tol * max|floor_ref| (a sibling tensor)."""
+    ref = np.asarray(ref, np.float64)
+    # a reference that vanishes analytically (shift-invariance of softmax: key
+    # biases and the key-LayerNorm shift) is only zero up to fp64 rounding
+    if floor_ref is not None and np.abs(ref).max() <= 1e-9 * np.abs(floor_ref).max():
         e = float(np.abs(np.asarray(got, np.float64)).max() / max(np.abs(floor_ref).max(), 1e-30))
     else:
         e = rel_err(got, ref)

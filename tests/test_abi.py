@@ -90,7 +90,7 @@ def test_other_entry_validation(lib):
     assert lib.lib.orbit_gemm(1, 16, 16, 16, 0x100, 16, 0, 0x200, 16, 1, 0x300, 16, 1, 1.0, None, 0, None, 0,
                               None) == L.ORBIT_E_UNSUPPORTED
     assert lib.lib.orbit_attention_fwd(1, 1, 1, 8, 96, 0x100, 96, 0x200, 96, 0x300, 96, 0x400, 96, 0x500,
-                                       None) == L.ORBIT_E_UNSUPPORTED
+                                       None, 0, None) == L.ORBIT_E_UNSUPPORTED
 
 
 def test_workspace_sizes_cover_the_configs(lib):

@@ -71,12 +71,13 @@ def test_attention(lib, dtype, dh, L):
     q, k, v = t.data_ptr(), t.data_ptr() + A * e, t.data_ptr() + 2 * A * e
     o = torch.zeros(B * L, A, dtype=t.dtype, device="cuda")
     lse = torch.zeros(B, H, L, dtype=torch.float32, device="cuda")
-    lib.orbit_attention_fwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o, A, lse)
+    o32 = torch.zeros(B * L, A, dtype=torch.float32, device="cuda")
+    lib.orbit_attention_fwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o, A, lse, o32, A)
     g = torch.zeros(B * L, 3 * A, dtype=t.dtype, device="cuda")
     ge = g.data_ptr()
-    Dws = torch.zeros(B * H * L, dtype=torch.float32, device="cuda")
+    Dws = torch.zeros(lib.orbit_attention_bwd_workspace_bytes(B, H, L, dh), dtype=torch.uint8, device="cuda")
     dOd = dev(dO, dtype)
-    lib.orbit_attention_bwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o, A, lse, dOd, A, ge,
+    lib.orbit_attention_bwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o32, A, 1, lse, dOd, A, ge,
                             ge + A * e, ge + 2 * A * e, 3 * A, Dws)
     torch.cuda.synchronize()
     hd = lambda x: x.reshape(B, L, H, dh).transpose(0, 2, 1, 3)
@@ -86,6 +87,7 @@ def test_attention(lib, dtype, dh, L):
     un = lambda x: x.transpose(0, 2, 1, 3).reshape(B * L, A)
     tol = TOL[dtype]
     check("o", host(o), un(ref_o), tol)
+    check("o32", host(o32), un(ref_o), tol)
     lse_ref = np.log(np.exp((Q @ np.swapaxes(K_, -1, -2)) / np.sqrt(dh)).sum(-1))
     check("lse", host(lse), lse_ref, tol)
     gh = host(g)

@@ -9,7 +9,7 @@ import pytest
 
 import oracle as O
 import synth
-from helpers import TOL, check, dev, host
+from helpers import TOL, check, compare, dev, host, rounder
 
 pytestmark = pytest.mark.gpu
 
@@ -91,11 +91,13 @@ def test_var_aggregate(lib, case):
     torch.cuda.synchronize()
     ref, cache = O.agg_fwd(tok, prm, H)
     rdtok, rg = O.agg_bwd(dz, cache, prm)
+    ref2, cache2 = O.agg_fwd(tok, prm, H, store=rounder(dtype))
+    rdtok2, rg2 = O.agg_bwd(dz, cache2, prm)
     tol = TOL[dtype]
-    check("z", host(z), ref, tol)
-    check("dtok", host(dtok), rdtok, tol)
+    compare("z", host(z), ref, ref2, tol)
+    compare("dtok", host(dtok), rdtok, rdtok2, tol)
     for k in rg:
-        check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["b_q"])
+        compare(f"d{k}", host(g[k]), rg[k], rg2[k], tol, floor_ref=rg["b_q"])
 
 
 # ---------------------------------------------------------------------------
@@ -143,11 +145,13 @@ def test_vit_block(lib, case):
     x, dy, prm, y, dx, g = _run_block(lib, case)
     ref, cache = O.block_fwd(x, prm, H, qk, 1e-5)
     rdx, rg = O.block_bwd(dy, cache, prm)
+    ref2, cache2 = O.block_fwd(x, prm, H, qk, 1e-5, store=rounder(dtype))
+    rdx2, rg2 = O.block_bwd(dy, cache2, prm)
     tol = TOL[dtype]
-    check("y", host(y), ref, tol)
-    check("dx", host(dx), rdx, tol)
+    compare("y", host(y), ref, ref2, tol)
+    compare("dx", host(dx), rdx, rdx2, tol)
     for k in rg:
-        check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["ln1_b"])
+        compare(f"d{k}", host(g[k]), rg[k], rg2[k], tol, floor_ref=rg["ln1_b"])
 
 
 def test_vit_block_accumulate(lib):
@@ -256,20 +260,26 @@ def _run_model(lib, c):
 
 def _check_model(vp, loss, inputs, c, tol):
     img, tgt, emb, agg, blocks, head = inputs
-    rl, pred, rg = O.model_fwd_bwd(img, tgt, emb, agg, blocks, head, p=4, agg_heads=c.agg_heads, heads=c.heads,
-                                   qk_norm=c.qk_norm, eps=c.eps)
+    kw = dict(p=4, agg_heads=c.agg_heads, heads=c.heads, qk_norm=c.qk_norm, eps=c.eps)
+    rl, pred, rg = O.model_fwd_bwd(img, tgt, emb, agg, blocks, head, **kw)
+    rl2, pred2, rg2 = O.model_fwd_bwd(img, tgt, emb, agg, blocks, head, store=rounder(c.dtype), **kw)
     assert abs(host(loss)[0] - rl) <= tol * abs(rl), (host(loss)[0], rl)
-    check("pred", host(vp.pred), pred, tol)
+    compare("pred", host(vp.pred), pred, pred2, tol)
     G = vp.grads
+    worst = []
     for k, v in rg["embed"].items():
-        check(f"embed.d{k}", host(G["embed"][k]), v, tol)
+        worst.append((compare(f"embed.d{k}", host(G["embed"][k]), v, rg2["embed"][k], tol), f"embed.{k}"))
     for k, v in rg["agg"].items():
-        check(f"agg.d{k}", host(G["agg"][k]), v, tol, floor_ref=rg["agg"]["b_q"])
+        worst.append((compare(f"agg.d{k}", host(G["agg"][k]), v, rg2["agg"][k], tol, floor_ref=rg["agg"]["b_q"]),
+                      f"agg.{k}"))
     for i, gb in enumerate(rg["blocks"]):
         for k, v in gb.items():
-            check(f"block{i}.d{k}", host(G["blocks"][i][k]), v, tol, floor_ref=gb["ln1_b"])
+            worst.append((compare(f"block{i}.d{k}", host(G["blocks"][i][k]), v, rg2["blocks"][i][k], tol,
+                                  floor_ref=gb["ln1_b"]), f"block{i}.{k}"))
     for k, v in rg["head"].items():
-        check(f"head.d{k}", host(G["head"][k]), v, tol)
+        worst.append((compare(f"head.d{k}", host(G["head"][k]), v, rg2["head"][k], tol), f"head.{k}"))
+    worst.sort(key=lambda t: -t[0][0])
+    print("largest errors (err, floor):", [(n, f"{e:.2e}", f"{fl:.2e}") for (e, fl), n in worst[:6]])
 
 
 def test_full_model_tiny_fp32(lib):

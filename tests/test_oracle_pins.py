@@ -525,3 +525,20 @@ def test_hybrid_stop_shard_sum(K, branch):
             assert np.allclose(gk["w_fc2"], g["w_fc2"][fc], atol=1e-12)
     assert np.allclose(ysum, y - x, atol=1e-12, rtol=0)
     assert np.allclose(dxsum, dx - dy, atol=1e-12, rtol=0)
+
+
+def test_store_hook_is_identity_when_exact():
+    """The storage hook does not touch the arithmetic: identity storage gives
+    bitwise the same results as none, and bf16 storage moves them slightly."""
+    x = _rand(2, 5, 16)
+    prm = _block_prm(16, 16, 32, 8)
+    dy = _rand(2, 5, 16)
+    y0, c0 = O.block_fwd(x, prm, 2)
+    y1, c1 = O.block_fwd(x, prm, 2, store=lambda a: a)
+    assert np.array_equal(y0, y1)
+    assert np.array_equal(O.block_bwd(dy, c0, prm)[0], O.block_bwd(dy, c1, prm)[0])
+    import synth
+    r = lambda a: synth.bf16_round(np.asarray(a, np.float32)).astype(np.float64)
+    y2, _ = O.block_fwd(x, prm, 2, store=r)
+    e = np.abs(y2 - y0).max() / np.abs(y0).max()
+    assert 0 < e < 2e-2
