@@ -1,0 +1,288 @@
+#!/usr/bin/env python
+"""Throughput of the ViT forward+backward pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 115m|1b|10b-shard|113b-shard|tiny]
+
+One step is one pass of the whole path over one batch of synthetic input,
+resident in HBM before the timed region starts:
+
+  full model (115m, 1b, tiny): patch embedding -> variable aggregation ->
+      pre-LN blocks -> head -> MSE loss -> the whole backward;
+  10b-shard : 4 blocks of one GPU's tensor-parallel shard, forward + backward;
+  113b-shard: variable aggregation + 2 shard blocks, forward + backward.
+
+Prints one JSON line. `value` is the achieved algorithmic TFLOP/s of the step
+(model flops: products counted once forward and twice backward; see
+paper_2404_14712_amd.model.pass_flops); `roofline` reports the dominant kernel
+timed with HIP events on the stream it runs on during the timed region;
+`cpu_baseline` times the fp64 oracle on a bounded sample of the same workload
+on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+WORKLOADS = {"115m": 2, "1b": 3, "10b-shard": 4, "113b-shard": 5, "tiny": 1}
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3      # MI355X fp32
+PEAK_HBM_GBS = 8000.0
+
+
+def dims_for(c):
+    from paper_2404_14712_amd.model import PassDims
+    mode = "full" if c.full_model else ("agg_blocks" if c.agg_only_prefix else "blocks")
+    return PassDims(mode=mode, dtype=c.dtype, B=c.B, L=c.L, d=c.d, blocks=c.blocks, heads=c.heads,
+                    head_dim=c.head_dim, mlp=c.mlp, qk_norm=c.qk_norm, eps=c.eps, V=c.V, grid=c.grid,
+                    agg_heads=c.agg_heads, agg_head_dim=c.agg_head_dim)
+
+
+def describe(c) -> dict:
+    kind = {"full": "full ClimaX-style ViT forward+backward (patch embed, variable aggregation, blocks, head, MSE)",
+            "blocks": "tensor-parallel shard blocks, forward+backward",
+            "agg_blocks": "variable aggregation + tensor-parallel shard blocks, forward+backward"}
+    z = dims_for(c)
+    out = {"workload": f"{c.name}: {kind[z.mode]}", "global_batch": c.B, "seq_len": c.L, "d": c.d,
+           "blocks": c.blocks, "local_heads": c.heads, "head_dim": c.head_dim, "local_mlp": c.mlp,
+           "qk_norm": c.qk_norm, "parallelism": "none (one GPU's share)"}
+    if c.V:
+        out.update({"variables": c.V, "agg_heads": c.agg_heads})
+    if c.grid[0]:
+        out["grid"] = f"{c.grid[0]}x{c.grid[1]}"
+    return out
+
+
+def device_inputs(c, device):
+    """Seeded synthetic parameters and inputs, resident on the device."""
+    import numpy as np
+    import torch
+
+    import synth
+
+    def D(a, dt=None):
+        dt = dt or c.dtype
+        a = np.ascontiguousarray(a, np.float32)
+        if dt == "bf16":
+            return torch.from_numpy(synth.bf16_bits(a).view(np.int16)).to(device).view(torch.bfloat16)
+        return torch.from_numpy(a).to(device)
+
+    P = lambda p: {k: (None if v is None else D(v)) for k, v in p.items()}
+    params = {"blocks": [P(synth.block_params(c, i)) for i in range(c.blocks)]}
+    z = dims_for(c)
+    inputs = {}
+    tdt = torch.bfloat16 if c.dtype == "bf16" else torch.float32
+    if z.mode == "full":
+        params["embed"] = P(synth.embed_params(c))
+        params["agg"] = P(synth.agg_params(c))
+        params["head"] = P(synth.head_params(c))
+        inputs["img"] = D(synth.image(c), "f32")
+        inputs["tgt"] = D(synth.target(c), "f32")
+    else:
+        # activations and the upstream gradient N(0, 1), drawn on the device (seeded)
+        gen = torch.Generator(device=device)
+        gen.manual_seed(synth.BASE_SEED + 100 * c.cfg)
+        inputs["dy"] = torch.randn(c.B, c.L, c.d, generator=gen, device=device, dtype=torch.float32).to(tdt)
+        if z.mode == "agg_blocks":
+            params["agg"] = P(synth.agg_params(c))
+            tok = torch.empty(c.B, c.L, c.V, c.d, device=device, dtype=tdt)
+            for b in range(c.B):
+                for l0 in range(0, c.L, 256):
+                    tok[b, l0:l0 + 256] = torch.randn(min(256, c.L - l0), c.V, c.d, generator=gen, device=device,
+                                                      dtype=torch.float32).to(tdt)
+            inputs["tok"] = tok
+        else:
+            inputs["x"] = torch.randn(c.B, c.L, c.d, generator=gen, device=device, dtype=torch.float32).to(tdt)
+    return params, inputs
+
+
+def cpu_baseline(c) -> dict:
+    """The fp64 oracle on a bounded sample of the workload (host cores)."""
+    import dataclasses
+
+    import numpy as np
+
+    import oracle as O
+    import synth
+    from paper_2404_14712_amd.model import pass_flops
+
+    z = dims_for(c)
+    if z.mode == "full":
+        Hg, Wg = c.grid
+        s = dataclasses.replace(c, B=1, blocks=1, grid=(max(4, Hg // 2), max(4, Wg // 2)),
+                                L=max(1, Hg // 8) * max(1, Wg // 8))
+        sample = (f"batch 1 of {c.B}, 1 of {c.blocks} blocks, {s.L} of {c.L} patches "
+                  f"({s.grid[0]}x{s.grid[1]} grid), all {c.V} variables, full width")
+    elif z.mode == "blocks":
+        s = dataclasses.replace(c, B=1, blocks=1)
+        sample = f"batch 1 of {c.B}, 1 of {c.blocks} blocks, full width"
+    else:
+        s = dataclasses.replace(c, L=128, blocks=1)
+        sample = f"128 of {c.L} tokens, 1 of {c.blocks} blocks, aggregation over all {c.V} variables"
+    zs = dims_for(s)
+    blocks = [synth.block_params(s, i) for i in range(s.blocks)]
+    t0 = time.perf_counter()
+    if zs.mode == "full":
+        O.model_fwd_bwd(synth.image(s), synth.target(s), synth.embed_params(s), synth.agg_params(s), blocks,
+                        synth.head_params(s), p=4, agg_heads=s.agg_heads, heads=s.heads, qk_norm=s.qk_norm)
+    else:
+        x = synth.activations(s, "x")
+        dy = synth.normal(s.cfg, "dy", x.shape)
+        if zs.mode == "agg_blocks":
+            tok = np.stack([synth.tokens_chunk(s, b, 0, s.L) for b in range(s.B)])
+            x, ca = O.agg_fwd(tok, synth.agg_params(s), s.agg_heads)
+        caches = []
+        for p in blocks:
+            x, cc = O.block_fwd(x, p, s.heads, s.qk_norm)
+            caches.append(cc)
+        g = dy
+        for p, cc in zip(blocks[::-1], caches[::-1]):
+            g, _ = O.block_bwd(g, cc, p)
+        if zs.mode == "agg_blocks":
+            O.agg_bwd(g, ca, synth.agg_params(s))
+    dt = time.perf_counter() - t0
+    fl = pass_flops(zs)["total"]
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"),
+                      default=None)
+    except Exception:
+        pass
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": threads or len(os.sched_getaffinity(0)),
+            "kind": "oracle", "sample": sample, "seconds": round(dt, 3), "sample_flops": fl}
+
+
+def read_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` measured with rocprofv3 counters, if a
+    summary for the current kernel exists (profiles/traffic.json)."""
+    f = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(f):
+        return None
+    try:
+        t = json.load(open(f))
+        e = t.get(kernel)
+        return None if e is None else e.get("bytes_per_launch")
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="115m", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU's share of the model; runs on more than one GPU are not part "
+              "of this build (the multi-GPU layout is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2404_14712_amd import load
+    from paper_2404_14712_amd.model import ViTPass, pass_flops
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    lib = load()
+    c = synth.CONFIGS[WORKLOADS[a.workload]]
+    z = dims_for(c)
+    params, inputs = device_inputs(c, dev)
+    vp = ViTPass(lib, z, params, device=dev)
+    flops = pass_flops(z)
+    step = lambda: vp.forward_backward(inputs)
+
+    for _ in range(max(1, a.warmup)):
+        step()
+    torch.cuda.synchronize()
+
+    # one instrumented step (not timed) finds the kernel with the largest total time
+    lib.orbit_timing_enable(1)
+    lib.orbit_timing_filter(None)
+    step()
+    torch.cuda.synchronize()
+    names = lib.orbit_timing_kernel_names()
+    # exact-name totals (a name may prefix another, so subtract longer names)
+    tot = {}
+    for n in names:
+        s = lib.orbit_timing_summary(n)
+        longer = [m for m in names if m != n and m.startswith(n)]
+        for m in longer:
+            t = lib.orbit_timing_summary(m)
+            s = {k: s[k] - t[k] for k in s}
+        tot[n] = s
+    step_kernel_ms = sum(v["ms"] for v in tot.values())
+    dominant = max(tot, key=lambda n: tot[n]["ms"])
+    breakdown = sorted(((n, v["ms"]) for n, v in tot.items()), key=lambda t: -t[1])[:8]
+
+    # timed region: HIP events around every launch of the dominant kernel
+    lib.orbit_timing_enable(1)
+    lib.orbit_timing_filter(dominant)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(a.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / a.steps
+    dk = lib.orbit_timing_summary(dominant)
+    lib.orbit_timing_enable(0)
+
+    tflops = flops["total"] / (ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_F32_TFLOPS
+    k_avg_ms = dk["ms"] / max(dk["launches"], 1)
+    k_flops = dk["flops"] / max(dk["launches"], 1)
+    k_bytes = dk["bytes"] / max(dk["launches"], 1)
+    if k_flops > 0:
+        achieved = k_flops / (k_avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4)}
+    else:
+        achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof.update({"traffic": read_traffic(dominant), "kernel": dominant, "launches": dk["launches"],
+                 "avg_launch_ms": round(k_avg_ms, 5), "algorithmic_flops_per_launch": k_flops,
+                 "algorithmic_bytes_per_launch": k_bytes})
+
+    samples = c.B / (ms * 1e-3)
+    out = {
+        "metric": "ViT fwd+bwd achieved TFLOPS/GPU and % bf16 MFMA peak; samples/sec",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if c.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) fields and N(0,sigma) weights)",
+        "config": describe(c),
+        "pct_peak": round(100 * tflops / peak, 2),
+        "samples_per_s": round(samples, 2),
+        "tokens_per_s": round(c.B * c.L / (ms * 1e-3), 1),
+        "flops_per_step": flops,
+        "kernel_ms_per_step": round(step_kernel_ms, 4),
+        "top_kernels_ms": [[n, round(t, 4)] for n, t in breakdown],
+        "roofline": roof,
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(c)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
