@@ -19,15 +19,33 @@
 namespace orbit {
 namespace {
 
+// Column reductions out[j] = sum_i x_i W[i][j] over the d rows of a [d, A]
+// weight: 64 columns x 16 row lanes per block (coalesced row reads), the 16
+// partial sums combined in a fixed order.
+constexpr int kGvCols = 64, kGvLanes = 16;
+
+ORBIT_DEV float gv_combine(float s, float (*red)[kGvCols], int cl, int q) {
+  red[q][cl] = s;
+  __syncthreads();
+  float t = 0.f;
+  if (q == 0)
+#pragma unroll
+    for (int k = 0; k < kGvLanes; ++k) t += red[k][cl];
+  return t;
+}
+
 // q[j] = q0 . w_q[:, j] + b_q[j]   (float32 out)
 template <typename T>
-__global__ void __launch_bounds__(256) agg_query(const T* __restrict__ q0, const T* __restrict__ wq,
-                                                 const T* __restrict__ bq, float* __restrict__ q, int d, int A) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= A) return;
+__global__ void __launch_bounds__(1024) agg_query(const T* __restrict__ q0, const T* __restrict__ wq,
+                                                  const T* __restrict__ bq, float* __restrict__ q, int d, int A) {
+  __shared__ float red[kGvLanes][kGvCols];
+  const int cl = threadIdx.x % kGvCols, lq = threadIdx.x / kGvCols;
+  const int j = blockIdx.x * kGvCols + cl;
   float s = 0.f;
-  for (int i = 0; i < d; ++i) s += to_f(q0[i]) * to_f(wq[(int64_t)i * A + j]);
-  q[j] = s + to_f(bq[j]);
+  if (j < A)
+    for (int i = lq; i < d; i += kGvLanes) s += to_f(q0[i]) * to_f(wq[(int64_t)i * A + j]);
+  const float t = gv_combine(s, red, cl, lq);
+  if (lq == 0 && j < A) q[j] = t + to_f(bq[j]);
 }
 
 // Ut[h][i] = sum_c w_k[i][h*dh + c] q[h*dh + c]   (one wave per (i, 8 heads))
@@ -90,15 +108,19 @@ __global__ void __launch_bounds__(256) agg_softmax_bwd(const float* __restrict__
 
 // dq[j] = sum_i w_k[i][j] dU[i][h(j)]
 template <typename T>
-__global__ void __launch_bounds__(256) agg_dq(const T* __restrict__ wk, const float* __restrict__ dU,
-                                              float* __restrict__ dq, int d, int H, int dh) {
+__global__ void __launch_bounds__(1024) agg_dq(const T* __restrict__ wk, const float* __restrict__ dU,
+                                               float* __restrict__ dq, int d, int H, int dh) {
+  __shared__ float red[kGvLanes][kGvCols];
   const int A = H * dh;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= A) return;
-  const int h = j / dh;
+  const int cl = threadIdx.x % kGvCols, lq = threadIdx.x / kGvCols;
+  const int j = blockIdx.x * kGvCols + cl;
   float s = 0.f;
-  for (int i = 0; i < d; ++i) s += to_f(wk[(int64_t)i * A + j]) * dU[(int64_t)i * H + h];
-  dq[j] = s;
+  if (j < A) {
+    const int h = j / dh;
+    for (int i = lq; i < d; i += kGvLanes) s += to_f(wk[(int64_t)i * A + j]) * dU[(int64_t)i * H + h];
+  }
+  const float t = gv_combine(s, red, cl, lq);
+  if (lq == 0 && j < A) dq[j] = t;
 }
 
 // dW_k[i][j] = dU[i][h(j)] q[j];  dW_q[i][j] = q0[i] dq[j]
@@ -235,12 +257,13 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
   KernelInfo kq{"agg_query", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   KernelInfo ku{"agg_fold_key", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   if (dt == ORBIT_BF16) {
-    ORBIT_TRY(launch(kq, agg_query<bf16>, dim3(g1(z.A)), dim3(256), 0, s, (const bf16*)p.q0, (const bf16*)p.w_q,
+    ORBIT_TRY(launch(kq, agg_query<bf16>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const bf16*)p.q0,
+                     (const bf16*)p.w_q,
                      (const bf16*)p.b_q, sv.q, z.d, z.A));
     ORBIT_TRY(launch(ku, agg_fold_key<bf16>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s, (const bf16*)p.w_k,
                      (const float*)sv.q, (bf16*)sv.Ut, z.d, z.H, z.dh));
   } else {
-    ORBIT_TRY(launch(kq, agg_query<float>, dim3(g1(z.A)), dim3(256), 0, s, (const float*)p.q0,
+    ORBIT_TRY(launch(kq, agg_query<float>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const float*)p.q0,
                      (const float*)p.w_q, (const float*)p.b_q, sv.q, z.d, z.A));
     ORBIT_TRY(launch(ku, agg_fold_key<float>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s,
                      (const float*)p.w_k, (const float*)sv.q, (float*)sv.Ut, z.d, z.H, z.dh));
@@ -395,7 +418,8 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
   KernelInfo kou{"agg_outer", 2.0 * z.d * z.A, 8.0 * z.d * z.A};
   KernelInfo kqb{"agg_query_bwd", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   if (dt == ORBIT_BF16) {
-    ORBIT_TRY(launch(kdq, agg_dq<bf16>, dim3(g1(z.A)), dim3(256), 0, s, (const bf16*)p.w_k, (const float*)dU, dq,
+    ORBIT_TRY(launch(kdq, agg_dq<bf16>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const bf16*)p.w_k,
+                     (const float*)dU, dq,
                      z.d, z.H, z.dh));
     ORBIT_TRY(launch(kou, agg_outer<bf16>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
                      dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const bf16*)p.q0, (const float*)dq,
@@ -403,7 +427,8 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
     ORBIT_TRY(launch(kqb, agg_query_bwd<bf16>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s, (const bf16*)p.w_q,
                      (const float*)dq, gr.q0, gr.b_q, gr.b_k, z.d, z.A, accumulate));
   } else {
-    ORBIT_TRY(launch(kdq, agg_dq<float>, dim3(g1(z.A)), dim3(256), 0, s, (const float*)p.w_k, (const float*)dU,
+    ORBIT_TRY(launch(kdq, agg_dq<float>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const float*)p.w_k,
+                     (const float*)dU,
                      dq, z.d, z.H, z.dh));
     ORBIT_TRY(launch(kou, agg_outer<float>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
                      dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const float*)p.q0, (const float*)dq,

@@ -35,6 +35,7 @@ struct GemmKArgs {
   int64_t lda, ldb, ldc;
   int64_t sA, sB, sB2, sC;
   int batch, splits, k_per_split;
+  int vec_ok;      // N, ldc, batch strides and epilogue operands allow 16-byte access
   float* partial;  // splits > 1: float32 partials [splits][batch][M][N]
   Epi epi;
 };
@@ -57,6 +58,51 @@ ORBIT_DEV void epi_apply(const Epi& e, int64_t bz, int r, int c, float v, OutT* 
   C[off] = from_f<OutT>(v);
 }
 
+// 8 consecutive columns c0..c0+7 of row r (16-byte aligned rows)
+template <typename T> ORBIT_DEV void ld8(const T* p, float* f) {
+  unpack(ld128(p), f, (T*)nullptr);
+  if constexpr (sizeof(T) == 4) unpack(ld128(p + 4), f + 4, (T*)nullptr);
+}
+template <typename T> ORBIT_DEV void st8(T* p, const float* f) {
+  st128(p, pack(f, (T*)nullptr));
+  if constexpr (sizeof(T) == 4) st128(p + 4, pack(f + 4, (T*)nullptr));
+}
+
+template <typename T, typename OutT>
+ORBIT_DEV void epi_apply8(const Epi& e, int64_t bz, int r, int c0, float* v, OutT* C, int64_t ldc) {
+  const int64_t off = (int64_t)r * ldc + c0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] *= e.alpha;
+  float t[8];
+  if (e.accumulate) {
+    ld8(C + off, t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[i];
+  }
+  if (e.bias) {
+    ld8(static_cast<const T*>(e.bias) + bz * e.sBias + c0, t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[i];
+  }
+  if (e.gelu_out) {
+    st8(static_cast<T*>(e.gelu_out) + (int64_t)r * e.ldgo + c0, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = gelu_f(v[i]);
+  }
+  if (e.gelu_in) {
+    ld8(static_cast<const T*>(e.gelu_in) + (int64_t)r * e.ldgi + c0, t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] *= gelu_grad_f(t[i]);
+  }
+  if (e.res) {
+    const int rr = e.res_row_mod ? r % e.res_row_mod : r;
+    ld8(static_cast<const T*>(e.res) + bz * e.sR + (int64_t)rr * e.ldr + c0, t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[i];
+  }
+  st8(C + off, v);
+}
+
 template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
 __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   constexpr int NT = WM * WN * 64;
@@ -65,23 +111,41 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   constexpr int PITCH = BKE + E;
   constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
   static_assert(TM >= 1 && TN >= 1, "wave tile must be at least 32x32");
-  __shared__ __attribute__((aligned(16))) T lds[2][(BM + BN) * PITCH];
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  T* lds = reinterpret_cast<T*>(smem);
+  constexpr int STAGE = (BM + BN) * PITCH;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
   const int z = blockIdx.z;
   const int split = z % g.splits;
   const int64_t bz = z / g.splits;
+
+  // tile order: consecutive hardware ids go round-robin over the 8 XCDs, so
+  // give each XCD a contiguous range of tiles, walked in groups of 8 tile
+  // rows (the group's A panels and the B panels it sweeps stay in that L2)
+  const int tiles_n = (g.N + BN - 1) / BN, tiles_m = (g.M + BM - 1) / BM;
+  const int nt = tiles_m * tiles_n;
+  int id = blockIdx.x;
+  const int full = nt - nt % 8;
+  if (id < full) id = (id % 8) * (full / 8) + id / 8;
+  constexpr int GROUP = 8;
+  const int per_group = GROUP * tiles_n;
+  const int first_m = (id / per_group) * GROUP;
+  const int gsize = min(tiles_m - first_m, GROUP);
+  const int tile_m = first_m + (id % per_group) % gsize;
+  const int tile_n = (id % per_group) / gsize;
+
   const T* A = static_cast<const T*>(g.A) + bz * g.sA;
   const T* B = static_cast<const T*>(g.B) + bz * g.sB;
   const T* B2 = g.B2 ? static_cast<const T*>(g.B2) + bz * g.sB2 : nullptr;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
   const int kbeg = split * g.k_per_split;
   const int kend = min(g.K, kbeg + g.k_per_split);
   const int nk = (kend - kbeg + BKE - 1) / BKE;
 
-  TileLoader<T, BM, BKE, NT, AK> la;
-  TileLoader<T, BN, BKE, NT, BKM> lb;
+  GemmStage<T, BM, BKE, NT, AK> la;
+  GemmStage<T, BN, BKE, NT, BKM> lb;
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -94,8 +158,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   if (nk > 0) {
     la.load(A, nullptr, 0, g.lda, m0, g.M, kbeg, kend, tid);
     lb.load(B, B2, g.k_split, g.ldb, n0, g.N, kbeg, kend, tid);
-    la.store(&lds[0][0], tid);
-    lb.store(&lds[0][BM * PITCH], tid);
+    la.store(lds, tid);
+    lb.store(lds + BM * PITCH, tid);
   }
   __syncthreads();
 
@@ -106,8 +170,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
       la.load(A, nullptr, 0, g.lda, m0, g.M, k0, kend, tid);
       lb.load(B, B2, g.k_split, g.ldb, n0, g.N, k0, kend, tid);
     }
-    const T* As = &lds[cur][0];
-    const T* Bs = &lds[cur][BM * PITCH];
+    const T* As = lds + cur * STAGE;
+    const T* Bs = As + BM * PITCH;
 #pragma unroll
     for (int kk = 0; kk < BKE / 16; ++kk) {
       Frag<T> af[TM], bfr[TN];
@@ -123,67 +187,138 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
         for (int j = 0; j < TN; ++j) mma16(acc[i][j], af[i], bfr[j]);
     }
     if (kt + 1 < nk) {
-      la.store(&lds[cur ^ 1][0], tid);
-      lb.store(&lds[cur ^ 1][BM * PITCH], tid);
+      T* nxt = lds + (cur ^ 1) * STAGE;
+      la.store(nxt, tid);
+      lb.store(nxt + BM * PITCH, tid);
     }
     __syncthreads();
   }
 
-  // epilogue
+  // Epilogue through LDS (the stages are free after the final barrier): each
+  // wave parks 32 rows of its accumulators at a time in a private region, then
+  // reads them back as 8 consecutive columns per lane for 16-byte stores.
+  constexpr int EP = WTN + 8;                        // row pitch (floats)
+  constexpr int LPR = WTN / 8;                       // lanes per row
+  constexpr int RPI = 64 / LPR;                      // rows per iteration
+  float* ew = reinterpret_cast<float*>(smem) + wave * 32 * EP;
   OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
+  const bool raw = g.splits > 1;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-        const int c = n0 + wn * WTN + j * 32 + (lane & 31);
-        if (r < g.M && c < g.N) {
-          if (g.splits > 1) {
-            g.partial[(((int64_t)split * g.batch + bz) * g.M + r) * g.N + c] = acc[i][j][v];
+      for (int v = 0; v < 16; ++v)
+        ew[((v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * EP + j * 32 + (lane & 31)] = acc[i][j][v];
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < 32 / RPI; ++it) {
+      const int rl = it * RPI + lane / LPR;
+      const int cl = (lane % LPR) * 8;
+      const int r = m0 + wm * WTM + i * 32 + rl;
+      const int c0 = n0 + wn * WTN + cl;
+      float v8[8];
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(ew + rl * EP + cl);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(ew + rl * EP + cl + 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { v8[q] = lo[q]; v8[4 + q] = hi[q]; }
+      if (r < g.M && c0 < g.N) {
+        if (raw) {
+          float* P = g.partial + (((int64_t)split * g.batch + bz) * g.M + r) * g.N;
+          if (g.vec_ok) {
+            st8(P + c0, v8);
           } else {
-            epi_apply<T, OutT>(g.epi, bz, r, c, acc[i][j][v], C, g.ldc);
+            for (int q = 0; q < 8 && c0 + q < g.N; ++q) P[c0 + q] = v8[q];
           }
+        } else if (g.vec_ok) {
+          epi_apply8<T, OutT>(g.epi, bz, r, c0, v8, C, g.ldc);
+        } else {
+          for (int q = 0; q < 8 && c0 + q < g.N; ++q) epi_apply<T, OutT>(g.epi, bz, r, c0 + q, v8[q], C, g.ldc);
         }
       }
+    }
+    __syncthreads();
+  }
 }
 
+// C = epilogue(sum over splits of the float32 partials): 8 consecutive columns
+// per thread, rows on grid.y (strided), batch on grid.z; 32-bit index math
 template <typename T, typename OutT>
-__global__ void __launch_bounds__(256) splitk_reduce(GemmKArgs g) {
+__global__ void __launch_bounds__(64) splitk_reduce(GemmKArgs g) {
+  const int c0 = (blockIdx.x * 64 + threadIdx.x) * 8;
+  if (c0 >= g.N) return;
+  const int64_t bz = blockIdx.z;
   const int64_t MN = (int64_t)g.M * g.N;
-  const int64_t total = MN * g.batch;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
-    const int64_t bz = idx / MN;
-    const int64_t rem = idx % MN;
-    const int r = (int)(rem / g.N), c = (int)(rem % g.N);
-    float v = 0.f;
-    for (int s = 0; s < g.splits; ++s) v += g.partial[((int64_t)s * g.batch + bz) * MN + rem];
-    OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
-    epi_apply<T, OutT>(g.epi, bz, r, c, v, C, g.ldc);
+  OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
+  for (int r = blockIdx.y; r < g.M; r += gridDim.y) {
+    const float* p = g.partial + bz * MN + (int64_t)r * g.N + c0;
+    const int64_t stride = (int64_t)g.batch * MN;
+    if (g.vec_ok) {
+      float v[8], t[8];
+      ld8(p, v);
+      for (int s = 1; s < g.splits; ++s) {
+        ld8(p + s * stride, t);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += t[i];
+      }
+      epi_apply8<T, OutT>(g.epi, bz, r, c0, v, C, g.ldc);
+    } else {
+      for (int q = 0; q < 8 && c0 + q < g.N; ++q) {
+        float v = 0.f;
+        for (int s = 0; s < g.splits; ++s) v += p[s * stride + q];
+        epi_apply<T, OutT>(g.epi, bz, r, c0 + q, v, C, g.ldc);
+      }
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 // host dispatch
 // ---------------------------------------------------------------------------
-struct TileCfg { int BM, BN, WM, WN; };
+struct TileCfg {
+  int BM, BN, WM, WN;
+  bool operator==(const TileCfg& o) const { return BM == o.BM && BN == o.BN && WM == o.WM && WN == o.WN; }
+};
+constexpr TileCfg kT256{256, 256, 2, 4};
+constexpr TileCfg kT256x128{256, 128, 4, 2};
+constexpr TileCfg kT128x256{128, 256, 2, 4};
 constexpr TileCfg kBig{128, 128, 2, 2};
 constexpr TileCfg kNarrowN{128, 32, 4, 1};
 constexpr TileCfg kNarrowM{32, 128, 1, 4};
 constexpr TileCfg kSmall{64, 64, 2, 2};
 
+int64_t tiles_of(const Gemm& g, const TileCfg& t) { return cdiv(g.M, t.BM) * cdiv(g.N, t.BN) * (int64_t)g.batch; }
+
+int bke_of(orbit_dtype dt) { return dt == ORBIT_BF16 ? 64 : 32; }
+
+// split-K factor that brings `tiles` work items up to one per CU, keeping at
+// least 8 K-steps per split
+int64_t splits_for(const Gemm& g, int64_t tiles) {
+  const int64_t ksteps = cdiv(g.K, bke_of(g.dtype));
+  if (tiles >= 240 || ksteps < 16) return 1;
+  return std::max<int64_t>(1, std::min<int64_t>(cdiv(256, tiles), ksteps / 8));
+}
+
 TileCfg pick_tile(const Gemm& g) {
   if (g.N <= 32) return kNarrowN;
   if (g.M <= 32) return kNarrowM;
   if (g.M <= 64 || g.N <= 64) return kSmall;
+  if (g.dtype == ORBIT_BF16 && g.K >= 256) {
+    // the largest tile that gives every CU a tile (directly, or through a
+    // split of a long K)
+    const TileCfg cands[] = {kT256, kT256x128, kT128x256};
+    for (const TileCfg& t : cands) {
+      if (g.M < t.BM || g.N < t.BN) continue;
+      const int64_t tiles = tiles_of(g, t);
+      if (tiles * splits_for(g, tiles) >= 240) return t;
+    }
+  }
   return kBig;
 }
 
-int bke_of(orbit_dtype dt) { return dt == ORBIT_BF16 ? 64 : 32; }
-
 int pick_splits(const Gemm& g, const TileCfg& t) {
-  const int64_t tiles = cdiv(g.M, t.BM) * cdiv(g.N, t.BN) * (int64_t)g.batch;
+  const int64_t tiles = tiles_of(g, t);
+  if (t.BM * t.BN >= 256 * 128) return (int)splits_for(g, tiles);
   const int bke = bke_of(g.dtype);
   const int64_t ksteps = cdiv(g.K, bke);
   if (tiles >= 256 || ksteps < 8) return 1;
@@ -210,20 +345,36 @@ orbit_status run_cfg(const Gemm& g, GemmKArgs& a, hipStream_t s) {
   const double bytes = ((double)g.M * g.K + (double)g.K * g.N) * sizeof(T) * g.batch +
                        (double)g.M * g.N * sizeof(OutT) * g.batch;
   KernelInfo ki{kname<T, OutT, BM, BN, WM, WN, AK, BKM>(), flops, bytes};
-  dim3 grid((unsigned)cdiv(g.N, BN), (unsigned)cdiv(g.M, BM), (unsigned)(g.batch * a.splits));
-  ORBIT_TRY(launch(ki, gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>, grid, dim3(WM * WN * 64), 0, s, a));
+  dim3 grid((unsigned)(cdiv(g.N, BN) * cdiv(g.M, BM)), 1, (unsigned)(g.batch * a.splits));
+  constexpr size_t lds = 2 * (size_t)(BM + BN) * (128 + 16);
+  static const bool attr = [] {
+    // lift the default dynamic-LDS cap for this instantiation (a failure here
+    // surfaces as a launch error below)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    (void)hipGetLastError();
+    return true;
+  }();
+  (void)attr;
+  ORBIT_TRY(launch(ki, gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>, grid, dim3(WM * WN * 64), lds, s, a));
   if (a.splits > 1) {
     const int64_t total = (int64_t)g.M * g.N * g.batch;
-    const unsigned blocks = (unsigned)std::min<int64_t>(cdiv(total, 256), 8192);
     KernelInfo kr{sizeof(OutT) == 2 ? "splitk_reduce<bf16>" : "splitk_reduce<f32>", 0.0,
                   (double)total * 4 * (a.splits + 1)};
-    ORBIT_TRY(launch(kr, splitk_reduce<T, OutT>, dim3(blocks), dim3(256), 0, s, a));
+    const dim3 grid((unsigned)cdiv(g.N, 512), (unsigned)std::min(g.M, 16384), (unsigned)g.batch);
+    ORBIT_TRY(launch(kr, splitk_reduce<T, OutT>, grid, dim3(64), 0, s, a));
   }
   return ORBIT_OK;
 }
 
 template <typename T, typename OutT, bool AK, bool BKM>
 orbit_status run_layout(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    if (t.BM == 256 && t.BN == 256 && t.WM == 2) return run_cfg<T, OutT, 256, 256, 2, 4, AK, BKM>(g, a, s);
+    if (t.BM == 256 && t.BN == 256 && t.WM == 4) return run_cfg<T, OutT, 256, 256, 4, 2, AK, BKM>(g, a, s);
+    if (t.BM == 256 && t.BN == 128) return run_cfg<T, OutT, 256, 128, 4, 2, AK, BKM>(g, a, s);
+    if (t.BM == 128 && t.BN == 256) return run_cfg<T, OutT, 128, 256, 2, 4, AK, BKM>(g, a, s);
+  }
   if (t.BM == 128 && t.BN == 128) return run_cfg<T, OutT, 128, 128, 2, 2, AK, BKM>(g, a, s);
   if (t.BM == 128 && t.BN == 32) return run_cfg<T, OutT, 128, 32, 4, 1, AK, BKM>(g, a, s);
   if (t.BM == 32 && t.BN == 128) return run_cfg<T, OutT, 32, 128, 1, 4, AK, BKM>(g, a, s);
@@ -280,6 +431,13 @@ orbit_status gemm(const Gemm& g, void* ws, size_t ws_bytes, hipStream_t s) {
     a.partial = static_cast<float*>(ws);
   }
   if (g.K <= 0) a.k_per_split = 0;
+  {
+    auto al = [](int64_t x) { return x % 8 == 0; };
+    auto ap = [](const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+    a.vec_ok = al(g.N) && al(g.ldc) && al(g.sC) && al(g.sBias) && al(g.ldgo) && al(g.ldgi) && al(g.ldr) &&
+               al(g.sR) && ap(g.C) && ap(g.bias) && ap(g.gelu_out) && ap(g.gelu_in) && ap(g.res) &&
+               (g.res == nullptr || g.res_row_mod == 0 || true);
+  }
   a.epi.alpha = g.alpha;
   a.epi.accumulate = g.accumulate ? 1 : 0;
   a.epi.bias = g.bias;

@@ -138,7 +138,9 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, i
 
 // ---- column sums ------------------------------------------------------------
 constexpr int kColsPerBlock = 512;  // 64 threads x 8 columns
-constexpr int kRowsPerChunk = 64;
+constexpr int kMaxChunks = 64;      // row chunks (partials per column)
+
+int rows_per_chunk(int rows) { return (int)std::max<int64_t>(16, cdiv(cdiv(rows, kMaxChunks), 4) * 4); }
 
 template <typename T, bool XS>
 __global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ dy, int64_t lddy, int rows,
@@ -146,12 +148,12 @@ __global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ dy, 
                                                       const float* __restrict__ mean,
                                                       const float* __restrict__ rstd,
                                                       float* __restrict__ part_s,
-                                                      float* __restrict__ part_x) {
+                                                      float* __restrict__ part_x, int rpc) {
   __shared__ float sm[2][4][kColsPerBlock];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const int c0 = blockIdx.x * kColsPerBlock + tx * 8;
   const int chunk = blockIdx.y;
-  const int r0 = chunk * kRowsPerChunk, r1 = min(rows, r0 + kRowsPerChunk);
+  const int r0 = chunk * rpc, r1 = min(rows, r0 + rpc);
   float as[8], ax[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) as[i] = ax[i] = 0.f;
@@ -192,13 +194,24 @@ __global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ dy, 
   }
 }
 
+// out[c] (+)= sum over chunks of part[chunk][c]: 16 columns x 16 chunk lanes
+// per block, each lane summing a fixed strided subset, combined in a fixed order
 __global__ void __launch_bounds__(256) colsum_final(const float* __restrict__ part, int chunks, int n,
                                                     float* __restrict__ out, int accumulate) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= n) return;
+  __shared__ float red[16][17];
+  const int cl = threadIdx.x & 15, q = threadIdx.x >> 4;
+  const int c = blockIdx.x * 16 + cl;
   float s = 0.f;
-  for (int k = 0; k < chunks; ++k) s += part[(int64_t)k * n + c];
-  out[c] = accumulate ? out[c] + s : s;
+  if (c < n)
+    for (int k = q; k < chunks; k += 16) s += part[(int64_t)k * n + c];
+  red[q][cl] = s;
+  __syncthreads();
+  if (q == 0 && c < n) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) t += red[k][cl];
+    out[c] = accumulate ? out[c] + t : t;
+  }
 }
 
 // ---- QK-LayerNorm -------------------------------------------------------------
@@ -329,16 +342,25 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
   }
 }
 
+// gain/shift gradients of QK-LayerNorm: e = which*dh + c over 4*dh outputs,
+// 4 lanes per output summing a strided subset of the block partials
 __global__ void __launch_bounds__(256) qkln_param_final(const float* __restrict__ part, int blocks, int dh,
                                                         float* dqg, float* dqb, float* dkg, float* dkb,
                                                         int accumulate) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= 4 * dh) return;
+  __shared__ float red[4][64];
+  const int el = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int e = blockIdx.x * 64 + el;
   float s = 0.f;
-  for (int k = 0; k < blocks; ++k) s += part[(int64_t)k * 4 * dh + e];
-  const int which = e / dh, c = e % dh;
-  float* out = which == 0 ? dqg : which == 1 ? dqb : which == 2 ? dkg : dkb;
-  out[c] = accumulate ? out[c] + s : s;
+  if (e < 4 * dh)
+    for (int k = q; k < blocks; k += 4) s += part[(int64_t)k * 4 * dh + e];
+  red[q][el] = s;
+  __syncthreads();
+  if (q == 0 && e < 4 * dh) {
+    const float t = (red[0][el] + red[1][el]) + (red[2][el] + red[3][el]);
+    const int which = e / dh, c = e % dh;
+    float* out = which == 0 ? dqg : which == 1 ? dqb : which == 2 ? dkg : dkb;
+    out[c] = accumulate ? out[c] + t : t;
+  }
 }
 
 // ---- elementwise --------------------------------------------------------------
@@ -407,7 +429,8 @@ template <typename T>
 orbit_status colsum_t(const void* dy, int64_t lddy, int rows, int n, const void* x, int64_t ldx,
                       const float* mean, const float* rstd, float* out_sum, float* out_xsum, int accumulate,
                       void* ws, hipStream_t s) {
-  const int chunks = (int)cdiv(rows, kRowsPerChunk);
+  const int rpc = rows_per_chunk(rows);
+  const int chunks = (int)cdiv(rows, rpc);
   float* ps = static_cast<float*>(ws);
   float* px = ps + (int64_t)chunks * n;
   dim3 grid((unsigned)cdiv(n, kColsPerBlock), (unsigned)chunks);
@@ -415,15 +438,15 @@ orbit_status colsum_t(const void* dy, int64_t lddy, int rows, int n, const void*
                 (x ? 2.0 : 1.0) * rows * (double)n * sizeof(T)};
   if (x) {
     ORBIT_TRY(launch(ki, colsum_partial<T, true>, grid, dim3(256), 0, s, (const T*)dy, lddy, rows, n,
-                     (const T*)x, ldx, mean, rstd, ps, px));
+                     (const T*)x, ldx, mean, rstd, ps, px, rpc));
   } else {
     ORBIT_TRY(launch(ki, colsum_partial<T, false>, grid, dim3(256), 0, s, (const T*)dy, lddy, rows, n,
-                     (const T*)nullptr, (int64_t)0, (const float*)nullptr, (const float*)nullptr, ps, px));
+                     (const T*)nullptr, (int64_t)0, (const float*)nullptr, (const float*)nullptr, ps, px, rpc));
   }
   KernelInfo kf{"colsum_final", 0.0, (double)chunks * n * 4};
-  if (out_sum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s,
+  if (out_sum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 16)), dim3(256), 0, s,
                                 (const float*)ps, chunks, n, out_sum, accumulate));
-  if (x && out_xsum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s,
+  if (x && out_xsum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 16)), dim3(256), 0, s,
                                       (const float*)px, chunks, n, out_xsum, accumulate));
   return ORBIT_OK;
 }
@@ -453,7 +476,7 @@ orbit_status qk_bwd_t(void* d, int64_t ldd, const void* src, int64_t lds, const 
   ORBIT_TRY(launch(ki, qkln_bwd_kernel<T, DH>, dim3(blocks), dim3(256), 0, s, (T*)d, ldd, (const T*)src, lds,
                    mean, rstd, (const T*)qg, (const T*)kg, T_, H, H * DH, part));
   KernelInfo kf{"qkln_param_final", 0.0, 4.0 * blocks * 4 * DH};
-  return launch(kf, qkln_param_final, dim3((unsigned)cdiv(4 * DH, 256)), dim3(256), 0, s, (const float*)part,
+  return launch(kf, qkln_param_final, dim3((unsigned)cdiv(4 * DH, 64)), dim3(256), 0, s, (const float*)part,
                 blocks, DH, dqg, dqb, dkg, dkb, accumulate);
 }
 
@@ -473,7 +496,7 @@ orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const v
 }
 
 size_t colsum_workspace_bytes(int rows, int n) {
-  return align_up((size_t)2 * cdiv(rows, kRowsPerChunk) * (size_t)n * sizeof(float));
+  return align_up((size_t)2 * cdiv(rows, rows_per_chunk(rows)) * (size_t)n * sizeof(float));
 }
 
 orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int n, const void* x, int64_t ldx,

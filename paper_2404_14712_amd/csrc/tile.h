@@ -132,3 +132,134 @@ struct TileLoader {
 };
 
 }  // namespace orbit
+
+namespace orbit {
+
+// Staging of one GEMM operand tile (ROWS x KD) into a K-contiguous LDS copy
+// S[row][k] (pitch KD + 16 bytes), read from HBM either K-major
+// (X[row*ld + k]) or M/N-major (X[k*ld + row]).
+//
+// Thread mapping keeps both the HBM reads and the LDS writes conflict-free:
+// consecutive lanes take consecutive 16-byte k-chunks of one LDS row, so 8
+// lanes (bf16: 8 chunks of 8) write one full 128-byte row. For the M/N-major
+// source each thread owns an E x E block (E k-rows of E row-elements), loads
+// it as E 16-byte reads (a wave reads 8 rows x 128 contiguous bytes per
+// instruction), transposes it in registers and writes E 16-byte k-runs.
+template <typename T, int ROWS, int KD, int NT, bool KMAJ>
+struct GemmStage {
+  static constexpr int E = 16 / (int)sizeof(T);
+  static constexpr int KC = KD / E;                 // 16-byte chunks per row
+  static constexpr int PITCH = KD + E;
+  static constexpr int NCH = KMAJ ? ROWS * KC : (KD / E) * (ROWS / E);
+  static constexpr int PER = (NCH + NT - 1) / NT;
+  static constexpr int REGS = KMAJ ? PER : PER * E;
+  static_assert(ROWS % E == 0 && KD % E == 0, "tile shape");
+  U128 r[REGS];
+
+  ORBIT_DEV void load(const T* X, const T* X2, int ksplit, int64_t ld, int row0, int rlim, int k0, int kend,
+                      int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (KMAJ) {
+        const int row = c / KC, kc = c % KC;
+        const int gr = row0 + row, gk = k0 + kc * E;
+        r[i] = (c < NCH && gr < rlim && gk < kend) ? ld128(X + (int64_t)gr * ld + gk) : zero128();
+      } else {
+        const int kc = c % KC, rc = c / KC;
+        const int gr = row0 + rc * E;
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          const int gk = k0 + kc * E + j;
+          const bool ok = c < NCH && gr < rlim && gk < kend;
+          const T* base = (X2 && gk >= ksplit) ? X2 + (int64_t)(gk - ksplit) * ld : X + (int64_t)gk * ld;
+          r[i * E + j] = ok ? ld128(base + gr) : zero128();
+        }
+      }
+    }
+  }
+
+  ORBIT_DEV void store(T* S, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c >= NCH) continue;
+      if (KMAJ) {
+        const int row = c / KC, kc = c % KC;
+        st128(S + row * PITCH + kc * E, r[i]);
+      } else {
+        const int kc = c % KC, rc = c / KC;
+        T* base = S + (rc * E) * PITCH + kc * E;
+        if constexpr (sizeof(T) == 2) {
+          // in[j] = k-row j holds row-elements e = 0..7 (2 per word);
+          // out[e] = row e holds k-values j = 0..7
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int w = e >> 1;
+            U128 o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const uint32_t lo = r[i * 8 + 2 * q].w[w], hi = r[i * 8 + 2 * q + 1].w[w];
+              o.w[q] = (e & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+            }
+            st128(base + e * PITCH, o);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            U128 o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) o.w[q] = r[i * 4 + q].w[e];
+            st128(base + e * PITCH, o);
+          }
+        }
+      }
+    }
+  }
+
+  // M/N-major source only: the transposed copy with mean[row] subtracted from
+  // every element first (float32 arithmetic, rounded back to T)
+  ORBIT_DEV void store_sub(T* S, int tid, const float* mean) const {
+    static_assert(!KMAJ, "store_sub applies to the M/N-major source");
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c >= NCH) continue;
+      const int kc = c % KC, rc = c / KC;
+      T* base = S + (rc * E) * PITCH + kc * E;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float m = mean[rc * E + e];
+        float f[8];
+#pragma unroll
+        for (int j = 0; j < E; ++j) f[j] = elem(r[i * E + j], e) - m;
+        st128(base + e * PITCH, pack(f, (T*)nullptr));
+      }
+    }
+  }
+
+  // M/N-major source only: the untransposed copy D[k][row] (pitch dpitch), i.e.
+  // the source rows as they are in HBM
+  ORBIT_DEV void store_rows(T* D, int dpitch, int tid) const {
+    static_assert(!KMAJ, "store_rows applies to the M/N-major source");
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c >= NCH) continue;
+      const int kc = c % KC, rc = c / KC;
+#pragma unroll
+      for (int j = 0; j < E; ++j) st128(D + (kc * E + j) * dpitch + rc * E, r[i * E + j]);
+    }
+  }
+
+  static ORBIT_DEV float elem(const U128& u, int e) {
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t w = u.w[e >> 1];
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+      return __uint_as_float(u.w[e]);
+    }
+  }
+};
+
+}  // namespace orbit
