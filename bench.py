@@ -77,7 +77,6 @@ def device_inputs(c, device):
     params = {"blocks": [P(synth.block_params(c, i)) for i in range(c.blocks)]}
     z = dims_for(c)
     inputs = {}
-    tdt = torch.bfloat16 if c.dtype == "bf16" else torch.float32
     if z.mode == "full":
         params["embed"] = P(synth.embed_params(c))
         params["agg"] = P(synth.agg_params(c))
@@ -86,19 +85,13 @@ def device_inputs(c, device):
         inputs["tgt"] = D(synth.target(c), "f32")
     else:
         # activations and the upstream gradient N(0, 1), drawn on the device (seeded)
-        gen = torch.Generator(device=device)
-        gen.manual_seed(synth.BASE_SEED + 100 * c.cfg)
-        inputs["dy"] = torch.randn(c.B, c.L, c.d, generator=gen, device=device, dtype=torch.float32).to(tdt)
+        inputs["dy"] = synth.device_normal(c.cfg, "dy", (c.B, c.L, c.d), c.dtype, device)
         if z.mode == "agg_blocks":
             params["agg"] = P(synth.agg_params(c))
-            tok = torch.empty(c.B, c.L, c.V, c.d, device=device, dtype=tdt)
-            for b in range(c.B):
-                for l0 in range(0, c.L, 256):
-                    tok[b, l0:l0 + 256] = torch.randn(min(256, c.L - l0), c.V, c.d, generator=gen, device=device,
-                                                      dtype=torch.float32).to(tdt)
-            inputs["tok"] = tok
+            inputs["tok"] = synth.device_normal(c.cfg, "tok", (c.B * c.L, c.V, c.d), c.dtype, device,
+                                                chunk_rows=256).view(c.B, c.L, c.V, c.d)
         else:
-            inputs["x"] = torch.randn(c.B, c.L, c.d, generator=gen, device=device, dtype=torch.float32).to(tdt)
+            inputs["x"] = synth.device_normal(c.cfg, "x", (c.B, c.L, c.d), c.dtype, device)
     return params, inputs
 
 
@@ -127,16 +120,24 @@ def cpu_baseline(c) -> dict:
         sample = f"128 of {c.L} tokens, 1 of {c.blocks} blocks, aggregation over all {c.V} variables"
     zs = dims_for(s)
     blocks = [synth.block_params(s, i) for i in range(s.blocks)]
-    t0 = time.perf_counter()
+
     if zs.mode == "full":
-        O.model_fwd_bwd(synth.image(s), synth.target(s), synth.embed_params(s), synth.agg_params(s), blocks,
-                        synth.head_params(s), p=4, agg_heads=s.agg_heads, heads=s.heads, qk_norm=s.qk_norm)
+        args = (synth.image(s), synth.target(s), synth.embed_params(s), synth.agg_params(s), blocks,
+                synth.head_params(s))
     else:
-        x = synth.activations(s, "x")
-        dy = synth.normal(s.cfg, "dy", x.shape)
+        x0 = synth.activations(s, "x")
+        dy = synth.normal(s.cfg, "dy", x0.shape)
         if zs.mode == "agg_blocks":
             tok = np.stack([synth.tokens_chunk(s, b, 0, s.L) for b in range(s.B)])
-            x, ca = O.agg_fwd(tok, synth.agg_params(s), s.agg_heads)
+            agg = synth.agg_params(s)
+
+    def once():
+        if zs.mode == "full":
+            O.model_fwd_bwd(*args, p=4, agg_heads=s.agg_heads, heads=s.heads, qk_norm=s.qk_norm)
+            return
+        x = x0
+        if zs.mode == "agg_blocks":
+            x, ca = O.agg_fwd(tok, agg, s.agg_heads)
         caches = []
         for p in blocks:
             x, cc = O.block_fwd(x, p, s.heads, s.qk_norm)
@@ -145,9 +146,19 @@ def cpu_baseline(c) -> dict:
         for p, cc in zip(blocks[::-1], caches[::-1]):
             g, _ = O.block_bwd(g, cc, p)
         if zs.mode == "agg_blocks":
-            O.agg_bwd(g, ca, synth.agg_params(s))
+            O.agg_bwd(g, ca, agg)
+
+    # repeat the sample until about 10 s of CPU work have been timed
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        once()
+        reps += 1
+        if time.perf_counter() - t0 >= 10.0 or reps >= 100:
+            break
     dt = time.perf_counter() - t0
-    fl = pass_flops(zs)["total"]
+    fl = pass_flops(zs)["total"] * reps
+    sample += f"; repeated {reps} times"
     threads = None
     try:
         from threadpoolctl import threadpool_info
@@ -159,16 +170,32 @@ def cpu_baseline(c) -> dict:
             "kind": "oracle", "sample": sample, "seconds": round(dt, 3), "sample_flops": fl}
 
 
-def read_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` measured with rocprofv3 counters, if a
-    summary for the current kernel exists (profiles/traffic.json)."""
+def source_digest() -> str:
+    """sha256 over the library's HIP/C++ sources and header: counter figures
+    taken from another version of the kernels are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2404_14712_amd", "csrc")
+    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)) + [os.path.join(ROOT, "include", "orbit.h")]
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
+def read_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload`, measured with rocprofv3
+    FETCH_SIZE / WRITE_SIZE counters scaled by a plain copy's readings
+    (profiles/traffic.json); None when absent or taken from other sources."""
     f = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(f):
         return None
     try:
         t = json.load(open(f))
-        e = t.get(kernel)
-        return None if e is None else e.get("bytes_per_launch")
+        if t.get("source_sha256") != source_digest() or t.get("workload") != workload:
+            return None
+        e = t["kernels"].get(kernel)
+        return None if e is None else round(e["fetch_bytes_per_launch"] + e["write_bytes_per_launch"])
     except Exception:
         return None
 
@@ -180,6 +207,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="115m", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 1 GiB device copy (reference for HBM byte counters) and exit")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the model; runs on more than one GPU are not part "
@@ -194,6 +223,17 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if a.copy_calibration:
+        # a streaming elementwise kernel that reads and writes exactly 1 GiB each
+        n = 1 << 28
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"kernel": "torch neg (float32)", "launches": 3,
+                                               "read_bytes_per_launch": 4 * n, "write_bytes_per_launch": 4 * n}}))
+        return
     lib = load()
     c = synth.CONFIGS[WORKLOADS[a.workload]]
     z = dims_for(c)
@@ -252,7 +292,7 @@ def main():
         achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof.update({"traffic": read_traffic(dominant), "kernel": dominant, "launches": dk["launches"],
+    roof.update({"traffic": read_traffic(dominant, a.workload), "kernel": dominant, "launches": dk["launches"],
                  "avg_launch_ms": round(k_avg_ms, 5), "algorithmic_flops_per_launch": k_flops,
                  "algorithmic_bytes_per_launch": k_bytes})
 

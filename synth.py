@@ -233,3 +233,22 @@ def small_config(cfg: int, **over) -> Config:
     """A copy of a config with some sizes replaced (parity cases that the oracle
     finishes in seconds)."""
     return dataclasses.replace(CONFIGS[cfg], **over)
+
+
+def device_normal(cfg: int, name: str, shape, dtype: str, device, chunk_rows: int = 0):
+    """N(0, 1) tensor drawn on the device by torch's seeded generator, for
+    inputs too large to draw on the host (full-size token and activation
+    tensors). Drawn in float32 and rounded to the dtype. With ``chunk_rows``,
+    the leading axis is drawn in slabs of that many rows (bounds the float32
+    temporary). Deterministic for a given device type and torch version."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed((BASE_SEED * 1000 + int(cfg) * 7919 + zlib.crc32(name.encode())) % (2 ** 63))
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    out = torch.empty(*shape, dtype=tdt, device=device)
+    n0 = shape[0]
+    step = chunk_rows if chunk_rows > 0 else n0
+    for a in range(0, n0, step):
+        b = min(n0, a + step)
+        out[a:b] = torch.randn(b - a, *shape[1:], generator=gen, device=device, dtype=torch.float32).to(tdt)
+    return out
