@@ -127,7 +127,7 @@ struct BlockWs {
   void* dO;    // [T, A]
   void* dqkv;  // [T, 3A]
   float* D;    // attention backward workspace
-  void* cws;
+  float *p_fc1, *p_fc2, *p_ln2, *p_proj, *p_qkv, *p_ln1;  // column-sum partials
   void* qws;
   void* gws;
   size_t gws_bytes;
@@ -162,7 +162,14 @@ size_t block_ws_layout(const BlockDims& z, void* base, size_t bytes, BlockWs* w,
   t.dO = c.take<char>(z.T * z.A * e);
   t.dqkv = c.take<char>(z.T * 3 * z.A * e);
   t.D = static_cast<float*>(static_cast<void*>(c.take<char>(attn_bwd_workspace_bytes(z.B, z.H, z.L, z.dh))));
-  t.cws = c.take<char>(colsum_workspace_bytes((int)z.T, std::max({z.d, 3 * z.A, z.F})));
+  // partials of the block's column reductions (all finished by one launch)
+  const int T = (int)z.T;
+  t.p_fc1 = c.take<float>(colsum_part_bytes(T, z.F, false) / sizeof(float));
+  t.p_fc2 = c.take<float>(colsum_part_bytes(T, z.d, false) / sizeof(float));
+  t.p_ln2 = c.take<float>(colsum_part_bytes(T, z.d, true) / sizeof(float));
+  t.p_proj = c.take<float>(colsum_part_bytes(T, z.d, false) / sizeof(float));
+  t.p_qkv = c.take<float>(colsum_part_bytes(T, 3 * z.A, false) / sizeof(float));
+  t.p_ln1 = c.take<float>(colsum_part_bytes(T, z.d, true) / sizeof(float));
   t.qws = c.take<char>(qk_norm_bwd_workspace_bytes(z.dh));
   const size_t g = block_gemm_ws(z);
   t.gws = c.take<char>(g);
@@ -303,7 +310,7 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.M = z.F; g.N = z.d; g.K = T;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(colsum(dt, dy, z.d, T, z.d, nullptr, 0, nullptr, nullptr, gr->b_fc2, nullptr, accumulate, w.cws, s));
+  ColFinal fin;  // parameter-gradient column sums, finished together at the end
   {
     Gemm g; g.dtype = dt; g.tag = "fc2_dx";
     g.A = dy; g.lda = z.d; g.B = p->w_fc2; g.ldb = z.d; g.b_kmajor = true;
@@ -317,7 +324,14 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.M = z.d; g.N = z.F; g.K = T;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(colsum(dt, w.du, z.F, T, z.F, nullptr, 0, nullptr, nullptr, gr->b_fc1, nullptr, accumulate, w.cws, s));
+  {
+    ColJob j[2];
+    j[0].src = w.du; j[0].ld = z.F; j[0].n = z.F; j[0].part = w.p_fc1; j[0].out_sum = gr->b_fc1;
+    j[1].src = dy; j[1].ld = z.d; j[1].n = z.d; j[1].part = w.p_fc2; j[1].out_sum = gr->b_fc2;
+    ORBIT_TRY(colsum_partials(dt, j, 2, T, s));
+    fin.add_job(j[0], T);
+    fin.add_job(j[1], T);
+  }
   {
     Gemm g; g.dtype = dt; g.tag = "fc1_dx";
     g.A = w.du; g.lda = z.F; g.B = p->w_fc1; g.ldb = z.F; g.b_kmajor = true;
@@ -325,7 +339,15 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, sv.x1, z.d, sv.mu2, sv.r2, p->ln2_g, dy, w.dx1, z.d, T, z.d, s));
-  ORBIT_TRY(colsum(dt, w.dh, z.d, T, z.d, sv.x1, z.d, sv.mu2, sv.r2, gr->ln2_b, gr->ln2_g, accumulate, w.cws, s));
+  {
+    ColJob j[2];
+    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = sv.x1; j[0].ldx = z.d; j[0].mean = sv.mu2;
+    j[0].rstd = sv.r2; j[0].part = w.p_ln2; j[0].out_sum = gr->ln2_b; j[0].out_xsum = gr->ln2_g;
+    j[1].src = w.dx1; j[1].ld = z.d; j[1].n = z.d; j[1].part = w.p_proj; j[1].out_sum = gr->b_proj;
+    ORBIT_TRY(colsum_partials(dt, j, 2, T, s));
+    fin.add_job(j[0], T);
+    fin.add_job(j[1], T);
+  }
   // attention sub-layer
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dw";
@@ -334,7 +356,6 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.M = z.A; g.N = z.d; g.K = T;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(colsum(dt, w.dx1, z.d, T, z.d, nullptr, 0, nullptr, nullptr, gr->b_proj, nullptr, accumulate, w.cws, s));
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dx";
     g.A = w.dx1; g.lda = z.d; g.B = p->w_proj; g.ldb = z.d; g.b_kmajor = true;
@@ -356,7 +377,7 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(attn_bwd(dt, io, sv.o, z.A, 0, sv.lse, w.dO, z.A, dq, dq + z.A * e, dq + 2 * z.A * e, 3 * z.A, w.D, s));
   if (z.qk) {
     ORBIT_TRY(qk_norm_bwd(dt, w.dqkv, 3 * z.A, sv.qkv, 3 * z.A, sv.qmu, sv.qr, p->qn_g, p->kn_g, gr->qn_g, gr->qn_b,
-                          gr->kn_g, gr->kn_b, accumulate, T, z.H, z.dh, w.qws, s));
+                          gr->kn_g, gr->kn_b, accumulate, T, z.H, z.dh, w.qws, &fin, s));
   } else if (!acc) {
     ORBIT_TRY(fill_f32(gr->qn_g, z.dh, 0.f, s));
     ORBIT_TRY(fill_f32(gr->qn_b, z.dh, 0.f, s));
@@ -370,8 +391,6 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.M = z.d; g.N = 3 * z.A; g.K = T;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(colsum(dt, w.dqkv, 3 * z.A, T, 3 * z.A, nullptr, 0, nullptr, nullptr, gr->b_qkv, nullptr, accumulate,
-                   w.cws, s));
   {
     Gemm g; g.dtype = dt; g.tag = "qkv_dx";
     g.A = w.dqkv; g.lda = 3 * z.A; g.B = p->w_qkv; g.ldb = 3 * z.A; g.b_kmajor = true;
@@ -379,8 +398,16 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, x, z.d, sv.mu1, sv.r1, p->ln1_g, w.dx1, dx, z.d, T, z.d, s));
-  ORBIT_TRY(colsum(dt, w.dh, z.d, T, z.d, x, z.d, sv.mu1, sv.r1, gr->ln1_b, gr->ln1_g, accumulate, w.cws, s));
-  return ORBIT_OK;
+  {
+    ColJob j[2];
+    j[0].src = w.dqkv; j[0].ld = 3 * z.A; j[0].n = 3 * z.A; j[0].part = w.p_qkv; j[0].out_sum = gr->b_qkv;
+    j[1].src = w.dh; j[1].ld = z.d; j[1].n = z.d; j[1].x = x; j[1].ldx = z.d; j[1].mean = sv.mu1;
+    j[1].rstd = sv.r1; j[1].part = w.p_ln1; j[1].out_sum = gr->ln1_b; j[1].out_xsum = gr->ln1_g;
+    ORBIT_TRY(colsum_partials(dt, j, 2, T, s));
+    fin.add_job(j[0], T);
+    fin.add_job(j[1], T);
+  }
+  return fin.run(accumulate, s);
 }
 
 // ---------------------------------------------------------------------------

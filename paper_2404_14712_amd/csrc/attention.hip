@@ -539,13 +539,19 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
   // per (sample, head) feature sums of q and k over the sequence
   float* qsum = D + (int64_t)io.B * io.H * io.L;
   float* ksum = qsum + (int64_t)io.B * io.H * DH;
-  void* cws = ksum + (int64_t)io.B * io.H * DH;
+  float* cws = ksum + (int64_t)io.B * io.H * DH;
   const int A = io.H * DH;
-  for (int bb = 0; bb < io.B; ++bb) {
-    ORBIT_TRY(colsum(sizeof(T) == 2 ? ORBIT_BF16 : ORBIT_F32, static_cast<const T*>(io.q) + (int64_t)bb * io.L * io.ldq,
-                     io.ldq, io.L, A, nullptr, 0, nullptr, nullptr, qsum + (int64_t)bb * A, nullptr, 0, cws, s));
-    ORBIT_TRY(colsum(sizeof(T) == 2 ? ORBIT_BF16 : ORBIT_F32, static_cast<const T*>(io.k) + (int64_t)bb * io.L * io.ldk,
-                     io.ldk, io.L, A, nullptr, 0, nullptr, nullptr, ksum + (int64_t)bb * A, nullptr, 0, cws, s));
+  {
+    ColJob j[2];
+    j[0].src = io.q; j[0].ld = io.ldq; j[0].sbatch = (int64_t)io.L * io.ldq; j[0].n = A; j[0].batch = io.B;
+    j[0].part = cws; j[0].out_sum = qsum; j[0].sout = A;
+    j[1].src = io.k; j[1].ld = io.ldk; j[1].sbatch = (int64_t)io.L * io.ldk; j[1].n = A; j[1].batch = io.B;
+    j[1].part = cws + colsum_part_bytes(io.L, A, false, io.B) / sizeof(float); j[1].out_sum = ksum; j[1].sout = A;
+    ORBIT_TRY(colsum_partials(sizeof(T) == 2 ? ORBIT_BF16 : ORBIT_F32, j, 2, io.L, s));
+    ColFinal f;
+    f.add_job(j[0], io.L);
+    f.add_job(j[1], io.L);
+    ORBIT_TRY(f.run(0, s));
   }
   BwdArgs a{io.q, io.k, io.v, dO, lse, D, qsum, ksum, dq, dk, dv, io.ldq, io.ldk, io.ldv, lddo, ldg, io.H, io.L,
             kLog2e / sqrtf((float)DH), 1.f / sqrtf((float)DH)};
@@ -562,7 +568,7 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
 }  // namespace
 
 size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh) {
-  return align_up((size_t)B * H * (L + 2 * dh) * sizeof(float)) + colsum_workspace_bytes(L, H * dh);
+  return align_up((size_t)B * H * (L + 2 * dh) * sizeof(float)) + 2 * colsum_part_bytes(L, H * dh, false, B);
 }
 
 orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32,

@@ -211,7 +211,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
       for (int v = 0; v < 16; ++v)
         ew[((v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * EP + j * 32 + (lane & 31)] = acc[i][j][v];
     __syncthreads();
-#pragma unroll
+    // kept rolled, so that the unrolled loops above index the accumulators statically
+#pragma unroll 1
     for (int it = 0; it < 32 / RPI; ++it) {
       const int rl = it * RPI + lane / LPR;
       const int cl = (lane % LPR) * 8;

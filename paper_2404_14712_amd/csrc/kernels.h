@@ -1,6 +1,8 @@
 // Host launchers of the non-GEMM kernels. Each enqueues on `s` and returns a
 // status; shapes are validated by the callers in abi.cpp.
 #pragma once
+#include <vector>
+
 #include "common.h"
 
 namespace orbit {
@@ -16,9 +18,36 @@ orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const v
                            void* dx, int64_t lddx, int rows, int n, hipStream_t s);
 
 // ---- deterministic column reductions over rows ----------------------------
-// Partials of sum_r dy[r, c] and (if x) sum_r dy[r, c] * xhat[r, c] with
-// xhat = (x - mean[r]) * rstd[r]; then a fixed-order final sum into float32
-// outputs (overwrite or accumulate). Workspace: colsum_workspace_bytes.
+// Phase 1 (colsum_partials, one launch for up to kColMaxJobs jobs over the
+// same number of rows): per-chunk partial sums of src[r, c] and, for LN jobs
+// (x != null), of src[r, c] * xhat[r, c] with xhat = (x - mean[r]) * rstd[r],
+// into the job's `part` buffer (colsum_part_bytes). A job may cover `batch`
+// independent row blocks (src + b * sbatch, outputs at out + b * sout).
+// Phase 2 (ColFinal): fixed-order sums of the partials into float32 outputs
+// (overwrite or accumulate), any number of outputs per launch.
+constexpr int kColMaxJobs = 8;
+constexpr int kColMaxFinal = 16;
+struct ColJob {
+  const void* src = nullptr; int64_t ld = 0; int64_t sbatch = 0;
+  const void* x = nullptr; int64_t ldx = 0; int64_t sxbatch = 0;
+  const float* mean = nullptr; const float* rstd = nullptr;
+  int n = 0, batch = 1;
+  float* part = nullptr;
+  float* out_sum = nullptr; float* out_xsum = nullptr; int64_t sout = 0;
+};
+int colsum_chunks(int rows);
+size_t colsum_part_bytes(int rows, int n, bool ln, int batch = 1);
+orbit_status colsum_partials(orbit_dtype dt, ColJob* jobs, int njobs, int rows, hipStream_t s);
+class ColFinal {
+ public:
+  void add(const float* part, int64_t ldp, int chunks, int n, float* out);
+  void add_job(const ColJob& J, int rows);
+  orbit_status run(int accumulate, hipStream_t s);
+ private:
+  struct Item { const float* part; int64_t ldp; float* out; int chunks, n; };
+  std::vector<Item> items;
+};
+// both phases for one (optionally LN) job; workspace: colsum_workspace_bytes
 size_t colsum_workspace_bytes(int rows, int n);
 orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int n,
                     const void* x, int64_t ldx, const float* mean, const float* rstd,
@@ -33,12 +62,13 @@ orbit_status colsum_f32(const float* dy, int64_t lddy, int rows, int n, float* o
 orbit_status qk_norm_fwd(orbit_dtype dt, const void* src, int64_t lds, void* dst, int64_t ldd,
                          const void* qg, const void* qb, const void* kg, const void* kb,
                          float* mean, float* rstd, int T, int H, int dh, float eps, hipStream_t s);
-// in place on dq/dk (rows of `d`, ld ldd): dxhat -> dx; gain/shift grads.
+// in place on dq/dk (rows of `d`, ld ldd): dxhat -> dx; gain/shift grads
+// (their final sums are queued on `fin` when given, else run here).
 size_t qk_norm_bwd_workspace_bytes(int dh);
 orbit_status qk_norm_bwd(orbit_dtype dt, void* d, int64_t ldd, const void* src, int64_t lds,
                          const float* mean, const float* rstd, const void* qg, const void* kg,
                          float* dqg, float* dqb, float* dkg, float* dkb, int accumulate,
-                         int T, int H, int dh, void* ws, hipStream_t s);
+                         int T, int H, int dh, void* ws, ColFinal* fin, hipStream_t s);
 
 // ---- attention: O = softmax(q k^T / sqrt(dh)) v per (sample, head) --------
 struct AttnIO {

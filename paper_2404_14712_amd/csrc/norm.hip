@@ -137,80 +137,119 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, i
 }
 
 // ---- column sums ------------------------------------------------------------
-constexpr int kColsPerBlock = 512;  // 64 threads x 8 columns
-constexpr int kMaxChunks = 64;      // row chunks (partials per column)
+// Phase 1: a grid of (column block, row chunk) blocks, 1024 threads each: 64
+// lanes x 8 consecutive columns, 16 row lanes striding over the chunk with 4
+// rows in flight; the 16 row lanes are combined in LDS in a fixed order and
+// the chunk's partial row is stored. Phase 2 sums the chunk partials of any
+// number of outputs in a fixed order (one launch for a whole backward call).
+constexpr int kCsCols = 512;      // columns per block (64 lanes x 8)
+constexpr int kCsRowLanes = 16;   // row lanes per block
+constexpr int kCsMaxChunks = 32;
 
-int rows_per_chunk(int rows) { return (int)std::max<int64_t>(16, cdiv(cdiv(rows, kMaxChunks), 4) * 4); }
+int cs_rows_per_chunk(int rows) {
+  return (int)std::max<int64_t>(64, cdiv(cdiv(rows, kCsMaxChunks), 16) * 16);
+}
 
-template <typename T, bool XS>
-__global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ dy, int64_t lddy, int rows,
-                                                      int n, const T* __restrict__ x, int64_t ldx,
-                                                      const float* __restrict__ mean,
-                                                      const float* __restrict__ rstd,
-                                                      float* __restrict__ part_s,
-                                                      float* __restrict__ part_x, int rpc) {
-  __shared__ float sm[2][4][kColsPerBlock];
+struct CsJobK {
+  const void* src; int64_t ld; int64_t sbatch;   // batch b: src + b * sbatch
+  const void* x; int64_t ldx; int64_t sxbatch;
+  const float* mean; const float* rstd;
+  float* part; int64_t spart;                     // [batch][chunks (x2 for LN)][n]
+  int n, cb0, batch;
+};
+struct CsArgs {
+  CsJobK job[kColMaxJobs];
+  int njobs, rows, rpc, chunks;
+};
+
+template <typename T>
+__global__ void __launch_bounds__(1024) colsum_partials_kernel(CsArgs a) {
+  __shared__ float red[2][kCsRowLanes][kCsCols + 4];
+  int j = 0;
+  while (j + 1 < a.njobs && (int)blockIdx.x >= a.job[j + 1].cb0) ++j;
+  const CsJobK& J = a.job[j];
+  const int cb = (int)blockIdx.x - J.cb0;
+  const int bz = blockIdx.z;
+  if (bz >= J.batch) return;
+  const bool ln = J.x != nullptr;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int c0 = blockIdx.x * kColsPerBlock + tx * 8;
+  const int c0 = cb * kCsCols + tx * 8;
   const int chunk = blockIdx.y;
-  const int r0 = chunk * rpc, r1 = min(rows, r0 + rpc);
-  float as[8], ax[8];
+  const int r0 = chunk * a.rpc, r1 = min(a.rows, r0 + a.rpc);
+  const T* src = static_cast<const T*>(J.src) + bz * J.sbatch;
+  const T* xs = ln ? static_cast<const T*>(J.x) + bz * J.sxbatch : nullptr;
+  float s[8], sx[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) as[i] = ax[i] = 0.f;
-  if (c0 < n) {
-    for (int r = r0 + ty; r < r1; r += 4) {
-      float d8[8];
-      load8(dy + (int64_t)r * lddy + c0, d8);
+  for (int i = 0; i < 8; ++i) s[i] = sx[i] = 0.f;
+  if (c0 < J.n) {
+    for (int rb = r0 + ty; rb < r1; rb += 4 * kCsRowLanes) {
+      float d[4][8], xv[4][8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) as[i] += d8[i];
-      if (XS) {
-        float x8[8];
-        load8(x + (int64_t)r * ldx + c0, x8);
-        const float mu = mean[r], rs = rstd[r];
+      for (int u = 0; u < 4; ++u) {
+        const int r = rb + u * kCsRowLanes;
+        if (r < r1) {
+          load8(src + (int64_t)r * J.ld + c0, d[u]);
+          if (ln) load8(xs + (int64_t)r * J.ldx + c0, xv[u]);
+        }
+      }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) ax[i] += d8[i] * ((x8[i] - mu) * rs);
+      for (int u = 0; u < 4; ++u) {
+        const int r = rb + u * kCsRowLanes;
+        if (r < r1) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) s[i] += d[u][i];
+          if (ln) {
+            const float mu = J.mean[(int64_t)bz * a.rows + r], rs = J.rstd[(int64_t)bz * a.rows + r];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) sx[i] += d[u][i] * ((xv[u][i] - mu) * rs);
+          }
+        }
       }
     }
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    sm[0][ty][tx * 8 + i] = as[i];
-    sm[1][ty][tx * 8 + i] = ax[i];
+    red[0][ty][tx * 8 + i] = s[i];
+    red[1][ty][tx * 8 + i] = sx[i];
   }
   __syncthreads();
-  // 256 threads reduce 512 columns (2 each) over the 4 row lanes, fixed order
+  // threads 0..511: the sum of column c; 512..1023: the x-weighted sum
+  const int which = threadIdx.x / kCsCols, cc = threadIdx.x % kCsCols;
+  const int c = cb * kCsCols + cc;
+  if (c < J.n && (which == 0 || ln)) {
+    float t = 0.f;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int cc = threadIdx.x + h * 256;
-    const int c = blockIdx.x * kColsPerBlock + cc;
-    if (c < n) {
-      const float s = (sm[0][0][cc] + sm[0][1][cc]) + (sm[0][2][cc] + sm[0][3][cc]);
-      part_s[(int64_t)chunk * n + c] = s;
-      if (XS) {
-        const float t = (sm[1][0][cc] + sm[1][1][cc]) + (sm[1][2][cc] + sm[1][3][cc]);
-        part_x[(int64_t)chunk * n + c] = t;
-      }
-    }
+    for (int q = 0; q < kCsRowLanes; ++q) t += red[which][q][cc];
+    J.part[bz * J.spart + ((int64_t)which * a.chunks + chunk) * J.n + c] = t;
   }
 }
 
-// out[c] (+)= sum over chunks of part[chunk][c]: 16 columns x 16 chunk lanes
-// per block, each lane summing a fixed strided subset, combined in a fixed order
-__global__ void __launch_bounds__(256) colsum_final(const float* __restrict__ part, int chunks, int n,
-                                                    float* __restrict__ out, int accumulate) {
-  __shared__ float red[16][17];
-  const int cl = threadIdx.x & 15, q = threadIdx.x >> 4;
-  const int c = blockIdx.x * 16 + cl;
+struct CsFinalK {
+  const float* part; int64_t ldp;   // partial k of element e at part[k * ldp + e]
+  float* out;
+  int chunks, n, cb0;
+};
+struct CsFinalArgs {
+  CsFinalK item[kColMaxFinal];
+  int nitems, accumulate;
+};
+
+// 64 elements x 4 chunk lanes per block; fixed-order sums
+__global__ void __launch_bounds__(256) colsum_final_kernel(CsFinalArgs a) {
+  __shared__ float red[4][64];
+  int j = 0;
+  while (j + 1 < a.nitems && (int)blockIdx.x >= a.item[j + 1].cb0) ++j;
+  const CsFinalK& I = a.item[j];
+  const int el = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int e = ((int)blockIdx.x - I.cb0) * 64 + el;
   float s = 0.f;
-  if (c < n)
-    for (int k = q; k < chunks; k += 16) s += part[(int64_t)k * n + c];
-  red[q][cl] = s;
+  if (e < I.n)
+    for (int k = q; k < I.chunks; k += 4) s += I.part[(int64_t)k * I.ldp + e];
+  red[q][el] = s;
   __syncthreads();
-  if (q == 0 && c < n) {
-    float t = 0.f;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) t += red[k][cl];
-    out[c] = accumulate ? out[c] + t : t;
+  if (q == 0 && e < I.n) {
+    const float t = (red[0][el] + red[1][el]) + (red[2][el] + red[3][el]);
+    I.out[e] = a.accumulate ? I.out[e] + t : t;
   }
 }
 
@@ -342,27 +381,6 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
   }
 }
 
-// gain/shift gradients of QK-LayerNorm: e = which*dh + c over 4*dh outputs,
-// 4 lanes per output summing a strided subset of the block partials
-__global__ void __launch_bounds__(256) qkln_param_final(const float* __restrict__ part, int blocks, int dh,
-                                                        float* dqg, float* dqb, float* dkg, float* dkb,
-                                                        int accumulate) {
-  __shared__ float red[4][64];
-  const int el = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int e = blockIdx.x * 64 + el;
-  float s = 0.f;
-  if (e < 4 * dh)
-    for (int k = q; k < blocks; k += 4) s += part[(int64_t)k * 4 * dh + e];
-  red[q][el] = s;
-  __syncthreads();
-  if (q == 0 && e < 4 * dh) {
-    const float t = (red[0][el] + red[1][el]) + (red[2][el] + red[3][el]);
-    const int which = e / dh, c = e % dh;
-    float* out = which == 0 ? dqg : which == 1 ? dqb : which == 2 ? dkg : dkb;
-    out[c] = accumulate ? out[c] + t : t;
-  }
-}
-
 // ---- elementwise --------------------------------------------------------------
 template <typename T>
 __global__ void __launch_bounds__(256) cast_kernel(const float* __restrict__ src, T* __restrict__ dst, int64_t n) {
@@ -425,32 +443,6 @@ orbit_status ln_bwd_dispatch(const void* dy, int64_t lddy, const void* x, int64_
   return ORBIT_E_UNSUPPORTED;
 }
 
-template <typename T>
-orbit_status colsum_t(const void* dy, int64_t lddy, int rows, int n, const void* x, int64_t ldx,
-                      const float* mean, const float* rstd, float* out_sum, float* out_xsum, int accumulate,
-                      void* ws, hipStream_t s) {
-  const int rpc = rows_per_chunk(rows);
-  const int chunks = (int)cdiv(rows, rpc);
-  float* ps = static_cast<float*>(ws);
-  float* px = ps + (int64_t)chunks * n;
-  dim3 grid((unsigned)cdiv(n, kColsPerBlock), (unsigned)chunks);
-  KernelInfo ki{sizeof(T) == 2 ? "colsum_partial<bf16>" : "colsum_partial<f32>", 0.0,
-                (x ? 2.0 : 1.0) * rows * (double)n * sizeof(T)};
-  if (x) {
-    ORBIT_TRY(launch(ki, colsum_partial<T, true>, grid, dim3(256), 0, s, (const T*)dy, lddy, rows, n,
-                     (const T*)x, ldx, mean, rstd, ps, px, rpc));
-  } else {
-    ORBIT_TRY(launch(ki, colsum_partial<T, false>, grid, dim3(256), 0, s, (const T*)dy, lddy, rows, n,
-                     (const T*)nullptr, (int64_t)0, (const float*)nullptr, (const float*)nullptr, ps, px, rpc));
-  }
-  KernelInfo kf{"colsum_final", 0.0, (double)chunks * n * 4};
-  if (out_sum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 16)), dim3(256), 0, s,
-                                (const float*)ps, chunks, n, out_sum, accumulate));
-  if (x && out_xsum) ORBIT_TRY(launch(kf, colsum_final, dim3((unsigned)cdiv(n, 16)), dim3(256), 0, s,
-                                      (const float*)px, chunks, n, out_xsum, accumulate));
-  return ORBIT_OK;
-}
-
 template <typename T, int DH>
 orbit_status qk_fwd_t(const void* src, int64_t lds, void* dst, int64_t ldd, const void* qg, const void* qb,
                       const void* kg, const void* kb, float* mean, float* rstd, int T_, int H, float eps,
@@ -467,7 +459,7 @@ orbit_status qk_fwd_t(const void* src, int64_t lds, void* dst, int64_t ldd, cons
 template <typename T, int DH>
 orbit_status qk_bwd_t(void* d, int64_t ldd, const void* src, int64_t lds, const float* mean, const float* rstd,
                       const void* qg, const void* kg, float* dqg, float* dqb, float* dkg, float* dkb,
-                      int accumulate, int T_, int H, void* ws, hipStream_t s) {
+                      int accumulate, int T_, int H, void* ws, ColFinal* fin, hipStream_t s) {
   const int64_t rows = (int64_t)T_ * 2 * H;
   const int blocks = (int)std::min<int64_t>(kQkBwdBlocks, cdiv(rows, 256 / (DH / 8)));
   float* part = static_cast<float*>(ws);
@@ -475,9 +467,11 @@ orbit_status qk_bwd_t(void* d, int64_t ldd, const void* src, int64_t lds, const 
                 3.0 * rows * DH * sizeof(T)};
   ORBIT_TRY(launch(ki, qkln_bwd_kernel<T, DH>, dim3(blocks), dim3(256), 0, s, (T*)d, ldd, (const T*)src, lds,
                    mean, rstd, (const T*)qg, (const T*)kg, T_, H, H * DH, part));
-  KernelInfo kf{"qkln_param_final", 0.0, 4.0 * blocks * 4 * DH};
-  return launch(kf, qkln_param_final, dim3((unsigned)cdiv(4 * DH, 64)), dim3(256), 0, s, (const float*)part,
-                blocks, DH, dqg, dqb, dkg, dkb, accumulate);
+  ColFinal own;
+  ColFinal& f = fin ? *fin : own;
+  float* outs[4] = {dqg, dqb, dkg, dkb};
+  for (int k = 0; k < 4; ++k) f.add(part + k * DH, 4 * DH, blocks, DH, outs[k]);
+  return fin ? ORBIT_OK : own.run(accumulate, s);
 }
 
 }  // namespace
@@ -495,23 +489,101 @@ orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const v
   return ln_bwd_dispatch<float>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
 }
 
-size_t colsum_workspace_bytes(int rows, int n) {
-  return align_up((size_t)2 * cdiv(rows, rows_per_chunk(rows)) * (size_t)n * sizeof(float));
+// ---- column sums: host side ------------------------------------------------
+int colsum_chunks(int rows) { return rows > 0 ? (int)cdiv(rows, cs_rows_per_chunk(rows)) : 0; }
+
+size_t colsum_part_bytes(int rows, int n, bool ln, int batch) {
+  return align_up((size_t)batch * (ln ? 2 : 1) * colsum_chunks(rows) * (size_t)n * sizeof(float));
 }
+
+orbit_status colsum_partials(orbit_dtype dt, ColJob* jobs, int njobs, int rows, hipStream_t s) {
+  if (njobs <= 0 || rows <= 0) return ORBIT_OK;
+  if (njobs > kColMaxJobs) {
+    set_error("colsum: %d jobs exceed the limit of %d", njobs, kColMaxJobs);
+    return ORBIT_E_ARG;
+  }
+  CsArgs a{};
+  a.njobs = njobs;
+  a.rows = rows;
+  a.rpc = cs_rows_per_chunk(rows);
+  a.chunks = (int)cdiv(rows, a.rpc);
+  int cb = 0, maxb = 1;
+  double bytes = 0;
+  for (int j = 0; j < njobs; ++j) {
+    const ColJob& J = jobs[j];
+    const int batch = std::max(1, J.batch);
+    CsJobK& K = a.job[j];
+    K.src = J.src; K.ld = J.ld; K.sbatch = J.sbatch;
+    K.x = J.x; K.ldx = J.ldx; K.sxbatch = J.sxbatch; K.mean = J.mean; K.rstd = J.rstd;
+    K.part = J.part; K.spart = (int64_t)(J.x ? 2 : 1) * a.chunks * J.n;
+    K.n = J.n; K.cb0 = cb; K.batch = batch;
+    cb += (int)cdiv(J.n, kCsCols);
+    maxb = std::max(maxb, batch);
+    bytes += (J.x ? 2.0 : 1.0) * batch * rows * (double)J.n * (dt == ORBIT_BF16 ? 2 : 4);
+  }
+  const dim3 grid((unsigned)cb, (unsigned)a.chunks, (unsigned)maxb);
+  KernelInfo ki{dt == ORBIT_BF16 ? "colsum_partials<bf16>" : "colsum_partials<f32>", 0.0, bytes};
+  if (dt == ORBIT_BF16) return launch(ki, colsum_partials_kernel<bf16>, grid, dim3(1024), 0, s, a);
+  return launch(ki, colsum_partials_kernel<float>, grid, dim3(1024), 0, s, a);
+}
+
+void ColFinal::add(const float* part, int64_t ldp, int chunks, int n, float* out) {
+  if (!out || n <= 0) return;
+  Item it{part, ldp, out, chunks, n};
+  items.push_back(it);
+}
+
+void ColFinal::add_job(const ColJob& J, int rows) {
+  const int ch = colsum_chunks(rows);
+  const int batch = std::max(1, J.batch);
+  for (int b = 0; b < batch; ++b) {
+    const float* p = J.part + (int64_t)b * (J.x ? 2 : 1) * ch * J.n;
+    add(p, J.n, ch, J.n, J.out_sum ? J.out_sum + (int64_t)b * J.sout : nullptr);
+    if (J.x) add(p + (int64_t)ch * J.n, J.n, ch, J.n, J.out_xsum ? J.out_xsum + (int64_t)b * J.sout : nullptr);
+  }
+}
+
+orbit_status ColFinal::run(int accumulate, hipStream_t s) {
+  size_t i = 0;
+  while (i < items.size()) {
+    CsFinalArgs a{};
+    a.accumulate = accumulate;
+    int cb = 0;
+    double bytes = 0;
+    for (; i < items.size() && a.nitems < kColMaxFinal; ++i) {
+      const Item& it = items[i];
+      CsFinalK& K = a.item[a.nitems++];
+      K.part = it.part; K.ldp = it.ldp; K.out = it.out; K.chunks = it.chunks; K.n = it.n; K.cb0 = cb;
+      cb += (int)cdiv(it.n, 64);
+      bytes += 4.0 * it.chunks * it.n;
+    }
+    KernelInfo kf{"colsum_final", 0.0, bytes};
+    ORBIT_TRY(launch(kf, colsum_final_kernel, dim3((unsigned)cb), dim3(256), 0, s, a));
+  }
+  items.clear();
+  return ORBIT_OK;
+}
+
+size_t colsum_workspace_bytes(int rows, int n) { return colsum_part_bytes(rows, n, true, 1); }
 
 orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int n, const void* x, int64_t ldx,
                     const float* mean, const float* rstd, float* out_sum, float* out_xsum, int accumulate,
                     void* ws, hipStream_t s) {
   if (rows <= 0 || n <= 0) return ORBIT_OK;
-  if (dt == ORBIT_BF16)
-    return colsum_t<bf16>(dy, lddy, rows, n, x, ldx, mean, rstd, out_sum, out_xsum, accumulate, ws, s);
-  return colsum_t<float>(dy, lddy, rows, n, x, ldx, mean, rstd, out_sum, out_xsum, accumulate, ws, s);
+  ColJob J{};
+  J.src = dy; J.ld = lddy; J.n = n;
+  J.x = x; J.ldx = ldx; J.mean = mean; J.rstd = rstd;
+  J.out_sum = out_sum; J.out_xsum = x ? out_xsum : nullptr;
+  J.part = static_cast<float*>(ws);
+  ORBIT_TRY(colsum_partials(dt, &J, 1, rows, s));
+  ColFinal f;
+  f.add_job(J, rows);
+  return f.run(accumulate, s);
 }
 
 orbit_status colsum_f32(const float* dy, int64_t lddy, int rows, int n, float* out_sum, int accumulate, void* ws,
                         hipStream_t s) {
-  if (rows <= 0 || n <= 0) return ORBIT_OK;
-  return colsum_t<float>(dy, lddy, rows, n, nullptr, 0, nullptr, nullptr, out_sum, nullptr, accumulate, ws, s);
+  return colsum(ORBIT_F32, dy, lddy, rows, n, nullptr, 0, nullptr, nullptr, out_sum, nullptr, accumulate, ws, s);
 }
 
 orbit_status qk_norm_fwd(orbit_dtype dt, const void* src, int64_t lds, void* dst, int64_t ldd, const void* qg,
@@ -536,9 +608,10 @@ size_t qk_norm_bwd_workspace_bytes(int dh) { return align_up((size_t)kQkBwdBlock
 
 orbit_status qk_norm_bwd(orbit_dtype dt, void* d, int64_t ldd, const void* src, int64_t lds, const float* mean,
                          const float* rstd, const void* qg, const void* kg, float* dqg, float* dqb, float* dkg,
-                         float* dkb, int accumulate, int T_, int H, int dh, void* ws, hipStream_t s) {
+                         float* dkb, int accumulate, int T_, int H, int dh, void* ws, ColFinal* fin,
+                         hipStream_t s) {
 #define QKB(TT, D) \
-  return qk_bwd_t<TT, D>(d, ldd, src, lds, mean, rstd, qg, kg, dqg, dqb, dkg, dkb, accumulate, T_, H, ws, s)
+  return qk_bwd_t<TT, D>(d, ldd, src, lds, mean, rstd, qg, kg, dqg, dqb, dkg, dkb, accumulate, T_, H, ws, fin, s)
   if (dt == ORBIT_BF16) {
     if (dh == 32) QKB(bf16, 32);
     if (dh == 64) QKB(bf16, 64);
