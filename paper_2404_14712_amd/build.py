@@ -43,9 +43,15 @@ def sources():
     return out
 
 
+# per-source code-generation options: the attention kernels keep their small
+# accumulators (scores, probabilities) in VGPRs, which the softmax reads and
+# writes every tile; the GEMMs keep their large accumulators in AGPRs
+PER_SOURCE = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=true"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + COMMON + DEVICE + ["-c", src, "-o", obj]
+    cmd = [hipcc()] + COMMON + DEVICE + PER_SOURCE.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

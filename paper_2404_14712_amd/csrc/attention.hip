@@ -128,36 +128,45 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(FwdArgs a) {
         mma16(s[mt], kf, qf[kk]);
       }
     }
-    // online softmax over this tile (log2 domain); lane owns query qi
+    // online softmax over this tile (log2 domain); lane owns query qi and,
+    // with its partner lane l ^ 32, the running max m and sum of that query
     const int jbase = jt * KT;
+    if (jbase + KT > L) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kv = jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
+          if (kv >= L) s[mt][v] = -INFINITY;
+        }
+    }
     float mloc = -INFINITY;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int kv = jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
-        const float x = kv < L ? s[mt][v] * a.sl2 : -INFINITY;
-        s[mt][v] = x;
-        mloc = fmaxf(mloc, x);
-      }
+      for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, s[mt][v]);
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float mnew = fmaxf(m, mloc);
-    const float alpha = exp2f(m - mnew);
+    const float mnew = fmaxf(m, mloc * a.sl2);
+    // rescale O and the sum only when some query's maximum moved
+    if (__ballot(mnew > m) != 0) {
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[c][v] *= alpha;
+      m = mnew;
+    }
     float ps = 0.f;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = exp2f(s[mt][v] - mnew);
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -m));
         s[mt][v] = p;
         ps += p;
       }
-    lsum = lsum * alpha + ps;
-    m = mnew;
-#pragma unroll
-    for (int c = 0; c < DH / 32; ++c)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[c][v] *= alpha;
+    lsum += ps;
     // O^T[c][q] += V^T[c][kv] P^T[kv][q]
 #pragma unroll
     for (int kk = 0; kk < KT / 16; ++kk) {
@@ -337,19 +346,33 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
   float cs = 0.f;
   DS sq, sd;
   const int nq = (L + 31) / 32;
+  // the next query tile (and its softmax statistics) is loaded while the
+  // current one is multiplied
+  sq.load(Q, a.ldq, 0, L, tid);
+  sd.load(dO, a.lddo, 0, L, tid);
+  float lse_n = 0.f, d_n = 0.f;
+  if (tid < 32) {
+    lse_n = tid < L ? lse[tid] * kLog2e : INFINITY;
+    d_n = tid < L ? Dv[tid] : 0.f;
+  }
   for (int it = 0; it < nq; ++it) {
-    const int q0 = it * 32;
-    sq.load(Q, a.ldq, q0, L, tid);
-    sd.load(dO, a.lddo, q0, L, tid);
     __syncthreads();  // previous tile fully consumed (and qbar visible)
     sq.store(qs, qt, tid, qbar);
     sd.store(ds_, dt, tid, nullptr);
     if (tid < 32) {
-      const int qq = q0 + tid;
-      lse_s[tid] = qq < L ? lse[qq] * kLog2e : INFINITY;
-      d_s[tid] = qq < L ? Dv[qq] : 0.f;
+      lse_s[tid] = lse_n;
+      d_s[tid] = d_n;
     }
     __syncthreads();
+    if (it + 1 < nq) {
+      const int q1 = (it + 1) * 32;
+      sq.load(Q, a.ldq, q1, L, tid);
+      sd.load(dO, a.lddo, q1, L, tid);
+      if (tid < 32) {
+        lse_n = q1 + tid < L ? lse[q1 + tid] * kLog2e : INFINITY;
+        d_n = q1 + tid < L ? Dv[q1 + tid] : 0.f;
+      }
+    }
 
     f32x16 s, dp;
 #pragma unroll
@@ -366,7 +389,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv(BwdArgs a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int qr = (v >> 2) * 8 + g * 4 + (v & 3);
-      const float p = exp2f(s[v] * a.sl2 - lse_s[qr]);
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[v], a.sl2, -lse_s[qr]));
       s[v] = p;
       dp[v] = p * (dp[v] - d_s[qr]);
       cs += dp[v];
@@ -454,18 +477,24 @@ __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
   LK lk, lvv;
   LT lt;
   const int nt = (L + KT - 1) / KT;
+  lk.load(K, nullptr, 0, a.ldk, 0, L, 0, DH, tid);
+  lvv.load(V, nullptr, 0, a.ldv, 0, L, 0, DH, tid);
+  lt.load(K, nullptr, 0, a.ldk, 0, DH, 0, L, tid);
   for (int jt = 0; jt < nt; ++jt) {
     const int j0 = jt * KT;
-    lk.load(K, nullptr, 0, a.ldk, j0, L, 0, DH, tid);
-    lvv.load(V, nullptr, 0, a.ldv, j0, L, 0, DH, tid);
-    lt.load(K + (int64_t)j0 * a.ldk, nullptr, 0, a.ldk, 0, DH, 0, L - j0, tid);
-    __syncthreads();
+    __syncthreads();  // previous tile fully consumed (and kbar visible)
     lk.store(ks, tid);
     lvv.store(vs, tid);
     // dQ_i = sum_j dS_ij k_j = sum_j dS_ij (k_j - kbar) since sum_j dS_ij = 0:
     // centred keys keep the product well conditioned when the keys are alike
     lt.store_sub(kt, tid, kbar);
     __syncthreads();
+    if (jt + 1 < nt) {  // the next key tile is loaded while this one is multiplied
+      const int j1 = j0 + KT;
+      lk.load(K, nullptr, 0, a.ldk, j1, L, 0, DH, tid);
+      lvv.load(V, nullptr, 0, a.ldv, j1, L, 0, DH, tid);
+      lt.load(K + (int64_t)j1 * a.ldk, nullptr, 0, a.ldk, 0, DH, 0, L - j1, tid);
+    }
 
     f32x16 s[2], dp[2];
 #pragma unroll
@@ -480,10 +509,16 @@ __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
         ld_frag(af, vs + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
         mma16(dp[mt], af, of[kk]);
       }
+      if (j0 + KT > L) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kvi = j0 + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
+          if (kvi >= L) s[mt][v] = -INFINITY;
+        }
+      }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int kvi = j0 + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
-        const float p = kvi < L ? exp2f(s[mt][v] * a.sl2 - lse2) : 0.f;
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -lse2));
         dp[mt][v] = p * (dp[mt][v] - Dq);
       }
     }

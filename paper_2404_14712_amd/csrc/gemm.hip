@@ -292,34 +292,56 @@ int64_t tiles_of(const Gemm& g, const TileCfg& t) { return cdiv(g.M, t.BM) * cdi
 
 int bke_of(orbit_dtype dt) { return dt == ORBIT_BF16 ? 64 : 32; }
 
-// split-K factor that brings `tiles` work items up to one per CU, keeping at
-// least 8 K-steps per split
-int64_t splits_for(const Gemm& g, int64_t tiles) {
-  const int64_t ksteps = cdiv(g.K, bke_of(g.dtype));
-  if (tiles >= 240 || ksteps < 16) return 1;
-  return std::max<int64_t>(1, std::min<int64_t>(cdiv(256, tiles), ksteps / 8));
+// bf16 products: the (tile, split) pair with the least modelled time. A
+// tile's rate is its throughput measured on MI355X at full occupancy for the
+// operand layout (forward A K-major/B N-major, input gradient both K-major,
+// weight gradient A M-major/B N-major); a launch of `items` work items runs
+// in ceil(items / 256) rounds over the 256 CUs; a split adds its float32
+// partials (written and read back) and the reduction launch.
+struct Choice { TileCfg t; int splits; };
+
+Choice pick_bf16(const Gemm& g) {
+  struct Cand { TileCfg t; double fwd, dx, dw; };  // TFLOP/s
+  const Cand cands[] = {{kT256, 950.0, 1030.0, 780.0},
+                        {kT256x128, 680.0, 850.0, 490.0},
+                        {kT128x256, 600.0, 870.0, 490.0},
+                        {kBig, 600.0, 890.0, 480.0}};
+  const double flops = 2.0 * g.M * g.N * (double)g.K * g.batch;
+  const int64_t ksteps = cdiv(g.K, 64);
+  Choice best{kBig, 1};
+  double best_us = 1e300;
+  for (const Cand& c : cands) {
+    if (g.M < c.t.BM || g.N < c.t.BN) continue;
+    const double rate = g.a_kmajor ? (g.b_kmajor ? c.dx : c.fwd) : c.dw;
+    const int64_t tiles = tiles_of(g, c.t);
+    for (int sp = 1; sp <= 16; sp *= 2) {
+      if (sp > 1 && (ksteps / sp < 8 || tiles * sp > 2048)) break;
+      const int64_t items = tiles * sp;
+      const double rounds = (double)cdiv(items, 256);
+      const double util = (double)items / (rounds * 256.0);
+      double us = flops / (rate * 1e12 * util) * 1e6;
+      if (sp > 1) us += (double)sp * g.M * g.N * g.batch * 8.0 / 5.0e12 * 1e6 + 6.0;
+      if (us < best_us * 0.98) {
+        best_us = us;
+        best = {c.t, sp};
+      }
+    }
+  }
+  return best;
 }
 
 TileCfg pick_tile(const Gemm& g) {
   if (g.N <= 32) return kNarrowN;
   if (g.M <= 32) return kNarrowM;
   if (g.M <= 64 || g.N <= 64) return kSmall;
-  if (g.dtype == ORBIT_BF16 && g.K >= 256) {
-    // the largest tile that gives every CU a tile (directly, or through a
-    // split of a long K)
-    const TileCfg cands[] = {kT256, kT256x128, kT128x256};
-    for (const TileCfg& t : cands) {
-      if (g.M < t.BM || g.N < t.BN) continue;
-      const int64_t tiles = tiles_of(g, t);
-      if (tiles * splits_for(g, tiles) >= 240) return t;
-    }
-  }
+  if (g.dtype == ORBIT_BF16 && g.K >= 256 && g.M >= 128 && g.N >= 128) return pick_bf16(g).t;
   return kBig;
 }
 
 int pick_splits(const Gemm& g, const TileCfg& t) {
+  if (g.dtype == ORBIT_BF16 && g.K >= 256 && g.M >= 128 && g.N >= 128 && t == pick_bf16(g).t)
+    return pick_bf16(g).splits;
   const int64_t tiles = tiles_of(g, t);
-  if (t.BM * t.BN >= 256 * 128) return (int)splits_for(g, tiles);
   const int bke = bke_of(g.dtype);
   const int64_t ksteps = cdiv(g.K, bke);
   if (tiles >= 256 || ksteps < 8) return 1;
