@@ -9,6 +9,7 @@
 // LDS so its fragments are two 8-byte reads. The backward uses the same idea
 // in both orientations (see the per-kernel comments).
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 #include "tile.h"
@@ -548,12 +549,451 @@ __global__ void __launch_bounds__(256) attn_bwd_dq(BwdArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 kernels with transposing LDS reads (ds_read_b64_tr_b16): every tile is
+// staged once, row-major, and the operands that are needed transposed (V^T in
+// the forward; dO^T, Q^T and K^T in the backward) are read as MFMA fragments
+// straight from that copy. Tiles are double-buffered in LDS (one barrier per
+// tile) and the last, partial tile is peeled so the main loop carries no masks.
+// ---------------------------------------------------------------------------
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+// A-operand fragment of a matrix stored M-contiguous in LDS (element (k, m) at
+// base[k * pitch + m]): rows m = lane % 32, a 16-deep K step in accumulator
+// slot order (slot j of lane group g = lane / 32 holds k = (j/4)*8 + 4g + j%4).
+// Each 16-lane group reads 4 k-rows x 16 m per transposing read; two reads.
+ORBIT_DEV void ld_frag_tr(Frag<bf16>& f, const bf16* base, int pitch, int lane) {
+  const int G = lane >> 4, r = lane & 15;
+  bf16* p0 = const_cast<bf16*>(base) + (4 * (G >> 1) + (r >> 2)) * pitch + 16 * (G & 1) + 4 * (r & 3);
+  bf16* p1 = p0 + 8 * pitch;
+  const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p0);
+  const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p1);
+  const s16x8 xy = __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+  f.v = __builtin_bit_cast(bf16x8, xy);
+}
+
+template <int DH>
+__global__ void __launch_bounds__(256) attn_fwd_tr(FwdArgs a) {
+  using T = bf16;
+  constexpr int KT = 64;
+  using LK = TileLoader<T, KT, DH, 256, true>;  // K and V rows [kv][c]
+  constexpr int KP = LK::PITCH;
+  __shared__ __attribute__((aligned(16))) T ks[2][KT * KP];
+  __shared__ __attribute__((aligned(16))) T vs[2][KT * KP];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int L = a.L;
+  const int64_t row0 = (int64_t)b * L;
+  const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
+  const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
+  const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
+
+  const int qi = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  Frag<T> qf[DH / 16];
+#pragma unroll
+  for (int kk = 0; kk < DH / 16; ++kk) {
+    if (qi < L) ld_frag(qf[kk], Q + (int64_t)qi * a.ldq + kk * 16 + g * 8);
+    else {
+      float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      frag_from(qf[kk], z);
+    }
+  }
+  f32x16 o[DH / 32];
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[c][v] = 0.f;
+  float m = -INFINITY, lsum = 0.f;
+
+  LK lk, lv;
+  const int nt = (L + KT - 1) / KT;
+  lk.load(K, nullptr, 0, a.ldk, 0, L, 0, DH, tid);
+  lv.load(V, nullptr, 0, a.ldv, 0, L, 0, DH, tid);
+  lk.store(ks[0], tid);
+  lv.store(vs[0], tid);
+  __syncthreads();
+
+  auto tile = [&](int jt, auto mask) {
+    const int cur = jt & 1;
+    if (jt + 1 < nt) {
+      const int j1 = (jt + 1) * KT;
+      lk.load(K, nullptr, 0, a.ldk, j1, L, 0, DH, tid);
+      lv.load(V, nullptr, 0, a.ldv, j1, L, 0, DH, tid);
+    }
+    const T* Ks = ks[cur];
+    const T* Vs = vs[cur];
+    f32x16 s[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[mt][v] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DH / 16; ++kk) {
+        Frag<T> kf;
+        ld_frag(kf, Ks + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+        mma16(s[mt], kf, qf[kk]);
+      }
+    }
+    if constexpr (decltype(mask)::value) {
+      const int jbase = jt * KT;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3) >= L) s[mt][v] = -INFINITY;
+    }
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, s[mt][v]);
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float mnew = fmaxf(m, mloc * a.sl2);
+    if (__ballot(mnew > m) != 0) {
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[c][v] *= alpha;
+      m = mnew;
+    }
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -m));
+        s[mt][v] = p;
+        lsum += p;
+      }
+    // O^T[c][q] += V^T[c][kv] P^T[kv][q]
+#pragma unroll
+    for (int kk = 0; kk < KT / 16; ++kk) {
+      Frag<T> pf;
+      acc_frag(pf, s[kk >> 1], (kk & 1) * 8);
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        Frag<T> vf;
+        ld_frag_tr(vf, Vs + kk * 16 * KP + c * 32, KP, lane);
+        mma16(o[c], vf, pf);
+      }
+    }
+    if (jt + 1 < nt) {
+      lk.store(ks[cur ^ 1], tid);
+      lv.store(vs[cur ^ 1], tid);
+    }
+    __syncthreads();
+  };
+  const int nfull = L / KT;
+  for (int jt = 0; jt < nfull; ++jt) tile(jt, std::false_type{});
+  if (nfull < nt) tile(nfull, std::true_type{});
+
+  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  if (qi < L) {
+    const float inv = 1.f / ltot;
+    T* O = static_cast<T*>(a.o) + (row0 + qi) * a.ldo + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + r4 * 8 + g * 4;
+        st4(O + col, o[c][r4 * 4] * inv, o[c][r4 * 4 + 1] * inv, o[c][r4 * 4 + 2] * inv, o[c][r4 * 4 + 3] * inv);
+      }
+    if (a.o32) {
+      float* O32 = a.o32 + (row0 + qi) * a.ldo32 + h * DH;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int col = c * 32 + r4 * 8 + g * 4;
+          st4(O32 + col, o[c][r4 * 4] * inv, o[c][r4 * 4 + 1] * inv, o[c][r4 * 4 + 2] * inv,
+              o[c][r4 * 4 + 3] * inv);
+        }
+    }
+    if (g == 0) a.lse[((int64_t)b * a.H + h) * L + qi] = (m + __log2f(ltot)) * kLn2;
+  }
+}
+
+// K/V-major backward (bf16): each wave owns 32 keys and sweeps 32-query tiles.
+// dK_j = sum_i dS_ij q_i runs on the uncentred queries; the part of the bf16
+// rounding of dS that the common query component qbar would amplify is put
+// back exactly: dK_j += qbar (sum_i dS_ij - sum_i bf16(dS_ij)), both sums in
+// float32, which equals the centred form sum_i bf16(dS_ij) (q_i - qbar) +
+// qbar sum_i dS_ij.
+template <int DH>
+__global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
+  using T = bf16;
+  constexpr int QT = 32;
+  using LQ = TileLoader<T, QT, DH, 256, true>;  // Q and dO rows [q][c]
+  constexpr int RP = LQ::PITCH;
+  __shared__ __attribute__((aligned(16))) T qs[2][QT * RP];
+  __shared__ __attribute__((aligned(16))) T os[2][QT * RP];
+  __shared__ float lse_s[2][QT], d_s[2][QT];
+  __shared__ float qbar[DH];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int L = a.L;
+  const int64_t row0 = (int64_t)b * L;
+  if (tid < DH) qbar[tid] = a.qsum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
+  const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
+  const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
+  const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
+  const T* dO = static_cast<const T*>(a.dO) + row0 * a.lddo + h * DH;
+  const float* lse = a.lse + ((int64_t)b * a.H + h) * L;
+  const float* Dv = a.D + ((int64_t)b * a.H + h) * L;
+
+  const int kv = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  Frag<T> kf[DH / 16], vf[DH / 16];
+#pragma unroll
+  for (int kk = 0; kk < DH / 16; ++kk) {
+    if (kv < L) {
+      ld_frag(kf[kk], K + (int64_t)kv * a.ldk + kk * 16 + g * 8);
+      ld_frag(vf[kk], V + (int64_t)kv * a.ldv + kk * 16 + g * 8);
+    } else {
+      float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      frag_from(kf[kk], z);
+      frag_from(vf[kk], z);
+    }
+  }
+  f32x16 dvt[DH / 32], dkt[DH / 32];
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dvt[c][v] = dkt[c][v] = 0.f;
+
+  float cs = 0.f, csr = 0.f;
+  LQ lq, lo;
+  const int nq = (L + QT - 1) / QT;
+  lq.load(Q, nullptr, 0, a.ldq, 0, L, 0, DH, tid);
+  lo.load(dO, nullptr, 0, a.lddo, 0, L, 0, DH, tid);
+  lq.store(qs[0], tid);
+  lo.store(os[0], tid);
+  if (tid < QT) {
+    lse_s[0][tid] = tid < L ? lse[tid] * kLog2e : INFINITY;
+    d_s[0][tid] = tid < L ? Dv[tid] : 0.f;
+  }
+  __syncthreads();
+  for (int it = 0; it < nq; ++it) {
+    const int cur = it & 1;
+    float lse_n = 0.f, d_n = 0.f;
+    if (it + 1 < nq) {
+      const int q1 = (it + 1) * QT;
+      lq.load(Q, nullptr, 0, a.ldq, q1, L, 0, DH, tid);
+      lo.load(dO, nullptr, 0, a.lddo, q1, L, 0, DH, tid);
+      if (tid < QT) {
+        lse_n = q1 + tid < L ? lse[q1 + tid] * kLog2e : INFINITY;
+        d_n = q1 + tid < L ? Dv[q1 + tid] : 0.f;
+      }
+    }
+    const T* Qs = qs[cur];
+    const T* Os = os[cur];
+    f32x16 s, dp;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) {
+      Frag<T> af;
+      ld_frag(af, Qs + (lane & 31) * RP + kk * 16 + g * 8);
+      mma16(s, af, kf[kk]);
+      ld_frag(af, Os + (lane & 31) * RP + kk * 16 + g * 8);
+      mma16(dp, af, vf[kk]);
+    }
+    // rows: query 8*(v/4) + 4g + v%4 of the tile; column: this lane's key
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int qr = (v >> 2) * 8 + g * 4 + (v & 3);
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[v], a.sl2, -lse_s[cur][qr]));
+      s[v] = p;
+      dp[v] = p * (dp[v] - d_s[cur][qr]);
+      cs += dp[v];
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      Frag<T> pf, sf;
+      acc_frag(pf, s, kk * 8);
+      acc_frag(sf, dp, kk * 8);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) csr += (float)sf.v[j];
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        Frag<T> af;
+        ld_frag_tr(af, Os + kk * 16 * RP + c * 32, RP, lane);
+        mma16(dvt[c], af, pf);
+        ld_frag_tr(af, Qs + kk * 16 * RP + c * 32, RP, lane);
+        mma16(dkt[c], af, sf);
+      }
+    }
+    if (it + 1 < nq) {
+      lq.store(qs[cur ^ 1], tid);
+      lo.store(os[cur ^ 1], tid);
+      if (tid < QT) {
+        lse_s[cur ^ 1][tid] = lse_n;
+        d_s[cur ^ 1][tid] = d_n;
+      }
+    }
+    __syncthreads();
+  }
+
+  cs += __shfl_xor(cs, 32, 64);
+  csr += __shfl_xor(csr, 32, 64);
+  const float corr = cs - csr;
+  if (kv < L) {
+    T* dK = static_cast<T*>(a.dk) + (row0 + kv) * a.ldg + h * DH;
+    T* dV = static_cast<T*>(a.dv) + (row0 + kv) * a.ldg + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + r4 * 8 + g * 4;
+        st4(dK + col, (dkt[c][r4 * 4] + qbar[col] * corr) * a.scale,
+            (dkt[c][r4 * 4 + 1] + qbar[col + 1] * corr) * a.scale,
+            (dkt[c][r4 * 4 + 2] + qbar[col + 2] * corr) * a.scale,
+            (dkt[c][r4 * 4 + 3] + qbar[col + 3] * corr) * a.scale);
+        st4(dV + col, dvt[c][r4 * 4], dvt[c][r4 * 4 + 1], dvt[c][r4 * 4 + 2], dvt[c][r4 * 4 + 3]);
+      }
+  }
+}
+
+// Q-major backward (bf16): each wave owns 32 queries and sweeps 64-key tiles.
+// dQ_i = sum_j dS_ij k_j = sum_j dS_ij (k_j - kbar) since sum_j dS_ij = 0; the
+// product runs on the uncentred keys and kbar sum_j bf16(dS_ij) (float32) is
+// subtracted, which equals the centred form sum_j bf16(dS_ij) (k_j - kbar).
+template <int DH>
+__global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
+  using T = bf16;
+  constexpr int KT = 64;
+  using LK = TileLoader<T, KT, DH, 256, true>;  // K and V rows [kv][c]
+  constexpr int KP = LK::PITCH;
+  __shared__ __attribute__((aligned(16))) T ks[2][KT * KP];
+  __shared__ __attribute__((aligned(16))) T vs[2][KT * KP];
+  __shared__ float kbar[DH];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int L = a.L;
+  const int64_t row0 = (int64_t)b * L;
+  if (tid < DH) kbar[tid] = a.ksum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
+  const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
+  const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
+  const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
+  const T* dO = static_cast<const T*>(a.dO) + row0 * a.lddo + h * DH;
+
+  const int qi = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  Frag<T> qf[DH / 16], of[DH / 16];
+#pragma unroll
+  for (int kk = 0; kk < DH / 16; ++kk) {
+    if (qi < L) {
+      ld_frag(qf[kk], Q + (int64_t)qi * a.ldq + kk * 16 + g * 8);
+      ld_frag(of[kk], dO + (int64_t)qi * a.lddo + kk * 16 + g * 8);
+    } else {
+      float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      frag_from(qf[kk], z);
+      frag_from(of[kk], z);
+    }
+  }
+  const float lse2 = qi < L ? a.lse[((int64_t)b * a.H + h) * L + qi] * kLog2e : INFINITY;
+  const float Dq = qi < L ? a.D[((int64_t)b * a.H + h) * L + qi] : 0.f;
+
+  f32x16 dqt[DH / 32];
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dqt[c][v] = 0.f;
+  float rs = 0.f;
+
+  LK lk, lv;
+  const int nt = (L + KT - 1) / KT;
+  lk.load(K, nullptr, 0, a.ldk, 0, L, 0, DH, tid);
+  lv.load(V, nullptr, 0, a.ldv, 0, L, 0, DH, tid);
+  lk.store(ks[0], tid);
+  lv.store(vs[0], tid);
+  __syncthreads();
+
+  auto tile = [&](int jt, auto mask) {
+    const int cur = jt & 1;
+    if (jt + 1 < nt) {
+      const int j1 = (jt + 1) * KT;
+      lk.load(K, nullptr, 0, a.ldk, j1, L, 0, DH, tid);
+      lv.load(V, nullptr, 0, a.ldv, j1, L, 0, DH, tid);
+    }
+    const T* Ks = ks[cur];
+    const T* Vs = vs[cur];
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[mt][v] = dp[mt][v] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DH / 16; ++kk) {
+        Frag<T> af;
+        ld_frag(af, Ks + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+        mma16(s[mt], af, qf[kk]);
+        ld_frag(af, Vs + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+        mma16(dp[mt], af, of[kk]);
+      }
+      if constexpr (decltype(mask)::value) {
+        const int jbase = jt * KT;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3) >= L) s[mt][v] = -INFINITY;
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -lse2));
+        dp[mt][v] = p * (dp[mt][v] - Dq);
+      }
+    }
+    // dQ^T[c][q] += K^T[c][kv] dS^T[kv][q]
+#pragma unroll
+    for (int kk = 0; kk < KT / 16; ++kk) {
+      Frag<T> sf;
+      acc_frag(sf, dp[kk >> 1], (kk & 1) * 8);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) rs += (float)sf.v[j];
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        Frag<T> af;
+        ld_frag_tr(af, Ks + kk * 16 * KP + c * 32, KP, lane);
+        mma16(dqt[c], af, sf);
+      }
+    }
+    if (jt + 1 < nt) {
+      lk.store(ks[cur ^ 1], tid);
+      lv.store(vs[cur ^ 1], tid);
+    }
+    __syncthreads();
+  };
+  const int nfull = L / KT;
+  for (int jt = 0; jt < nfull; ++jt) tile(jt, std::false_type{});
+  if (nfull < nt) tile(nfull, std::true_type{});
+
+  rs += __shfl_xor(rs, 32, 64);
+  if (qi < L) {
+    T* dQ = static_cast<T*>(a.dq) + (row0 + qi) * a.ldg + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = c * 32 + r4 * 8 + g * 4;
+        st4(dQ + col, (dqt[c][r4 * 4] - kbar[col] * rs) * a.scale,
+            (dqt[c][r4 * 4 + 1] - kbar[col + 1] * rs) * a.scale,
+            (dqt[c][r4 * 4 + 2] - kbar[col + 2] * rs) * a.scale,
+            (dqt[c][r4 * 4 + 3] - kbar[col + 3] * rs) * a.scale);
+      }
+  }
+}
+
 template <typename T, int DH>
 orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32, hipStream_t s) {
   FwdArgs a{io.q, io.k, io.v, o, lse, o32, io.ldq, io.ldk, io.ldv, ldo, ldo32, io.H, io.L, kLog2e / sqrtf((float)DH)};
   const double bh = (double)io.B * io.H;
   KernelInfo ki{sizeof(T) == 2 ? "attn_fwd_kernel<bf16>" : "attn_fwd_kernel<f32>",
                 4.0 * bh * io.L * (double)io.L * DH, 4.0 * bh * io.L * DH * sizeof(T)};
+  if constexpr (sizeof(T) == 2)
+    return launch(ki, attn_fwd_tr<DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
   return launch(ki, attn_fwd_kernel<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
 }
 
@@ -594,10 +1034,16 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
   const double fl = 4.0 * bh * io.L * (double)io.L * DH;
   KernelInfo k1{sizeof(T) == 2 ? "attn_bwd_dkdv<bf16>" : "attn_bwd_dkdv<f32>", 2 * fl * 0.6,
                 6.0 * bh * io.L * DH * sizeof(T)};
-  ORBIT_TRY(launch(k1, attn_bwd_dkdv<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a));
+  const dim3 grid((unsigned)cdiv(io.L, 128), io.H, io.B);
+  if constexpr (sizeof(T) == 2) {
+    ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH>, grid, dim3(256), 0, s, a));
+  } else {
+    ORBIT_TRY(launch(k1, attn_bwd_dkdv<T, DH>, grid, dim3(256), 0, s, a));
+  }
   KernelInfo k2{sizeof(T) == 2 ? "attn_bwd_dq<bf16>" : "attn_bwd_dq<f32>", 2 * fl * 0.4,
                 5.0 * bh * io.L * DH * sizeof(T)};
-  return launch(k2, attn_bwd_dq<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
+  if constexpr (sizeof(T) == 2) return launch(k2, attn_bwd_dq_tr<DH>, grid, dim3(256), 0, s, a);
+  return launch(k2, attn_bwd_dq<T, DH>, grid, dim3(256), 0, s, a);
 }
 
 }  // namespace

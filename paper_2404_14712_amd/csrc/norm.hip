@@ -234,21 +234,26 @@ struct CsFinalArgs {
   int nitems, accumulate;
 };
 
-// 64 elements x 4 chunk lanes per block; fixed-order sums
+// 16 elements x 16 chunk lanes per block; each lane sums a fixed strided subset
+// of the chunks (8 loads in flight), the 16 lane sums are combined in order
 __global__ void __launch_bounds__(256) colsum_final_kernel(CsFinalArgs a) {
-  __shared__ float red[4][64];
+  __shared__ float red[16][17];
   int j = 0;
   while (j + 1 < a.nitems && (int)blockIdx.x >= a.item[j + 1].cb0) ++j;
   const CsFinalK& I = a.item[j];
-  const int el = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int e = ((int)blockIdx.x - I.cb0) * 64 + el;
+  const int el = threadIdx.x & 15, q = threadIdx.x >> 4;
+  const int e = ((int)blockIdx.x - I.cb0) * 16 + el;
   float s = 0.f;
-  if (e < I.n)
-    for (int k = q; k < I.chunks; k += 4) s += I.part[(int64_t)k * I.ldp + e];
+  if (e < I.n) {
+#pragma unroll 8
+    for (int k = q; k < I.chunks; k += 16) s += I.part[(int64_t)k * I.ldp + e];
+  }
   red[q][el] = s;
   __syncthreads();
   if (q == 0 && e < I.n) {
-    const float t = (red[0][el] + red[1][el]) + (red[2][el] + red[3][el]);
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) t += red[k][el];
     I.out[e] = a.accumulate ? I.out[e] + t : t;
   }
 }
@@ -554,7 +559,7 @@ orbit_status ColFinal::run(int accumulate, hipStream_t s) {
       const Item& it = items[i];
       CsFinalK& K = a.item[a.nitems++];
       K.part = it.part; K.ldp = it.ldp; K.out = it.out; K.chunks = it.chunks; K.n = it.n; K.cb0 = cb;
-      cb += (int)cdiv(it.n, 64);
+      cb += (int)cdiv(it.n, 16);
       bytes += 4.0 * it.chunks * it.n;
     }
     KernelInfo kf{"colsum_final", 0.0, bytes};
