@@ -13,6 +13,7 @@
 #include <string>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "gemm.h"
 #include "tile.h"
@@ -103,17 +104,25 @@ ORBIT_DEV void epi_apply8(const Epi& e, int64_t bz, int r, int c0, float* v, Out
   st8(C + off, v);
 }
 
+// operand staging: K-major tiles (and every float32 tile) as K-contiguous LDS
+// rows; bf16 M/N-major tiles as they are, read through transposing LDS reads
+template <typename T, bool KMAJ, int ROWS, int KD, int NT>
+using StageOf = std::conditional_t<(!KMAJ && sizeof(T) == 2), GemmStageMN<ROWS, KD, NT>,
+                                   GemmStage<T, ROWS, KD, NT, KMAJ>>;
+
 template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
 __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   constexpr int NT = WM * WN * 64;
   constexpr int BKE = 128 / (int)sizeof(T);
   constexpr int E = 16 / (int)sizeof(T);
-  constexpr int PITCH = BKE + E;
   constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
   static_assert(TM >= 1 && TN >= 1, "wave tile must be at least 32x32");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T* lds = reinterpret_cast<T*>(smem);
-  constexpr int STAGE = (BM + BN) * PITCH;
+  using SA = StageOf<T, AK, BM, BKE, NT>;
+  using SB = StageOf<T, BKM, BN, BKE, NT>;
+  constexpr int STAGE = SA::SIZE + SB::SIZE;
+  static_assert((WM * WN) * 32 * (BN / WN + 8) * 4 <= 2 * STAGE * (int)sizeof(T), "epilogue fits the stages");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
@@ -144,8 +153,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   const int kend = min(g.K, kbeg + g.k_per_split);
   const int nk = (kend - kbeg + BKE - 1) / BKE;
 
-  GemmStage<T, BM, BKE, NT, AK> la;
-  GemmStage<T, BN, BKE, NT, BKM> lb;
+  SA la;
+  SB lb;
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -159,7 +168,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
     la.load(A, nullptr, 0, g.lda, m0, g.M, kbeg, kend, tid);
     lb.load(B, B2, g.k_split, g.ldb, n0, g.N, kbeg, kend, tid);
     la.store(lds, tid);
-    lb.store(lds + BM * PITCH, tid);
+    lb.store(lds + SA::SIZE, tid);
   }
   __syncthreads();
 
@@ -171,16 +180,14 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
       lb.load(B, B2, g.k_split, g.ldb, n0, g.N, k0, kend, tid);
     }
     const T* As = lds + cur * STAGE;
-    const T* Bs = As + BM * PITCH;
+    const T* Bs = As + SA::SIZE;
 #pragma unroll
     for (int kk = 0; kk < BKE / 16; ++kk) {
       Frag<T> af[TM], bfr[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        ld_frag(af[i], As + (wm * WTM + i * 32 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8);
+      for (int i = 0; i < TM; ++i) SA::frag(af[i], As, wm * WTM + i * 32, kk, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        ld_frag(bfr[j], Bs + (wn * WTN + j * 32 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8);
+      for (int j = 0; j < TN; ++j) SB::frag(bfr[j], Bs, wn * WTN + j * 32, kk, lane);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -189,7 +196,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
     if (kt + 1 < nk) {
       T* nxt = lds + (cur ^ 1) * STAGE;
       la.store(nxt, tid);
-      lb.store(nxt + BM * PITCH, tid);
+      lb.store(nxt + SA::SIZE, tid);
     }
     __syncthreads();
   }
@@ -292,35 +299,43 @@ int64_t tiles_of(const Gemm& g, const TileCfg& t) { return cdiv(g.M, t.BM) * cdi
 
 int bke_of(orbit_dtype dt) { return dt == ORBIT_BF16 ? 64 : 32; }
 
-// bf16 products: the (tile, split) pair with the least modelled time. A
-// tile's rate is its throughput measured on MI355X at full occupancy for the
-// operand layout (forward A K-major/B N-major, input gradient both K-major,
-// weight gradient A M-major/B N-major); a launch of `items` work items runs
-// in ceil(items / 256) rounds over the 256 CUs; a split adds its float32
-// partials (written and read back) and the reduction launch.
+// bf16 products: the (tile, split) pair with the least modelled time, from
+// throughputs measured on MI355X per operand layout (forward: A K-major, B
+// N-major; input gradient: both K-major; weight gradient: A M-major, B
+// N-major). A work item (tile x K-slice) costs its K-steps plus ~4 K-steps of
+// prologue/epilogue at the tile's per-CU rate; the busiest CU runs
+// ceil(items / 256) of them. The 4-wave 128x128 tile reaches its rate with two
+// blocks per CU and ~55% of it alone. A split adds its float32 partials,
+// written and read back mostly through the L2/MALL, and the reduction launch.
 struct Choice { TileCfg t; int splits; };
 
 Choice pick_bf16(const Gemm& g) {
-  struct Cand { TileCfg t; double fwd, dx, dw; };  // TFLOP/s
-  const Cand cands[] = {{kT256, 950.0, 1030.0, 780.0},
-                        {kT256x128, 680.0, 850.0, 490.0},
-                        {kT128x256, 600.0, 870.0, 490.0},
-                        {kBig, 600.0, 890.0, 480.0}};
-  const double flops = 2.0 * g.M * g.N * (double)g.K * g.batch;
-  const int64_t ksteps = cdiv(g.K, 64);
+  struct Cand { TileCfg t; double fwd, dx, dw; int slots; };  // TFLOP/s; blocks per CU
+  const Cand cands[] = {{kT256, 1000.0, 1050.0, 960.0, 1},
+                        {kT256x128, 820.0, 830.0, 790.0, 1},
+                        {kT128x256, 800.0, 860.0, 755.0, 1},
+                        {kBig, 790.0, 900.0, 785.0, 2}};
   Choice best{kBig, 1};
   double best_us = 1e300;
   for (const Cand& c : cands) {
     if (g.M < c.t.BM || g.N < c.t.BN) continue;
     const double rate = g.a_kmajor ? (g.b_kmajor ? c.dx : c.fwd) : c.dw;
+    const double cu_flops_per_us = rate * 1e12 / 256.0 * 1e-6;
+    const double kstep_flops = 2.0 * c.t.BM * c.t.BN * 64.0;
     const int64_t tiles = tiles_of(g, c.t);
+    const int64_t ksteps = cdiv(g.K, 64);
     for (int sp = 1; sp <= 16; sp *= 2) {
       if (sp > 1 && (ksteps / sp < 8 || tiles * sp > 2048)) break;
       const int64_t items = tiles * sp;
-      const double rounds = (double)cdiv(items, 256);
-      const double util = (double)items / (rounds * 256.0);
-      double us = flops / (rate * 1e12 * util) * 1e6;
-      if (sp > 1) us += (double)sp * g.M * g.N * g.batch * 8.0 / 5.0e12 * 1e6 + 6.0;
+      const int64_t ks = cdiv(cdiv(g.K, sp), 64);
+      int64_t n = cdiv(items, 256);
+      double eff = 1.0;
+      if (c.slots == 2) {
+        if (n == 1) eff = 0.55;
+        else n = 2 * cdiv(items, 512);
+      }
+      double us = (double)n * (double)(ks + 4) * kstep_flops / (cu_flops_per_us * eff);
+      if (sp > 1) us += (double)sp * g.M * g.N * g.batch * 8.0 / 8.0e12 * 1e6 + 3.0;
       if (us < best_us * 0.98) {
         best_us = us;
         best = {c.t, sp};
@@ -369,7 +384,8 @@ orbit_status run_cfg(const Gemm& g, GemmKArgs& a, hipStream_t s) {
                        (double)g.M * g.N * sizeof(OutT) * g.batch;
   KernelInfo ki{kname<T, OutT, BM, BN, WM, WN, AK, BKM>(), flops, bytes};
   dim3 grid((unsigned)(cdiv(g.N, BN) * cdiv(g.M, BM)), 1, (unsigned)(g.batch * a.splits));
-  constexpr size_t lds = 2 * (size_t)(BM + BN) * (128 + 16);
+  constexpr int NT = WM * WN * 64, BKE = 128 / (int)sizeof(T);
+  constexpr size_t lds = 2 * (size_t)(StageOf<T, AK, BM, BKE, NT>::SIZE + StageOf<T, BKM, BN, BKE, NT>::SIZE) * sizeof(T);
   static const bool attr = [] {
     // lift the default dynamic-LDS cap for this instantiation (a failure here
     // surfaces as a launch error below)

@@ -154,7 +154,13 @@ struct GemmStage {
   static constexpr int PER = (NCH + NT - 1) / NT;
   static constexpr int REGS = KMAJ ? PER : PER * E;
   static_assert(ROWS % E == 0 && KD % E == 0, "tile shape");
+  static constexpr int SIZE = ROWS * PITCH;         // elements of LDS per stage
   U128 r[REGS];
+
+  // MFMA fragment of rows row0 .. row0+31 for the 16-deep step kk
+  static ORBIT_DEV void frag(Frag<T>& f, const T* S, int row0, int kk, int lane) {
+    ld_frag(f, S + (row0 + (lane & 31)) * PITCH + kk * 16 + (lane >> 5) * 8);
+  }
 
   ORBIT_DEV void load(const T* X, const T* X2, int ksplit, int64_t ld, int row0, int rlim, int k0, int kend,
                       int tid) {
@@ -217,47 +223,61 @@ struct GemmStage {
     }
   }
 
-  // M/N-major source only: the transposed copy with mean[row] subtracted from
-  // every element first (float32 arithmetic, rounded back to T)
-  ORBIT_DEV void store_sub(T* S, int tid, const float* mean) const {
-    static_assert(!KMAJ, "store_sub applies to the M/N-major source");
+};
+
+// bf16 M/N-major operand tile kept as it is in HBM: S[k][row], rows
+// contiguous. The row pitch is chosen so that consecutive k-rows start 64 or
+// 192 bytes apart modulo 256: the four k-rows one 16-lane group reads in a
+// transposing LDS read (ds_read_b64_tr_b16) then fall in distinct banks.
+// Staging is a plain 16-byte copy (coalesced along the rows in HBM); the MFMA
+// fragments (8 consecutive k of one row per lane, as the K-major stage gives)
+// come from two transposing reads.
+template <int ROWS, int KD, int NT>
+struct GemmStageMN {
+  using T = bf16;
+  static constexpr int E = 8;
+  static constexpr int PAD = ((2 * ROWS) % 256 == 0 || (2 * ROWS) % 256 == 128) ? 32 : 0;
+  static constexpr int PITCH = ROWS + PAD;
+  static constexpr int RC = ROWS / E;               // 16-byte chunks per k-row
+  static constexpr int NCH = KD * RC;
+  static constexpr int PER = (NCH + NT - 1) / NT;
+  static constexpr int SIZE = KD * PITCH;
+  static_assert(ROWS % E == 0 && KD % 16 == 0, "tile shape");
+  U128 r[PER];
+
+  static ORBIT_DEV void frag(Frag<T>& f, const T* S, int row0, int kk, int lane) {
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const int G = lane >> 4, q = lane & 15;
+    // group G: k-rows 8*(G/2) + q/4 (+4 for the second read), rows 16*(G%2) + 4*(q%4) .. +3;
+    // lane 16G + i receives row 16*(G%2) + i at those four k
+    T* p0 = const_cast<T*>(S) + (kk * 16 + 8 * (G >> 1) + (q >> 2)) * PITCH + row0 + 16 * (G & 1) + 4 * (q & 3);
+    T* p1 = p0 + 4 * PITCH;
+    const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p0);
+    const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p1);
+    const s16x8 xy = __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+    f.v = __builtin_bit_cast(bf16x8, xy);
+  }
+
+  ORBIT_DEV void load(const T* X, const T* X2, int ksplit, int64_t ld, int row0, int rlim, int k0, int kend,
+                      int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      const int kr = c / RC, rc = c % RC;
+      const int gk = k0 + kr, gr = row0 + rc * E;
+      const bool ok = c < NCH && gr < rlim && gk < kend;
+      const T* base = (X2 && gk >= ksplit) ? X2 + (int64_t)(gk - ksplit) * ld : X + (int64_t)gk * ld;
+      r[i] = ok ? ld128(base + gr) : zero128();
+    }
+  }
+
+  ORBIT_DEV void store(T* S, int tid) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
       if (c >= NCH) continue;
-      const int kc = c % KC, rc = c / KC;
-      T* base = S + (rc * E) * PITCH + kc * E;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float m = mean[rc * E + e];
-        float f[8];
-#pragma unroll
-        for (int j = 0; j < E; ++j) f[j] = elem(r[i * E + j], e) - m;
-        st128(base + e * PITCH, pack(f, (T*)nullptr));
-      }
-    }
-  }
-
-  // M/N-major source only: the untransposed copy D[k][row] (pitch dpitch), i.e.
-  // the source rows as they are in HBM
-  ORBIT_DEV void store_rows(T* D, int dpitch, int tid) const {
-    static_assert(!KMAJ, "store_rows applies to the M/N-major source");
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * NT;
-      if (c >= NCH) continue;
-      const int kc = c % KC, rc = c / KC;
-#pragma unroll
-      for (int j = 0; j < E; ++j) st128(D + (kc * E + j) * dpitch + rc * E, r[i * E + j]);
-    }
-  }
-
-  static ORBIT_DEV float elem(const U128& u, int e) {
-    if constexpr (sizeof(T) == 2) {
-      const uint32_t w = u.w[e >> 1];
-      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
-    } else {
-      return __uint_as_float(u.w[e]);
+      st128(S + (c / RC) * PITCH + (c % RC) * E, r[i]);
     }
   }
 };
