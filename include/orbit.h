@@ -153,7 +153,8 @@ orbit_status orbit_patch_embed_bwd(const orbit_embed_desc* desc, const float* im
  * NULL), A = heads*head_dim (a column shard of the projections when A != d,
  * with the W_o row-shard output left unreduced). The library evaluates the
  * exact algebraic refolding (query through W_k, weights applied before W_v),
- * which has the same value. */
+ * which has the same value. heads must divide 64 and be a multiple of 8
+ * (bf16) or 4 (float32); otherwise ORBIT_E_UNSUPPORTED. */
 typedef struct {
   int32_t B, L, V, d, heads, head_dim;
   int32_t dtype;

@@ -421,6 +421,7 @@ static orbit_status embed_check(const char* fn, const orbit_embed_desc* d) {
   REQ(d->H % 4 == 0 && d->W % 4 == 0, ORBIT_E_ARG, "%s: H=%d and W=%d must be multiples of the patch", fn, d->H,
       d->W);
   REQ(d->d % 8 == 0, ORBIT_E_ARG, "%s: d=%d must be a multiple of 8", fn, d->d);
+  REQ((int64_t)d->B * (d->H / 4) * (d->W / 4) * d->V < (1ll << 31), ORBIT_E_UNSUPPORTED, "%s: too many tokens", fn);
   return ORBIT_OK;
 }
 
@@ -466,6 +467,8 @@ static orbit_status agg_check(const char* fn, const orbit_agg_desc* d) {
   // per-token rows of `heads` values are read as 16-byte vectors
   REQ((d->heads * (int)esz(d->dtype)) % 16 == 0, ORBIT_E_UNSUPPORTED,
       "%s: heads=%d must be a multiple of %d for this dtype", fn, d->heads, 16 / (int)esz(d->dtype));
+  // the softmax over variables runs one wave per token with 64 / heads lanes per head
+  REQ(64 % d->heads == 0, ORBIT_E_UNSUPPORTED, "%s: heads=%d must divide 64", fn, d->heads);
   REQ((int64_t)d->B * d->L * d->V < (1ll << 31), ORBIT_E_UNSUPPORTED, "%s: too many tokens", fn);
   return ORBIT_OK;
 }

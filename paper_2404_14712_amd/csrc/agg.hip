@@ -15,6 +15,7 @@
 #include "agg.h"
 #include "gemm.h"
 #include "kernels.h"
+#include "tile.h"
 
 namespace orbit {
 namespace {
@@ -62,47 +63,55 @@ __global__ void __launch_bounds__(256) agg_fold_key(const T* __restrict__ wk, co
   Ut[(int64_t)h * d + i] = from_f<T>(s);
 }
 
-// softmax over v of S[(t*V + v)*H + h]: a32[t][h][v] (float32) and ab[t][h][0..Vp) (dtype, zero padded)
+// softmax over v of S[(t*V + v)*H + h]: a32[t][h][v] (float32) and
+// ab[t][h][0..Vp) (dtype, zero padded). One wave per token: the token's V x H
+// scores are one contiguous block; lane l takes head l % H and variables
+// l / H, l / H + 64 / H, ...; the per-head max and sum combine the lanes of one
+// head in a fixed butterfly order. H divides 64.
 template <typename T>
 __global__ void __launch_bounds__(256) agg_softmax(const float* __restrict__ S, float* __restrict__ a32,
                                                    T* __restrict__ ab, int64_t T_, int V, int Vp, int H) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (t, h)
-  if (idx >= T_ * H) return;
-  const int64_t t = idx / H;
-  const int h = (int)(idx % H);
-  const float* s = S + t * V * H + h;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const int h = lane % H, step = 64 / H;
+  const float* st = S + t * V * H;
   float m = -INFINITY;
-  for (int v = 0; v < V; ++v) m = fmaxf(m, s[(int64_t)v * H]);
+  for (int v = lane / H; v < V; v += step) m = fmaxf(m, st[v * H + h]);
+  for (int o = H; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
   float z = 0.f;
-  for (int v = 0; v < V; ++v) z += __expf(s[(int64_t)v * H] - m);
+  for (int v = lane / H; v < V; v += step) z += __expf(st[v * H + h] - m);
+  for (int o = H; o < 64; o <<= 1) z += __shfl_xor(z, o, 64);
   const float inv = 1.f / z;
-  float* ao = a32 + idx * V;
-  T* bo = ab + idx * Vp;
-  for (int v = 0; v < V; ++v) {
-    const float p = __expf(s[(int64_t)v * H] - m) * inv;
-    ao[v] = p;
+  float* ao = a32 + (t * H + h) * V;
+  T* bo = ab + (t * H + h) * Vp;
+  for (int v = lane / H; v < Vp; v += step) {
+    const float p = v < V ? __expf(st[v * H + h] - m) * inv : 0.f;
+    if (v < V) ao[v] = p;
     bo[v] = from_f<T>(p);
   }
-  for (int v = V; v < Vp; ++v) bo[v] = from_f<T>(0.f);
 }
 
 // softmax backward per (t, h): ds = a (da - sum a da) * scale.
-// ac[(t*V + v)*2H + h] = a, ac[(t*V + v)*2H + H + h] = ds   (dtype)
+// ac[(t*V + v)*2H + h] = a, ac[(t*V + v)*2H + H + h] = ds   (dtype); one wave per
+// token, lanes as in agg_softmax
 template <typename T>
 __global__ void __launch_bounds__(256) agg_softmax_bwd(const float* __restrict__ a32, const float* __restrict__ da,
                                                        T* __restrict__ ac, int64_t T_, int V, int H, float scale) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= T_ * H) return;
-  const int64_t t = idx / H;
-  const int h = (int)(idx % H);
-  const float* a = a32 + idx * V;
-  const float* g = da + idx * V;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const int h = lane % H, step = 64 / H;
+  const float* a = a32 + (t * H + h) * V;
+  const float* g = da + (t * H + h) * V;
   float dot = 0.f;
-  for (int v = 0; v < V; ++v) dot += a[v] * g[v];
+  for (int v = lane / H; v < V; v += step) dot += a[v] * g[v];
+  for (int o = H; o < 64; o <<= 1) dot += __shfl_xor(dot, o, 64);
   T* o = ac + t * V * 2 * H;
-  for (int v = 0; v < V; ++v) {
-    o[(int64_t)v * 2 * H + h] = from_f<T>(a[v]);
-    o[(int64_t)v * 2 * H + H + h] = from_f<T>(a[v] * (g[v] - dot) * scale);
+  for (int v = lane / H; v < V; v += step) {
+    const float av = a[v];
+    o[(int64_t)v * 2 * H + h] = from_f<T>(av);
+    o[(int64_t)v * 2 * H + H + h] = from_f<T>(av * (g[v] - dot) * scale);
   }
 }
 
@@ -161,6 +170,75 @@ __global__ void __launch_bounds__(256) agg_query_bwd(const T* __restrict__ wq, c
   }
 }
 
+// dtok_t [V, d] = [a^T | ds] [V, 2H] . [dxbar_t ; U^T] [2H, d] for bf16, one
+// block per (token, 512 columns): the 2H x 512 right-hand slab is staged in LDS
+// as stored (rows contiguous) and read through transposing LDS reads; the
+// left-hand rows (2H contiguous values per variable) are MFMA fragments read
+// straight from HBM. MT = ceil(V / 32) row tiles, KS = 2H / 16 K-steps.
+constexpr int kDtokCols = 512;
+
+template <int MT, int KS>
+__global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, const bf16* __restrict__ dxbar,
+                                                const bf16* __restrict__ Ut, bf16* __restrict__ dtok, int V, int d,
+                                                int H) {
+  using Stage = GemmStageMN<kDtokCols, 16 * KS, 256>;
+  constexpr int P = Stage::PITCH;
+  __shared__ __attribute__((aligned(16))) bf16 Bs[16 * KS * P];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int64_t t = blockIdx.y;
+  const int c0 = blockIdx.x * kDtokCols;
+  // stage rows k < H from dxbar_t, rows k >= H from U^T (zero past column d)
+  constexpr int RC = kDtokCols / 8;
+  for (int c = tid; c < 16 * KS * RC; c += 256) {
+    const int k = c / RC, cc = c % RC;
+    const int col = c0 + cc * 8;
+    U128 v = zero128();
+    if (col < d) v = ld128(k < H ? dxbar + (t * H + k) * d + col : Ut + (int64_t)(k - H) * d + col);
+    st128(Bs + k * P + cc * 8, v);
+  }
+  Frag<bf16> af[MT][KS];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int v = mt * 32 + (lane & 31);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (v < V) ld_frag(af[mt][ks], ac + (t * V + v) * (2 * H) + ks * 16 + g * 8);
+      else {
+        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        frag_from(af[mt][ks], z);
+      }
+    }
+  }
+  __syncthreads();
+  bf16* out = dtok + t * V * d;
+#pragma unroll 1
+  for (int j = 0; j < kDtokCols / 128; ++j) {
+    const int n0 = wave * (kDtokCols / 4) + j * 32;
+    f32x16 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[mt][i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      Frag<bf16> bfr;
+      Stage::frag(bfr, Bs, n0, ks, lane);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) mma16(acc[mt], af[mt][ks], bfr);
+    }
+    const int col = c0 + n0 + (lane & 31);
+    if (col < d) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int v = mt * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
+          if (v < V) out[(int64_t)v * d + col] = (bf16)acc[mt][i];
+        }
+    }
+  }
+}
+
 unsigned g1(int64_t n) { return (unsigned)std::max<int64_t>(1, cdiv(n, 256)); }
 
 struct Sizes {
@@ -209,15 +287,20 @@ size_t agg_saved_bytes(const orbit_agg_desc& a) {
 // backward workspace: dzh [T, A] | dxbar [T, H, d] | da f32 [T, H, V] | ac [T*V, 2H] | dU f32 [d, H]
 //                     | dq f32 [A] | colsum | gemm split-K
 static size_t gemm_ws_max(const Sizes& z, orbit_dtype dt) {
-  // the only products that may split K are the ones with few output tiles
-  Gemm g = base_gemm(dt);
+  // split-K partials of every product of the forward and backward passes
+  const int T = (int)z.T, TV = (int)(z.T * z.V);
+  const int sh[][6] = {
+      // M, N, K, A K-major, B K-major, batch
+      {TV, z.H, z.d, 1, 1, 1},    {z.H, z.d, z.V, 1, 0, T},   {T, z.dh, z.d, 1, 0, z.H},
+      {T, z.d, z.A, 1, 0, 1},     {z.A, z.d, T, 0, 0, 1},     {T, z.A, z.d, 1, 1, 1},
+      {z.d, z.dh, T, 0, 0, z.H},  {T, z.d, z.dh, 1, 1, z.H},  {z.H, z.V, z.d, 1, 1, T},
+      {z.d, z.H, TV, 0, 0, 1}};
   size_t m = 0;
-  g.M = z.d; g.N = z.H; g.K = (int)(z.T * z.V); g.a_kmajor = false; g.b_kmajor = false;
-  m = std::max(m, gemm_workspace_bytes(g));
-  g.M = z.A; g.N = z.d; g.K = (int)z.T;
-  m = std::max(m, gemm_workspace_bytes(g));
-  g.M = z.d; g.N = z.dh; g.K = (int)z.T; g.batch = z.H;
-  m = std::max(m, gemm_workspace_bytes(g));
+  for (const auto& x : sh) {
+    Gemm g = base_gemm(dt);
+    g.M = x[0]; g.N = x[1]; g.K = x[2]; g.a_kmajor = x[3]; g.b_kmajor = x[4]; g.batch = x[5];
+    m = std::max(m, gemm_workspace_bytes(g));
+  }
   return m;
 }
 
@@ -282,10 +365,10 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
   // 3. softmax over variables
   KernelInfo ks{"agg_softmax", 0.0, (double)TV * z.H * 8};
   if (dt == ORBIT_BF16)
-    ORBIT_TRY(launch(ks, agg_softmax<bf16>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)S, sv.a32,
+    ORBIT_TRY(launch(ks, agg_softmax<bf16>, dim3((unsigned)cdiv(z.T, 4)), dim3(256), 0, s, (const float*)S, sv.a32,
                      (bf16*)ab, z.T, z.V, z.Vp, z.H));
   else
-    ORBIT_TRY(launch(ks, agg_softmax<float>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)S, sv.a32,
+    ORBIT_TRY(launch(ks, agg_softmax<float>, dim3((unsigned)cdiv(z.T, 4)), dim3(256), 0, s, (const float*)S, sv.a32,
                      (float*)ab, z.T, z.V, z.Vp, z.H));
   // 4. xbar_t = a_t [H, V] X_t [V, d]   (batched over tokens)
   {
@@ -398,10 +481,10 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
   // softmax backward -> ac = [a | ds] per (t, v) row
   KernelInfo ksb{"agg_softmax_bwd", 0.0, (double)TV * z.H * (8 + 4 * esz(dt))};
   if (dt == ORBIT_BF16)
-    ORBIT_TRY(launch(ksb, agg_softmax_bwd<bf16>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)sv.a32,
+    ORBIT_TRY(launch(ksb, agg_softmax_bwd<bf16>, dim3((unsigned)cdiv(z.T, 4)), dim3(256), 0, s, (const float*)sv.a32,
                      (const float*)da, (bf16*)ac, z.T, z.V, z.H, scale));
   else
-    ORBIT_TRY(launch(ksb, agg_softmax_bwd<float>, dim3(g1(z.T * z.H)), dim3(256), 0, s, (const float*)sv.a32,
+    ORBIT_TRY(launch(ksb, agg_softmax_bwd<float>, dim3((unsigned)cdiv(z.T, 4)), dim3(256), 0, s, (const float*)sv.a32,
                      (const float*)da, (float*)ac, z.T, z.V, z.H, scale));
   // dU [d, H] = X^T ds  (reduction over all T*V token rows)
   {
@@ -437,6 +520,22 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
                      (const float*)p.w_q, (const float*)dq, gr.q0, gr.b_q, gr.b_k, z.d, z.A, accumulate));
   }
   // dtok_t [V, d] = [a^T | ds] [V, 2H] . [dxbar_t ; U^T] [2H, d]   (batched over tokens)
+  if (dt == ORBIT_BF16 && z.V <= 96 && (z.H == 8 || z.H == 16 || z.H == 32)) {
+    KernelInfo kd{"agg_dtok", 2.0 * z.T * z.V * (double)z.d * 2 * z.H,
+                  (double)z.T * (z.V + z.H) * z.d * 2.0};
+    const dim3 grid((unsigned)cdiv(z.d, kDtokCols), (unsigned)z.T);
+    const int mt = (int)cdiv(z.V, 32), ks = 2 * z.H / 16;
+    const bf16* acp = static_cast<const bf16*>(ac);
+    const bf16* dxp = static_cast<const bf16*>(dxbar);
+    const bf16* up = static_cast<const bf16*>(sv.Ut);
+    bf16* dp = static_cast<bf16*>(dtok);
+#define DTOK(M, K) \
+  if (mt == M && ks == K) return launch(kd, agg_dtok<M, K>, grid, dim3(256), 0, s, acp, dxp, up, dp, z.V, z.d, z.H)
+    DTOK(1, 1); DTOK(2, 1); DTOK(3, 1);
+    DTOK(1, 2); DTOK(2, 2); DTOK(3, 2);
+    DTOK(1, 4); DTOK(2, 4); DTOK(3, 4);
+#undef DTOK
+  }
   {
     Gemm g = base_gemm(dt);
     g.tag = "agg_dtok";

@@ -8,6 +8,7 @@
 #include <algorithm>
 
 #include "kernels.h"
+#include "tile.h"
 
 namespace orbit {
 namespace {
@@ -148,6 +149,90 @@ __global__ void __launch_bounds__(256) patch_bwd_partial(const float* __restrict
   }
 }
 
+// bf16: dW_pe[v] = sum_t P[t,v]^T dtok[t,v,:] on MFMA. A block takes 256
+// columns of one variable over a slice of kPbTokens tokens, 16 tokens per
+// K-step. Left operand rows: the 16 pixels, split exactly enough into bf16
+// high and low parts (two products), plus a row of ones whose product is the
+// bias gradient; right operand: the dtok rows of the step, staged in LDS as
+// stored and read through transposing reads. Partials per token slice in the
+// layout patch_bwd_final sums.
+constexpr int kPbCols = 256;
+constexpr int kPbTokens = 1024;
+
+__global__ void __launch_bounds__(256) patch_bwd_mfma(const float* __restrict__ img, const bf16* __restrict__ dtok,
+                                                      float* __restrict__ part, int V, int Hg, int Wg, int d,
+                                                      int64_t ntok) {
+  using Stage = GemmStageMN<kPbCols, 16, 256>;
+  constexpr int P = Stage::PITCH;
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][16 * P];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int v = blockIdx.y, c0 = blockIdx.x * kPbCols;
+  const int64_t t_begin = (int64_t)blockIdx.z * kPbTokens;
+  const int64_t t_end = std::min<int64_t>(ntok, t_begin + kPbTokens);
+  const int nw = Wg / 4, L = (Hg / 4) * nw;
+  const int p = lane & 31;  // operand row: pixel (0..15), ones (16), zero
+  f32x16 acc_hi[2], acc_lo[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc_hi[j][i] = acc_lo[j][i] = 0.f;
+  Stage st;
+  const bf16* X = dtok + (int64_t)v * d;
+  const int64_t ld = (int64_t)V * d;
+  // token indices of the slice are below 2^31 (checked by the caller)
+  st.load(X, nullptr, 0, ld, c0, d, (int)t_begin, (int)t_end, tid);
+  st.store(Bs[0], tid);
+  __syncthreads();
+  const int nsteps = (int)((t_end - t_begin + 15) / 16);
+  for (int it = 0; it < nsteps; ++it) {
+    const int cur = it & 1;
+    const int64_t t0 = t_begin + (int64_t)it * 16;
+    if (it + 1 < nsteps) st.load(X, nullptr, 0, ld, c0, d, (int)(t0 + 16), (int)t_end, tid);
+    float hi[8], lo[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t t = t0 + 8 * g + j;
+      float val = 0.f, one = 0.f;
+      if (t < t_end) {
+        if (p < 16) {
+          const int b = (int)(t / L), l = (int)(t % L);
+          const int ph = l / nw, pw = l % nw;
+          val = img[(((int64_t)b * V + v) * Hg + ph * 4 + (p >> 2)) * Wg + pw * 4 + (p & 3)];
+        } else if (p == 16) {
+          one = 1.f;
+        }
+      }
+      const float h = (float)(bf16)val;
+      hi[j] = p == 16 ? one : h;
+      lo[j] = val - h;
+    }
+    Frag<bf16> ahi, alo;
+    frag_from(ahi, hi);
+    frag_from(alo, lo);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      Frag<bf16> bfr;
+      Stage::frag(bfr, Bs[cur], wave * 64 + j * 32, 0, lane);
+      mma16(acc_hi[j], ahi, bfr);
+      mma16(acc_lo[j], alo, bfr);
+    }
+    if (it + 1 < nsteps) st.store(Bs[cur ^ 1], tid);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = c0 + wave * 64 + j * 32 + (lane & 31);
+    if (c < d) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = (i >> 2) * 8 + g * 4 + (i & 3);
+        if (r <= 16)
+          part[(((int64_t)blockIdx.z * V + v) * 17 + r) * d + c] = acc_hi[j][i] + (r < 16 ? acc_lo[j][i] : 0.f);
+      }
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256) patch_bwd_final(const float* __restrict__ part, int chunks, int V, int d,
                                                        float* dw, float* db, float* dve, int accumulate) {
   const int64_t per = (int64_t)V * 17 * d;
@@ -191,7 +276,9 @@ size_t patch_embed_bwd_workspace_bytes(int B, int V, int Hg, int Wg, int p, int 
   (void)p;
   const int64_t n = (int64_t)B * (Hg / 4) * (Wg / 4);
   const int lanes = d / 8 >= 256 ? 1 : 256 / (d / 8);
-  return align_up((size_t)cdiv(n, kBwdPatchesPerChunk) * lanes * V * 17 * (size_t)d * sizeof(float));
+  // partials of the float32 path (chunks x lanes) or of the bf16 path (token slices)
+  const int64_t slices = std::max<int64_t>(cdiv(n, kBwdPatchesPerChunk) * lanes, cdiv(n, kPbTokens));
+  return align_up((size_t)slices * V * 17 * (size_t)d * sizeof(float));
 }
 
 orbit_status patch_embed_bwd(orbit_dtype dt, const float* img, const void* dtok, float* dw, float* db, float* dve,
@@ -206,8 +293,14 @@ orbit_status patch_embed_bwd(orbit_dtype dt, const float* img, const void* dtok,
   KernelInfo ki{dt == ORBIT_BF16 ? "patch_bwd_partial<bf16>" : "patch_bwd_partial<f32>", toks * d * 2 * 17,
                 toks * (kPP * 4.0 + d * (dt == ORBIT_BF16 ? 2.0 : 4.0))};
   if (dt == ORBIT_BF16) {
-    ORBIT_TRY(launch(ki, patch_bwd_partial<bf16>, grid, dim3(256), 0, s, img, (const bf16*)dtok, part, B, V, Hg,
-                     Wg, d));
+    const int slices = (int)cdiv(n, kPbTokens);
+    KernelInfo km{"patch_bwd_mfma", toks * d * 2 * 17, toks * (kPP * 4.0 + d * 2.0)};
+    ORBIT_TRY(launch(km, patch_bwd_mfma, dim3((unsigned)cdiv(d, kPbCols), V, slices), dim3(256), 0, s, img,
+                     (const bf16*)dtok, part, V, Hg, Wg, d, n));
+    const int64_t per = (int64_t)V * 17 * d;
+    KernelInfo kf{"patch_bwd_final", 0.0, (double)slices * per * 4};
+    return launch(kf, patch_bwd_final, dim3((unsigned)std::min<int64_t>(cdiv(per, 256), 4096)), dim3(256), 0, s,
+                  (const float*)part, slices, V, d, dw, db, dve, accumulate);
   } else {
     ORBIT_TRY(launch(ki, patch_bwd_partial<float>, grid, dim3(256), 0, s, img, (const float*)dtok, part, B, V,
                      Hg, Wg, d));

@@ -234,27 +234,34 @@ struct CsFinalArgs {
   int nitems, accumulate;
 };
 
-// 16 elements x 16 chunk lanes per block; each lane sums a fixed strided subset
-// of the chunks (8 loads in flight), the 16 lane sums are combined in order
+// EL = 256 / CL elements x CL chunk lanes per block; each lane sums a fixed
+// strided subset of the chunks (8 loads in flight), the CL lane sums are
+// combined in order. CL = 16 for many chunks, 1 for a few.
+template <int CL>
 __global__ void __launch_bounds__(256) colsum_final_kernel(CsFinalArgs a) {
-  __shared__ float red[16][17];
+  constexpr int EL = 256 / CL;
+  __shared__ float red[CL][EL + 1];
   int j = 0;
   while (j + 1 < a.nitems && (int)blockIdx.x >= a.item[j + 1].cb0) ++j;
   const CsFinalK& I = a.item[j];
-  const int el = threadIdx.x & 15, q = threadIdx.x >> 4;
-  const int e = ((int)blockIdx.x - I.cb0) * 16 + el;
+  const int el = threadIdx.x % EL, q = threadIdx.x / EL;
+  const int64_t e = (int64_t)((int)blockIdx.x - I.cb0) * EL + el;
   float s = 0.f;
   if (e < I.n) {
 #pragma unroll 8
-    for (int k = q; k < I.chunks; k += 16) s += I.part[(int64_t)k * I.ldp + e];
+    for (int k = q; k < I.chunks; k += CL) s += I.part[(int64_t)k * I.ldp + e];
   }
-  red[q][el] = s;
-  __syncthreads();
-  if (q == 0 && e < I.n) {
-    float t = 0.f;
+  if constexpr (CL == 1) {
+    if (e < I.n) I.out[e] = a.accumulate ? I.out[e] + s : s;
+  } else {
+    red[q][el] = s;
+    __syncthreads();
+    if (q == 0 && e < I.n) {
+      float t = 0.f;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) t += red[k][el];
-    I.out[e] = a.accumulate ? I.out[e] + t : t;
+      for (int k = 0; k < CL; ++k) t += red[k][el];
+      I.out[e] = a.accumulate ? I.out[e] + t : t;
+    }
   }
 }
 
@@ -551,19 +558,26 @@ void ColFinal::add_job(const ColJob& J, int rows) {
 orbit_status ColFinal::run(int accumulate, hipStream_t s) {
   size_t i = 0;
   while (i < items.size()) {
+    // a launch takes consecutive items of the same kind (many or few chunks)
+    const bool many = items[i].chunks > 8;
+    const int el = many ? 16 : 256;
     CsFinalArgs a{};
     a.accumulate = accumulate;
-    int cb = 0;
+    int64_t cb = 0;
     double bytes = 0;
-    for (; i < items.size() && a.nitems < kColMaxFinal; ++i) {
+    for (; i < items.size() && a.nitems < kColMaxFinal && (items[i].chunks > 8) == many; ++i) {
       const Item& it = items[i];
       CsFinalK& K = a.item[a.nitems++];
-      K.part = it.part; K.ldp = it.ldp; K.out = it.out; K.chunks = it.chunks; K.n = it.n; K.cb0 = cb;
-      cb += (int)cdiv(it.n, 16);
+      K.part = it.part; K.ldp = it.ldp; K.out = it.out; K.chunks = it.chunks; K.n = it.n; K.cb0 = (int)cb;
+      cb += cdiv(it.n, el);
       bytes += 4.0 * it.chunks * it.n;
     }
     KernelInfo kf{"colsum_final", 0.0, bytes};
-    ORBIT_TRY(launch(kf, colsum_final_kernel, dim3((unsigned)cb), dim3(256), 0, s, a));
+    if (many) {
+      ORBIT_TRY(launch(kf, colsum_final_kernel<16>, dim3((unsigned)cb), dim3(256), 0, s, a));
+    } else {
+      ORBIT_TRY(launch(kf, colsum_final_kernel<1>, dim3((unsigned)cb), dim3(256), 0, s, a));
+    }
   }
   items.clear();
   return ORBIT_OK;

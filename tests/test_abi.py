@@ -84,6 +84,10 @@ def test_other_entry_validation(lib):
     assert lib.lib.orbit_patch_embed(ctypes.byref(e), 0x100, 0x200, 0x300, None, 0x400, None) == L.ORBIT_E_ARG
     a = L.AggDesc(1, 4, 5, 64, 4, 16, 1)  # 4 heads in bf16: rows of heads values are not 16 bytes
     assert lib.orbit_var_aggregate_saved_bytes(a) == 0
+    a = L.AggDesc(1, 4, 5, 192, 24, 8, 1)  # 24 heads do not divide 64
+    assert lib.orbit_var_aggregate_saved_bytes(a) == 0
+    a = L.AggDesc(1, 4, 5, 256, 32, 8, 1)
+    assert lib.orbit_var_aggregate_saved_bytes(a) > 0
     h = L.HeadDesc(1, 4, 64, 60, 1, 1e-5, 0)  # out not a multiple of 8
     assert lib.orbit_head_saved_bytes(h) == 0
     assert lib.lib.orbit_mse_loss(0x100, 0x200, 0, 1.0, 0x300, None, 0x400, 1024, None) == L.ORBIT_E_ARG
