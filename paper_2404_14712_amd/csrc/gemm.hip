@@ -1,14 +1,20 @@
-// MFMA GEMM for gfx950 with LDS-staged, register-prefetched double-buffered
-// tiles and a fused epilogue (bias, GELU with pre-activation store, GELU
-// derivative, residual, accumulate). Three operand layouts cover all linear
-// layers: forward (A K-major, B N-major), input gradient (both K-major) and
-// weight gradient (both M/N-major: the reduction runs over tokens).
+// MFMA GEMMs for gfx950 with fused epilogues (bias, GELU with pre-activation
+// store, GELU derivative, residual, accumulate). Three operand layouts cover
+// all linear layers: forward (A K-major, B N-major), input gradient (both
+// K-major) and weight gradient (both M/N-major: the reduction runs over
+// tokens).
 //
-// LDS holds both operands K-contiguous ([row][k], padded by 16 bytes per row)
-// so every MFMA fragment is one 16-byte LDS read. M/N-major operands are
-// transposed on the way in: each thread loads a 4(k) x 16-byte tile from HBM
-// (coalesced along the contiguous dimension) and scatters it as 4-element
-// k-runs.
+// Large bf16 products run on gemm_dma_kernel: 256x256 tiles, 8 waves (two per
+// SIMD, each owning a 128x64 block of C), operands copied HBM -> LDS by the
+// buffer unit (buffer_load ... lds, 16 bytes per lane, no register staging)
+// into a four-stage ring of 32-deep K slices, XOR-swizzled so that both the
+// copies and the MFMA fragment reads are free of bank conflicts. K-major
+// slices are read with ds_read_b128, M/N-major slices (kept as stored) with
+// transposing reads (ds_read_b64_tr_b16).
+//
+// Every other product (float32, small or unaligned shapes, concatenated K)
+// runs on gemm_kernel: register-prefetched, double-buffered LDS tiles with
+// K-contiguous staging.
 #include <stdio.h>
 #include <string>
 
@@ -114,7 +120,6 @@ template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bo
 __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   constexpr int NT = WM * WN * 64;
   constexpr int BKE = 128 / (int)sizeof(T);
-  constexpr int E = 16 / (int)sizeof(T);
   constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
   static_assert(TM >= 1 && TN >= 1, "wave tile must be at least 32x32");
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -249,6 +254,254 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// gemm_dma_kernel: bf16, 256x256x32 stages, 4-stage LDS ring, 8 waves
+// ---------------------------------------------------------------------------
+constexpr int DBM = 256, DBN = 256, DBK = 32, DNS = 4, DWM = 2, DWN = 4;
+constexpr int DNT = DWM * DWN * 64;
+constexpr int DOPB = DBM * DBK * 2;      // bytes of one operand slice (16 KB)
+constexpr int DSTB = 2 * DOPB;           // bytes of one stage (A slice + B slice)
+constexpr int DNL = DOPB / 1024 / (DWM * DWN);  // 1 KB copies per operand slice per wave
+constexpr unsigned kOobOffset = 0x80000000u;    // beyond num_records: the copy reads zeros
+constexpr int kDmaLds = DNS * DSTB;
+
+#define ORBIT_LDS __attribute__((address_space(3)))
+
+ORBIT_DEV __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) {
+  // raw buffer over [base, base + 2 GiB); offsets at or past kOobOffset read zeros
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
+}
+
+// one wave copies 64 x 16 bytes from rsrc + voff (per lane) to LDS byte address
+// lds + 16 * lane. M0 carries the wave-uniform LDS address; the copy is
+// written as inline assembly so that the compiler does not order LDS reads
+// behind it (completion is awaited explicitly with s_waitcnt vmcnt).
+ORBIT_DEV void dma16(__amdgpu_buffer_rsrc_t r, unsigned lds, unsigned voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff), "s"(r)
+               : "memory");
+}
+template <int N> ORBIT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Copy plan of one operand slice (256 rows x 32 k), per lane.
+//  K-major source X[row*ld + k]: LDS row r holds 64 bytes (4 chunks of 8 k);
+//    logical chunk c sits at physical chunk c ^ ((r >> 2) & 3). A 1 KB copy
+//    covers 16 rows.
+//  M/N-major source X[k*ld + row]: LDS k-row kr holds 512 bytes (32 chunks of 8
+//    rows); logical chunk c sits at physical chunk c ^ (4 * (kr & 3)). A 1 KB
+//    copy covers 2 k-rows.
+template <bool KMAJ>
+struct DmaPlan {
+  unsigned voff[DNL];
+  ORBIT_DEV void init(int64_t ld, int row0, int rlim, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < DNL; ++j) {
+      const int blk = wave * DNL + j;
+      if (KMAJ) {
+        const int r = blk * 16 + (lane >> 2);
+        const int c = (lane & 3) ^ ((lane >> 4) & 3);
+        voff[j] = (row0 + r < rlim) ? (unsigned)(r * ld * 2 + c * 16) : kOobOffset;
+      } else {
+        const int kr = blk * 2 + (lane >> 5);
+        const int c = (lane & 31) ^ (4 * (kr & 3));
+        voff[j] = (row0 + c * 8 < rlim) ? (unsigned)(kr * ld * 2 + c * 16) : kOobOffset;
+      }
+    }
+  }
+  ORBIT_DEV void issue(const bf16* base, unsigned lds, int wave) const {
+    const __amdgpu_buffer_rsrc_t r = buffer_rsrc(base);
+#pragma unroll
+    for (int j = 0; j < DNL; ++j) dma16(r, lds + (wave * DNL + j) * 1024, voff[j]);
+  }
+};
+
+// MFMA fragment reads from one operand slice: rows row0 + 32 i + (lane & 31),
+// k-slots 8 (lane >> 5) .. +7 of the 16-deep step kk.
+template <bool KMAJ, int NF>
+struct DmaFrag {
+  unsigned off[NF];
+  unsigned x[2];
+  ORBIT_DEV void init(int row0, int lane) {
+    if (KMAJ) {
+      const int f = (lane >> 2) & 3, h = lane >> 5;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) x[kk] = (unsigned)(((2 * kk + h) ^ f) << 4);
+      off[0] = (unsigned)((row0 + (lane & 31)) * 64);
+    } else {
+      // transposing read: 16-lane group G reads k-rows 8 (G >> 1) + (q >> 2) (and
+      // +4) at rows 16 (G & 1) + 4 (q & 3) .. +3; lane 16 G + i receives row
+      // 16 (G & 1) + i at those k
+      const int G = lane >> 4, q = lane & 15;
+      const int xs = 4 * ((q >> 2) & 3);
+      const int cb = 2 * (G & 1) + ((q & 3) >> 1);
+#pragma unroll
+      for (int i = 0; i < NF; ++i) {
+        const int c = ((row0 >> 3) + i * 4 + cb) ^ xs;
+        off[i] = (unsigned)((8 * (G >> 1) + (q >> 2)) * 512 + c * 16 + (q & 1) * 8);
+      }
+    }
+  }
+  ORBIT_DEV void read(bf16x8& f, const char* S, int i, int kk) const {
+    if (KMAJ) {
+      f = *reinterpret_cast<const bf16x8*>(S + off[0] + i * 2048 + x[kk]);
+    } else {
+      typedef short s16x4 __attribute__((ext_vector_type(4)));
+      const char* p0 = S + off[i] + kk * 8192;
+      const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ORBIT_LDS s16x4*)p0);
+      const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ORBIT_LDS s16x4*)(p0 + 2048));
+      f = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+  }
+};
+
+template <bool AK, bool BKM, typename OutT>
+__global__ void __launch_bounds__(DNT, 1) gemm_dma_kernel(GemmKArgs g) {
+  constexpr int TM = DBM / DWM / 32, TN = DBN / DWN / 32;  // 4 x 2 MFMA tiles per wave
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % DWM, wn = wave / DWM;
+  const int z = blockIdx.z;
+  const int split = z % g.splits;
+  const int64_t bz = z / g.splits;
+
+  // tile order: XCD-contiguous ranges of tile ids, walked in groups of 8 tile rows
+  const int tiles_n = (g.N + DBN - 1) / DBN, tiles_m = (g.M + DBM - 1) / DBM;
+  const int nt = tiles_m * tiles_n;
+  int id = blockIdx.x;
+  const int full = nt - nt % 8;
+  if (id < full) id = (id % 8) * (full / 8) + id / 8;
+  const int per_group = 8 * tiles_n;
+  const int first_m = (id / per_group) * 8;
+  const int gsize = min(tiles_m - first_m, 8);
+  const int tile_m = first_m + (id % per_group) % gsize;
+  const int tile_n = (id % per_group) / gsize;
+  const int m0 = tile_m * DBM, n0 = tile_n * DBN;
+  const int kbeg = split * g.k_per_split;
+  const int kend = min(g.K, kbeg + g.k_per_split);
+  const int nk = max(kend - kbeg, 0) / DBK;
+
+  const bf16* A = static_cast<const bf16*>(g.A) + bz * g.sA;
+  const bf16* B = static_cast<const bf16*>(g.B) + bz * g.sB;
+  const bf16* Ab = AK ? A + (int64_t)m0 * g.lda + kbeg : A + (int64_t)kbeg * g.lda + m0;
+  const bf16* Bb = BKM ? B + (int64_t)n0 * g.ldb + kbeg : B + (int64_t)kbeg * g.ldb + n0;
+  const int64_t a_step = AK ? DBK : (int64_t)DBK * g.lda;
+  const int64_t b_step = BKM ? DBK : (int64_t)DBK * g.ldb;
+
+  DmaPlan<AK> pa;
+  DmaPlan<BKM> pb;
+  pa.init(g.lda, m0, g.M, wave, lane);
+  pb.init(g.ldb, n0, g.N, wave, lane);
+  DmaFrag<AK, TM> ra;
+  DmaFrag<BKM, TN> rb;
+  ra.init(wm * TM * 32, lane);
+  rb.init(wn * TN * 32, lane);
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const unsigned lds0 = (unsigned)(uintptr_t)(ORBIT_LDS void*)smem;
+  auto issue = [&](int st) {
+    const unsigned b = lds0 + (st % DNS) * DSTB;
+    pa.issue(Ab + st * a_step, b, wave);
+    pb.issue(Bb + st * b_step, b + DOPB, wave);
+  };
+  // prologue: stages 0 .. DNS-2 in flight, wait for stage 0 (each wave's
+  // copies complete in issue order; 2 DNL copies per stage per wave)
+#pragma unroll
+  for (int st = 0; st < DNS - 1; ++st)
+    if (st < nk) issue(st);
+  if (nk > 2) wait_vmcnt<4 * DNL>(); else if (nk > 1) wait_vmcnt<2 * DNL>(); else wait_vmcnt<0>();
+  __syncthreads();
+
+  bf16x8 fa[2][TM], fb[2][TN];
+  if (nk > 0) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) ra.read(fa[0][i], smem, i, 0);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) rb.read(fb[0][j], smem + DOPB, j, 0);
+  }
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const char* cur = smem + (kt % DNS) * DSTB;
+    const char* nxt = smem + ((kt + 1) % DNS) * DSTB;
+    // the slot of stage kt + 3 held stage kt - 1, which every wave finished
+    // reading before the barrier that ended the previous iteration
+    if (kt + DNS - 1 < nk) issue(kt + DNS - 1);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) ra.read(fa[1][i], cur, i, 1);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) rb.read(fb[1][j], cur + DOPB, j, 1);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
+    // stage kt + 1 landed (copies of stages kt + 2, kt + 3 may still be in flight)
+    if (kt + 3 < nk) wait_vmcnt<4 * DNL>(); else if (kt + 2 < nk) wait_vmcnt<2 * DNL>(); else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) ra.read(fa[0][i], nxt, i, 0);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) rb.read(fb[0][j], nxt + DOPB, j, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][i], fb[1][j], acc[i][j], 0, 0, 0);
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  // epilogue through LDS: each wave parks 32 rows of its accumulators in a
+  // private region and reads them back as 8 consecutive columns per lane
+  constexpr int WTN = TN * 32, EP = WTN + 8, LPR = WTN / 8, RPI = 64 / LPR;
+  static_assert(DWM * DWN * 32 * EP * 4 <= kDmaLds, "epilogue fits the LDS ring");
+  float* ew = reinterpret_cast<float*>(smem) + wave * 32 * EP;
+  OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
+  const bool raw = g.splits > 1;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        ew[((v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * EP + j * 32 + (lane & 31)] = acc[i][j][v];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll 1
+    for (int it = 0; it < 32 / RPI; ++it) {
+      const int rl = it * RPI + lane / LPR;
+      const int cl = (lane % LPR) * 8;
+      const int r = m0 + wm * TM * 32 + i * 32 + rl;
+      const int c0 = n0 + wn * WTN + cl;
+      float v8[8];
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(ew + rl * EP + cl);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(ew + rl * EP + cl + 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { v8[q] = lo[q]; v8[4 + q] = hi[q]; }
+      if (r < g.M && c0 < g.N) {
+        if (raw) {
+          float* P = g.partial + (((int64_t)split * g.batch + bz) * g.M + r) * g.N;
+          if (g.vec_ok) {
+            st8(P + c0, v8);
+          } else {
+            for (int q = 0; q < 8 && c0 + q < g.N; ++q) P[c0 + q] = v8[q];
+          }
+        } else if (g.vec_ok) {
+          epi_apply8<bf16, OutT>(g.epi, bz, r, c0, v8, C, g.ldc);
+        } else {
+          for (int q = 0; q < 8 && c0 + q < g.N; ++q) epi_apply<bf16, OutT>(g.epi, bz, r, c0 + q, v8[q], C, g.ldc);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 // C = epilogue(sum over splits of the float32 partials): 8 consecutive columns
 // per thread, rows on grid.y (strided), batch on grid.z; 32-bit index math
 template <typename T, typename OutT>
@@ -285,8 +538,12 @@ __global__ void __launch_bounds__(64) splitk_reduce(GemmKArgs g) {
 // ---------------------------------------------------------------------------
 struct TileCfg {
   int BM, BN, WM, WN;
-  bool operator==(const TileCfg& o) const { return BM == o.BM && BN == o.BN && WM == o.WM && WN == o.WN; }
+  bool dma = false;  // gemm_dma_kernel (bf16 only)
+  bool operator==(const TileCfg& o) const {
+    return BM == o.BM && BN == o.BN && WM == o.WM && WN == o.WN && dma == o.dma;
+  }
 };
+constexpr TileCfg kDma{DBM, DBN, DWM, DWN, true};
 constexpr TileCfg kT256{256, 256, 2, 4};
 constexpr TileCfg kT256x128{256, 128, 4, 2};
 constexpr TileCfg kT128x256{128, 256, 2, 4};
@@ -298,6 +555,16 @@ constexpr TileCfg kSmall{64, 64, 2, 2};
 int64_t tiles_of(const Gemm& g, const TileCfg& t) { return cdiv(g.M, t.BM) * cdiv(g.N, t.BN) * (int64_t)g.batch; }
 
 int bke_of(orbit_dtype dt) { return dt == ORBIT_BF16 ? 64 : 32; }
+
+// gemm_dma_kernel's requirements: whole 32-deep K slices, 16-byte aligned
+// operand rows, and per-lane byte offsets within a tile below 2^31
+bool dma_ok(const Gemm& g) {
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+  const int64_t lim = (int64_t)1 << 24;
+  return g.dtype == ORBIT_BF16 && g.B2 == nullptr && g.K % DBK == 0 && (g.a_kmajor || !g.b_kmajor) &&
+         g.lda % 8 == 0 && g.ldb % 8 == 0 && g.sA % 8 == 0 && g.sB % 8 == 0 && g.lda < lim && g.ldb < lim &&
+         al16(g.A) && al16(g.B);
+}
 
 // bf16 products: the (tile, split) pair with the least modelled time, from
 // throughputs measured on MI355X per operand layout (forward: A K-major, B
@@ -311,14 +578,17 @@ struct Choice { TileCfg t; int splits; };
 
 Choice pick_bf16(const Gemm& g) {
   struct Cand { TileCfg t; double fwd, dx, dw; int slots; };  // TFLOP/s; blocks per CU
-  const Cand cands[] = {{kT256, 1000.0, 1050.0, 960.0, 1},
+  const Cand cands[] = {{kDma, 1190.0, 1200.0, 1190.0, 1},
+                        {kT256, 1000.0, 1050.0, 960.0, 1},
                         {kT256x128, 820.0, 830.0, 790.0, 1},
                         {kT128x256, 800.0, 860.0, 755.0, 1},
                         {kBig, 790.0, 900.0, 785.0, 2}};
+  const bool dma = dma_ok(g);
   Choice best{kBig, 1};
   double best_us = 1e300;
   for (const Cand& c : cands) {
     if (g.M < c.t.BM || g.N < c.t.BN) continue;
+    if (c.t.dma && !dma) continue;
     const double rate = g.a_kmajor ? (g.b_kmajor ? c.dx : c.fwd) : c.dw;
     const double cu_flops_per_us = rate * 1e12 / 256.0 * 1e-6;
     const double kstep_flops = 2.0 * c.t.BM * c.t.BN * 64.0;
@@ -366,6 +636,29 @@ int pick_splits(const Gemm& g, const TileCfg& t) {
   return (int)std::max<int64_t>(s, 1);
 }
 
+template <typename OutT>
+orbit_status splitk_finish(const Gemm& g, GemmKArgs& a, hipStream_t s);
+
+template <bool AK, bool BKM, typename OutT>
+orbit_status run_dma(const Gemm& g, GemmKArgs& a, hipStream_t s) {
+  static const std::string name = std::string("gemm_dma<") + (AK ? "AK" : "AM") + "," + (BKM ? "BK" : "BN") + "," +
+                                  (sizeof(OutT) == 2 ? "bf16" : "f32") + ">";
+  const double flops = 2.0 * g.M * g.N * (double)g.K * g.batch;
+  const double bytes = ((double)g.M * g.K + (double)g.K * g.N) * 2.0 * g.batch +
+                       (double)g.M * g.N * sizeof(OutT) * g.batch;
+  KernelInfo ki{name.c_str(), flops, bytes};
+  static const bool attr = [] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_dma_kernel<AK, BKM, OutT>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kDmaLds);
+    (void)hipGetLastError();
+    return true;
+  }();
+  (void)attr;
+  dim3 grid((unsigned)(cdiv(g.N, DBN) * cdiv(g.M, DBM)), 1, (unsigned)(g.batch * a.splits));
+  ORBIT_TRY(launch(ki, gemm_dma_kernel<AK, BKM, OutT>, grid, dim3(DNT), (size_t)kDmaLds, s, a));
+  return a.splits > 1 ? splitk_finish<OutT>(g, a, s) : ORBIT_OK;
+}
+
 template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
 const char* kname() {
   static std::string s = [] {
@@ -396,19 +689,23 @@ orbit_status run_cfg(const Gemm& g, GemmKArgs& a, hipStream_t s) {
   }();
   (void)attr;
   ORBIT_TRY(launch(ki, gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>, grid, dim3(WM * WN * 64), lds, s, a));
-  if (a.splits > 1) {
-    const int64_t total = (int64_t)g.M * g.N * g.batch;
-    KernelInfo kr{sizeof(OutT) == 2 ? "splitk_reduce<bf16>" : "splitk_reduce<f32>", 0.0,
-                  (double)total * 4 * (a.splits + 1)};
-    const dim3 grid((unsigned)cdiv(g.N, 512), (unsigned)std::min(g.M, 16384), (unsigned)g.batch);
-    ORBIT_TRY(launch(kr, splitk_reduce<T, OutT>, grid, dim3(64), 0, s, a));
-  }
-  return ORBIT_OK;
+  return a.splits > 1 ? splitk_finish<OutT>(g, a, s) : ORBIT_OK;
+}
+
+template <typename OutT>
+orbit_status splitk_finish(const Gemm& g, GemmKArgs& a, hipStream_t s) {
+  const int64_t total = (int64_t)g.M * g.N * g.batch;
+  KernelInfo kr{sizeof(OutT) == 2 ? "splitk_reduce<bf16>" : "splitk_reduce<f32>", 0.0,
+                (double)total * 4 * (a.splits + 1)};
+  const dim3 grid((unsigned)cdiv(g.N, 512), (unsigned)std::min(g.M, 16384), (unsigned)g.batch);
+  if (g.dtype == ORBIT_BF16) return launch(kr, splitk_reduce<bf16, OutT>, grid, dim3(64), 0, s, a);
+  return launch(kr, splitk_reduce<float, OutT>, grid, dim3(64), 0, s, a);
 }
 
 template <typename T, typename OutT, bool AK, bool BKM>
 orbit_status run_layout(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
+    if (t.dma) return run_dma<AK, BKM, OutT>(g, a, s);
     if (t.BM == 256 && t.BN == 256 && t.WM == 2) return run_cfg<T, OutT, 256, 256, 2, 4, AK, BKM>(g, a, s);
     if (t.BM == 256 && t.BN == 256 && t.WM == 4) return run_cfg<T, OutT, 256, 256, 4, 2, AK, BKM>(g, a, s);
     if (t.BM == 256 && t.BN == 128) return run_cfg<T, OutT, 256, 128, 4, 2, AK, BKM>(g, a, s);
