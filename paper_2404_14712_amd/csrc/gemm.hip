@@ -255,15 +255,10 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// gemm_dma_kernel: bf16, 256x256x32 stages, 4-stage LDS ring, 8 waves
+// gemm_dma_kernel: bf16, 32-deep K stages in an NS-deep LDS ring
 // ---------------------------------------------------------------------------
-constexpr int DBM = 256, DBN = 256, DBK = 32, DNS = 4, DWM = 2, DWN = 4;
-constexpr int DNT = DWM * DWN * 64;
-constexpr int DOPB = DBM * DBK * 2;      // bytes of one operand slice (16 KB)
-constexpr int DSTB = 2 * DOPB;           // bytes of one stage (A slice + B slice)
-constexpr int DNL = DOPB / 1024 / (DWM * DWN);  // 1 KB copies per operand slice per wave
+constexpr int DBK = 32;
 constexpr unsigned kOobOffset = 0x80000000u;    // beyond num_records: the copy reads zeros
-constexpr int kDmaLds = DNS * DSTB;
 
 #define ORBIT_LDS __attribute__((address_space(3)))
 
@@ -282,27 +277,31 @@ ORBIT_DEV void dma16(__amdgpu_buffer_rsrc_t r, unsigned lds, unsigned voff) {
 }
 template <int N> ORBIT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
-// Copy plan of one operand slice (256 rows x 32 k), per lane.
+// Copy plan of one operand slice (ROWS rows x 32 k) over NW waves, per lane.
 //  K-major source X[row*ld + k]: LDS row r holds 64 bytes (4 chunks of 8 k);
 //    logical chunk c sits at physical chunk c ^ ((r >> 2) & 3). A 1 KB copy
 //    covers 16 rows.
-//  M/N-major source X[k*ld + row]: LDS k-row kr holds 512 bytes (32 chunks of 8
-//    rows); logical chunk c sits at physical chunk c ^ (4 * (kr & 3)). A 1 KB
-//    copy covers 2 k-rows.
-template <bool KMAJ>
+//  M/N-major source X[k*ld + row]: LDS k-row kr holds 2 ROWS bytes (ROWS / 8
+//    chunks of 8 rows); logical chunk c sits at physical chunk c ^ (4 (kr & 3)).
+//    A 1 KB copy covers 512 / ROWS k-rows.
+template <bool KMAJ, int ROWS, int NW>
 struct DmaPlan {
-  unsigned voff[DNL];
+  static constexpr int BYTES = ROWS * DBK * 2;
+  static constexpr int NL = BYTES / 1024 / NW;  // 1 KB copies per wave
+  static_assert(NL >= 1 && BYTES % (1024 * NW) == 0, "copy split");
+  unsigned voff[NL];
   ORBIT_DEV void init(int64_t ld, int row0, int rlim, int wave, int lane) {
 #pragma unroll
-    for (int j = 0; j < DNL; ++j) {
-      const int blk = wave * DNL + j;
+    for (int j = 0; j < NL; ++j) {
+      const int blk = wave * NL + j;
       if (KMAJ) {
         const int r = blk * 16 + (lane >> 2);
         const int c = (lane & 3) ^ ((lane >> 4) & 3);
         voff[j] = (row0 + r < rlim) ? (unsigned)(r * ld * 2 + c * 16) : kOobOffset;
       } else {
-        const int kr = blk * 2 + (lane >> 5);
-        const int c = (lane & 31) ^ (4 * (kr & 3));
+        constexpr int CPR = ROWS / 8, KPB = 64 / CPR;
+        const int kr = blk * KPB + lane / CPR;
+        const int c = (lane % CPR) ^ (4 * (kr & 3));
         voff[j] = (row0 + c * 8 < rlim) ? (unsigned)(kr * ld * 2 + c * 16) : kOobOffset;
       }
     }
@@ -310,13 +309,13 @@ struct DmaPlan {
   ORBIT_DEV void issue(const bf16* base, unsigned lds, int wave) const {
     const __amdgpu_buffer_rsrc_t r = buffer_rsrc(base);
 #pragma unroll
-    for (int j = 0; j < DNL; ++j) dma16(r, lds + (wave * DNL + j) * 1024, voff[j]);
+    for (int j = 0; j < NL; ++j) dma16(r, lds + (wave * NL + j) * 1024, voff[j]);
   }
 };
 
 // MFMA fragment reads from one operand slice: rows row0 + 32 i + (lane & 31),
 // k-slots 8 (lane >> 5) .. +7 of the 16-deep step kk.
-template <bool KMAJ, int NF>
+template <bool KMAJ, int NF, int ROWS>
 struct DmaFrag {
   unsigned off[NF];
   unsigned x[2];
@@ -336,7 +335,7 @@ struct DmaFrag {
 #pragma unroll
       for (int i = 0; i < NF; ++i) {
         const int c = ((row0 >> 3) + i * 4 + cb) ^ xs;
-        off[i] = (unsigned)((8 * (G >> 1) + (q >> 2)) * 512 + c * 16 + (q & 1) * 8);
+        off[i] = (unsigned)((8 * (G >> 1) + (q >> 2)) * (2 * ROWS) + c * 16 + (q & 1) * 8);
       }
     }
   }
@@ -345,27 +344,57 @@ struct DmaFrag {
       f = *reinterpret_cast<const bf16x8*>(S + off[0] + i * 2048 + x[kk]);
     } else {
       typedef short s16x4 __attribute__((ext_vector_type(4)));
-      const char* p0 = S + off[i] + kk * 8192;
+      const char* p0 = S + off[i] + kk * 16 * (2 * ROWS);
       const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ORBIT_LDS s16x4*)p0);
-      const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ORBIT_LDS s16x4*)(p0 + 2048));
+      const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ORBIT_LDS s16x4*)(p0 + 4 * (2 * ROWS)));
       f = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
     }
   }
 };
 
-template <bool AK, bool BKM, typename OutT>
-__global__ void __launch_bounds__(DNT, 1) gemm_dma_kernel(GemmKArgs g) {
-  constexpr int TM = DBM / DWM / 32, TN = DBN / DWN / 32;  // 4 x 2 MFMA tiles per wave
+// Tile configurations of the direct-to-LDS kernel. BIG: 256x256 on 8 waves
+// (two per SIMD, 128x64 each), four stages, one block per CU. HALF: 256x128
+// on 4 waves (128x64 each), three stages (72 KB), two independent blocks per
+// CU, which fills the GPU on products with few 256x256 tiles.
+template <int BM_, int BN_, int WM_, int WN_, int NS_, int OCC_>
+struct DmaCfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_, OCC = OCC_;
+  static constexpr int NW = WM * WN, NT = NW * 64;
+  static constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+  static constexpr int OPA = BM * DBK * 2, OPB = BN * DBK * 2, STB = OPA + OPB;
+  static constexpr int EPB = NW * 32 * (TN * 32 + 8) * 4;   // epilogue staging
+  static constexpr int LDS = NS * STB > EPB ? NS * STB : EPB;
+};
+using DmaBig = DmaCfg<256, 256, 2, 4, 4, 1>;
+using DmaHalf = DmaCfg<256, 128, 2, 2, 3, 2>;
+
+// wait until stage s has landed when copies of the next `ahead` stages
+// (each NLS copies per wave) may still be in flight
+template <int NLS, int NS>
+ORBIT_DEV void wait_stage(int ahead) {
+  static_assert(NS == 3 || NS == 4, "ring depth");
+  if (NS == 4 && ahead >= 2) wait_vmcnt<2 * NLS>();
+  else if (ahead >= 1) wait_vmcnt<NLS>();
+  else wait_vmcnt<0>();
+}
+
+template <bool AK, bool BKM, typename OutT, typename CF>
+__global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) {
+  constexpr int BM = CF::BM, BN = CF::BN, WM = CF::WM, NS = CF::NS;
+  constexpr int TM = CF::TM, TN = CF::TN, OPA = CF::OPA, STB = CF::STB;
+  using PA = DmaPlan<AK, BM, CF::NW>;
+  using PB = DmaPlan<BKM, BN, CF::NW>;
+  constexpr int NLS = PA::NL + PB::NL;  // copies per stage per wave
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave % DWM, wn = wave / DWM;
+  const int wm = wave % WM, wn = wave / WM;
   const int z = blockIdx.z;
   const int split = z % g.splits;
   const int64_t bz = z / g.splits;
 
   // tile order: XCD-contiguous ranges of tile ids, walked in groups of 8 tile rows
-  const int tiles_n = (g.N + DBN - 1) / DBN, tiles_m = (g.M + DBM - 1) / DBM;
+  const int tiles_n = (g.N + BN - 1) / BN, tiles_m = (g.M + BM - 1) / BM;
   const int nt = tiles_m * tiles_n;
   int id = blockIdx.x;
   const int full = nt - nt % 8;
@@ -375,7 +404,7 @@ __global__ void __launch_bounds__(DNT, 1) gemm_dma_kernel(GemmKArgs g) {
   const int gsize = min(tiles_m - first_m, 8);
   const int tile_m = first_m + (id % per_group) % gsize;
   const int tile_n = (id % per_group) / gsize;
-  const int m0 = tile_m * DBM, n0 = tile_n * DBN;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
   const int kbeg = split * g.k_per_split;
   const int kend = min(g.K, kbeg + g.k_per_split);
   const int nk = max(kend - kbeg, 0) / DBK;
@@ -387,12 +416,12 @@ __global__ void __launch_bounds__(DNT, 1) gemm_dma_kernel(GemmKArgs g) {
   const int64_t a_step = AK ? DBK : (int64_t)DBK * g.lda;
   const int64_t b_step = BKM ? DBK : (int64_t)DBK * g.ldb;
 
-  DmaPlan<AK> pa;
-  DmaPlan<BKM> pb;
+  PA pa;
+  PB pb;
   pa.init(g.lda, m0, g.M, wave, lane);
   pb.init(g.ldb, n0, g.N, wave, lane);
-  DmaFrag<AK, TM> ra;
-  DmaFrag<BKM, TN> rb;
+  DmaFrag<AK, TM, BM> ra;
+  DmaFrag<BKM, TN, BN> rb;
   ra.init(wm * TM * 32, lane);
   rb.init(wn * TN * 32, lane);
 
@@ -406,49 +435,48 @@ __global__ void __launch_bounds__(DNT, 1) gemm_dma_kernel(GemmKArgs g) {
 
   const unsigned lds0 = (unsigned)(uintptr_t)(ORBIT_LDS void*)smem;
   auto issue = [&](int st) {
-    const unsigned b = lds0 + (st % DNS) * DSTB;
+    const unsigned b = lds0 + (st % NS) * STB;
     pa.issue(Ab + st * a_step, b, wave);
-    pb.issue(Bb + st * b_step, b + DOPB, wave);
+    pb.issue(Bb + st * b_step, b + OPA, wave);
   };
-  // prologue: stages 0 .. DNS-2 in flight, wait for stage 0 (each wave's
-  // copies complete in issue order; 2 DNL copies per stage per wave)
+  // prologue: stages 0 .. NS-2 in flight (each wave's copies complete in issue
+  // order), then wait for stage 0
 #pragma unroll
-  for (int st = 0; st < DNS - 1; ++st)
+  for (int st = 0; st < NS - 1; ++st)
     if (st < nk) issue(st);
-  if (nk > 2) wait_vmcnt<4 * DNL>(); else if (nk > 1) wait_vmcnt<2 * DNL>(); else wait_vmcnt<0>();
+  wait_stage<NLS, NS>(min(nk - 1, NS - 2));
   __syncthreads();
 
   bf16x8 fa[2][TM], fb[2][TN];
-  if (nk > 0) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i) ra.read(fa[0][i], smem, i, 0);
+  for (int i = 0; i < TM; ++i) ra.read(fa[0][i], smem, i, 0);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) rb.read(fb[0][j], smem + DOPB, j, 0);
-  }
+  for (int j = 0; j < TN; ++j) rb.read(fb[0][j], smem + OPA, j, 0);
 
   for (int kt = 0; kt < nk; ++kt) {
-    const char* cur = smem + (kt % DNS) * DSTB;
-    const char* nxt = smem + ((kt + 1) % DNS) * DSTB;
-    // the slot of stage kt + 3 held stage kt - 1, which every wave finished
+    const char* cur = smem + (kt % NS) * STB;
+    const char* nxt = smem + ((kt + 1) % NS) * STB;
+    // the slot of stage kt + NS - 1 held stage kt - 1, which every wave finished
     // reading before the barrier that ended the previous iteration
-    if (kt + DNS - 1 < nk) issue(kt + DNS - 1);
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
 #pragma unroll
     for (int i = 0; i < TM; ++i) ra.read(fa[1][i], cur, i, 1);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) rb.read(fb[1][j], cur + DOPB, j, 1);
+    for (int j = 0; j < TN; ++j) rb.read(fb[1][j], cur + OPA, j, 1);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
-    // stage kt + 1 landed (copies of stages kt + 2, kt + 3 may still be in flight)
-    if (kt + 3 < nk) wait_vmcnt<4 * DNL>(); else if (kt + 2 < nk) wait_vmcnt<2 * DNL>(); else wait_vmcnt<0>();
+    // stage kt + 1 landed (copies of the stages after it may still be in flight)
+    wait_stage<NLS, NS>(min(nk - kt - 2, NS - 2));
     __syncthreads();
-    if (kt + 1 < nk) {
+    // next stage's first fragments (unconditionally: past the last stage this
+    // reads a stale but in-bounds slot, and keeping the loop branch-free lets
+    // the reads overlap the MFMAs below)
 #pragma unroll
-      for (int i = 0; i < TM; ++i) ra.read(fa[0][i], nxt, i, 0);
+    for (int i = 0; i < TM; ++i) ra.read(fa[0][i], nxt, i, 0);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) rb.read(fb[0][j], nxt + DOPB, j, 0);
-    }
+    for (int j = 0; j < TN; ++j) rb.read(fb[0][j], nxt + OPA, j, 0);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -460,7 +488,6 @@ __global__ void __launch_bounds__(DNT, 1) gemm_dma_kernel(GemmKArgs g) {
   // epilogue through LDS: each wave parks 32 rows of its accumulators in a
   // private region and reads them back as 8 consecutive columns per lane
   constexpr int WTN = TN * 32, EP = WTN + 8, LPR = WTN / 8, RPI = 64 / LPR;
-  static_assert(DWM * DWN * 32 * EP * 4 <= kDmaLds, "epilogue fits the LDS ring");
   float* ew = reinterpret_cast<float*>(smem) + wave * 32 * EP;
   OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
   const bool raw = g.splits > 1;
@@ -543,7 +570,8 @@ struct TileCfg {
     return BM == o.BM && BN == o.BN && WM == o.WM && WN == o.WN && dma == o.dma;
   }
 };
-constexpr TileCfg kDma{DBM, DBN, DWM, DWN, true};
+constexpr TileCfg kDma{DmaBig::BM, DmaBig::BN, DmaBig::WM, DmaBig::WN, true};
+constexpr TileCfg kDmaHalf{DmaHalf::BM, DmaHalf::BN, DmaHalf::WM, DmaHalf::WN, true};
 constexpr TileCfg kT256{256, 256, 2, 4};
 constexpr TileCfg kT256x128{256, 128, 4, 2};
 constexpr TileCfg kT128x256{128, 256, 2, 4};
@@ -571,18 +599,20 @@ bool dma_ok(const Gemm& g) {
 // N-major; input gradient: both K-major; weight gradient: A M-major, B
 // N-major). A work item (tile x K-slice) costs its K-steps plus ~4 K-steps of
 // prologue/epilogue at the tile's per-CU rate; the busiest CU runs
-// ceil(items / 256) of them. The 4-wave 128x128 tile reaches its rate with two
-// blocks per CU and ~55% of it alone. A split adds its float32 partials,
+// ceil(items / 256) of them. Tiles that run two blocks per CU reach their rate
+// only with both resident (55-67% of it alone). A split adds its float32 partials,
 // written and read back mostly through the L2/MALL, and the reduction launch.
 struct Choice { TileCfg t; int splits; };
 
 Choice pick_bf16(const Gemm& g) {
-  struct Cand { TileCfg t; double fwd, dx, dw; int slots; };  // TFLOP/s; blocks per CU
-  const Cand cands[] = {{kDma, 1190.0, 1200.0, 1190.0, 1},
-                        {kT256, 1000.0, 1050.0, 960.0, 1},
-                        {kT256x128, 820.0, 830.0, 790.0, 1},
-                        {kT128x256, 800.0, 860.0, 755.0, 1},
-                        {kBig, 790.0, 900.0, 785.0, 2}};
+  // TFLOP/s per layout; blocks per CU; fraction of the rate with one block per CU
+  struct Cand { TileCfg t; double fwd, dx, dw; int slots; double eff1; };
+  const Cand cands[] = {{kDma, 1250.0, 1300.0, 1290.0, 1, 1.0},
+                        {kDmaHalf, 1070.0, 1030.0, 1140.0, 2, 0.67},
+                        {kT256, 1000.0, 1050.0, 960.0, 1, 1.0},
+                        {kT256x128, 820.0, 830.0, 790.0, 1, 1.0},
+                        {kT128x256, 800.0, 860.0, 755.0, 1, 1.0},
+                        {kBig, 790.0, 900.0, 785.0, 2, 0.55}};
   const bool dma = dma_ok(g);
   Choice best{kBig, 1};
   double best_us = 1e300;
@@ -601,7 +631,7 @@ Choice pick_bf16(const Gemm& g) {
       int64_t n = cdiv(items, 256);
       double eff = 1.0;
       if (c.slots == 2) {
-        if (n == 1) eff = 0.55;
+        if (n == 1) eff = c.eff1;
         else n = 2 * cdiv(items, 512);
       }
       double us = (double)n * (double)(ks + 4) * kstep_flops / (cu_flops_per_us * eff);
@@ -639,23 +669,24 @@ int pick_splits(const Gemm& g, const TileCfg& t) {
 template <typename OutT>
 orbit_status splitk_finish(const Gemm& g, GemmKArgs& a, hipStream_t s);
 
-template <bool AK, bool BKM, typename OutT>
+template <bool AK, bool BKM, typename OutT, typename CF>
 orbit_status run_dma(const Gemm& g, GemmKArgs& a, hipStream_t s) {
-  static const std::string name = std::string("gemm_dma<") + (AK ? "AK" : "AM") + "," + (BKM ? "BK" : "BN") + "," +
+  static const std::string name = std::string("gemm_dma<") + std::to_string(CF::BM) + "x" + std::to_string(CF::BN) +
+                                  "," + (AK ? "AK" : "AM") + "," + (BKM ? "BK" : "BN") + "," +
                                   (sizeof(OutT) == 2 ? "bf16" : "f32") + ">";
   const double flops = 2.0 * g.M * g.N * (double)g.K * g.batch;
   const double bytes = ((double)g.M * g.K + (double)g.K * g.N) * 2.0 * g.batch +
                        (double)g.M * g.N * sizeof(OutT) * g.batch;
   KernelInfo ki{name.c_str(), flops, bytes};
   static const bool attr = [] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_dma_kernel<AK, BKM, OutT>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, kDmaLds);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_dma_kernel<AK, BKM, OutT, CF>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, CF::LDS);
     (void)hipGetLastError();
     return true;
   }();
   (void)attr;
-  dim3 grid((unsigned)(cdiv(g.N, DBN) * cdiv(g.M, DBM)), 1, (unsigned)(g.batch * a.splits));
-  ORBIT_TRY(launch(ki, gemm_dma_kernel<AK, BKM, OutT>, grid, dim3(DNT), (size_t)kDmaLds, s, a));
+  dim3 grid((unsigned)(cdiv(g.N, CF::BN) * cdiv(g.M, CF::BM)), 1, (unsigned)(g.batch * a.splits));
+  ORBIT_TRY(launch(ki, gemm_dma_kernel<AK, BKM, OutT, CF>, grid, dim3(CF::NT), (size_t)CF::LDS, s, a));
   return a.splits > 1 ? splitk_finish<OutT>(g, a, s) : ORBIT_OK;
 }
 
@@ -705,7 +736,8 @@ orbit_status splitk_finish(const Gemm& g, GemmKArgs& a, hipStream_t s) {
 template <typename T, typename OutT, bool AK, bool BKM>
 orbit_status run_layout(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
-    if (t.dma) return run_dma<AK, BKM, OutT>(g, a, s);
+    if (t.dma && t.BN == DmaHalf::BN) return run_dma<AK, BKM, OutT, DmaHalf>(g, a, s);
+    if (t.dma) return run_dma<AK, BKM, OutT, DmaBig>(g, a, s);
     if (t.BM == 256 && t.BN == 256 && t.WM == 2) return run_cfg<T, OutT, 256, 256, 2, 4, AK, BKM>(g, a, s);
     if (t.BM == 256 && t.BN == 256 && t.WM == 4) return run_cfg<T, OutT, 256, 256, 4, 2, AK, BKM>(g, a, s);
     if (t.BM == 256 && t.BN == 128) return run_cfg<T, OutT, 256, 128, 4, 2, AK, BKM>(g, a, s);

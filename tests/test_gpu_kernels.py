@@ -22,7 +22,8 @@ GEMM_SHAPES = [(37, 40, 24), (200, 136, 72), (130, 264, 520), (1, 48, 64), (300,
                (24, 520, 200), (48, 1032, 40), (60, 264, 136),
                (257, 129 * 8, 8),
                # direct-to-LDS kernel: ragged tiles, odd stage counts, split-K
-               (300, 520, 256), (520, 1032, 1024), (1000, 264, 4096), (264, 2048, 544)]
+               (300, 520, 256), (520, 1032, 1024), (1000, 264, 4096), (264, 2048, 544),
+               (1024, 512, 2048), (2048, 1024, 1024), (776, 392, 1056)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
