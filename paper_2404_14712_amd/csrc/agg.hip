@@ -20,33 +20,54 @@
 namespace orbit {
 namespace {
 
-// Column reductions out[j] = sum_i x_i W[i][j] over the d rows of a [d, A]
-// weight: 64 columns x 16 row lanes per block (coalesced row reads), the 16
-// partial sums combined in a fixed order.
-constexpr int kGvCols = 64, kGvLanes = 16;
+// Weighted column sums out[j] = sum_i c_ij W[i][j] over the d rows of a [d, A]
+// weight, with c_ij = x[i] (query projection) or dU[i][j / dh] (query
+// gradient). Phase 1: one block per slice of kGvRows rows, threads along the
+// columns (coalesced row reads), one float32 partial per (slice, column);
+// phase 2 sums the slices in order (deterministic).
+constexpr int kGvRows = 64;
 
-ORBIT_DEV float gv_combine(float s, float (*red)[kGvCols], int cl, int q) {
-  red[q][cl] = s;
-  __syncthreads();
-  float t = 0.f;
-  if (q == 0)
+template <typename T, bool DQ>
+__global__ void __launch_bounds__(256) agg_gemv_part(const T* __restrict__ W, const T* __restrict__ x,
+                                                     const float* __restrict__ dU, float* __restrict__ part, int d,
+                                                     int A, int H, int dh) {
+  const int i0 = blockIdx.x * kGvRows, i1 = min(d, i0 + kGvRows);
+  for (int j = threadIdx.x; j < A; j += 256) {
+    const int h = j / dh;
+    float s = 0.f;
+    int i = i0;
+    for (; i + 8 <= i1; i += 8) {
+      float w[8], c[8];
 #pragma unroll
-    for (int k = 0; k < kGvLanes; ++k) t += red[k][cl];
-  return t;
+      for (int u = 0; u < 8; ++u) {
+        w[u] = to_f(W[(int64_t)(i + u) * A + j]);
+        c[u] = DQ ? dU[(int64_t)(i + u) * H + h] : to_f(x[i + u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += c[u] * w[u];
+    }
+    for (; i < i1; ++i) s += (DQ ? dU[(int64_t)i * H + h] : to_f(x[i])) * to_f(W[(int64_t)i * A + j]);
+    part[(int64_t)blockIdx.x * A + j] = s;
+  }
 }
 
-// q[j] = q0 . w_q[:, j] + b_q[j]   (float32 out)
+// out[j] = sum over slices of part[slice][j] (+ bias[j])
 template <typename T>
-__global__ void __launch_bounds__(1024) agg_query(const T* __restrict__ q0, const T* __restrict__ wq,
-                                                  const T* __restrict__ bq, float* __restrict__ q, int d, int A) {
-  __shared__ float red[kGvLanes][kGvCols];
-  const int cl = threadIdx.x % kGvCols, lq = threadIdx.x / kGvCols;
-  const int j = blockIdx.x * kGvCols + cl;
+__global__ void __launch_bounds__(256) agg_gemv_final(const float* __restrict__ part, int slices, int A,
+                                                      const T* __restrict__ bias, float* __restrict__ out) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= A) return;
   float s = 0.f;
-  if (j < A)
-    for (int i = lq; i < d; i += kGvLanes) s += to_f(q0[i]) * to_f(wq[(int64_t)i * A + j]);
-  const float t = gv_combine(s, red, cl, lq);
-  if (lq == 0 && j < A) q[j] = t + to_f(bq[j]);
+  int k = 0;
+  for (; k + 16 <= slices; k += 16) {
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = part[(int64_t)(k + u) * A + j];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) s += v[u];
+  }
+  for (; k < slices; ++k) s += part[(int64_t)k * A + j];
+  out[j] = bias ? s + to_f(bias[j]) : s;
 }
 
 // Ut[h][i] = sum_c w_k[i][h*dh + c] q[h*dh + c]   (one wave per (i, 8 heads))
@@ -115,23 +136,6 @@ __global__ void __launch_bounds__(256) agg_softmax_bwd(const float* __restrict__
   }
 }
 
-// dq[j] = sum_i w_k[i][j] dU[i][h(j)]
-template <typename T>
-__global__ void __launch_bounds__(1024) agg_dq(const T* __restrict__ wk, const float* __restrict__ dU,
-                                               float* __restrict__ dq, int d, int H, int dh) {
-  __shared__ float red[kGvLanes][kGvCols];
-  const int A = H * dh;
-  const int cl = threadIdx.x % kGvCols, lq = threadIdx.x / kGvCols;
-  const int j = blockIdx.x * kGvCols + cl;
-  float s = 0.f;
-  if (j < A) {
-    const int h = j / dh;
-    for (int i = lq; i < d; i += kGvLanes) s += to_f(wk[(int64_t)i * A + j]) * dU[(int64_t)i * H + h];
-  }
-  const float t = gv_combine(s, red, cl, lq);
-  if (lq == 0 && j < A) dq[j] = t;
-}
-
 // dW_k[i][j] = dU[i][h(j)] q[j];  dW_q[i][j] = q0[i] dq[j]
 template <typename T>
 __global__ void __launch_bounds__(256) agg_outer(const float* __restrict__ dU, const float* __restrict__ q,
@@ -174,16 +178,20 @@ __global__ void __launch_bounds__(256) agg_query_bwd(const T* __restrict__ wq, c
 // block per (token, 512 columns): the 2H x 512 right-hand slab is staged in LDS
 // as stored (rows contiguous) and read through transposing LDS reads; the
 // left-hand rows (2H contiguous values per variable) are MFMA fragments read
-// straight from HBM. MT = ceil(V / 32) row tiles, KS = 2H / 16 K-steps.
+// straight from HBM. MT = ceil(V / 32) row tiles, KS = 2H / 16 K-steps. Each
+// wave produces 64 columns at a time and writes them through a private LDS
+// area, so that every lane stores 16 contiguous bytes (a wave covers 8 rows x
+// 128 bytes per store).
 constexpr int kDtokCols = 512;
-
 template <int MT, int KS>
 __global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, const bf16* __restrict__ dxbar,
                                                 const bf16* __restrict__ Ut, bf16* __restrict__ dtok, int V, int d,
                                                 int H) {
   using Stage = GemmStageMN<kDtokCols, 16 * KS, 256>;
   constexpr int P = Stage::PITCH;
+  constexpr int EP = 64 + 4;  // staging pitch (floats)
   __shared__ __attribute__((aligned(16))) bf16 Bs[16 * KS * P];
+  __shared__ __attribute__((aligned(16))) float ew_all[4][32 * EP];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
   const int64_t t = blockIdx.y;
   const int c0 = blockIdx.x * kDtokCols;
@@ -211,35 +219,71 @@ __global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, con
   }
   __syncthreads();
   bf16* out = dtok + t * V * d;
+  float* ew = ew_all[wave];
 #pragma unroll 1
-  for (int j = 0; j < kDtokCols / 128; ++j) {
-    const int n0 = wave * (kDtokCols / 4) + j * 32;
-    f32x16 acc[MT];
+  for (int j = 0; j < kDtokCols / 256; ++j) {
+    const int n0 = wave * (kDtokCols / 4) + j * 64;
+    f32x16 acc[MT][2];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[mt][i] = 0.f;
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[mt][h][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      Frag<bf16> bfr;
-      Stage::frag(bfr, Bs, n0, ks, lane);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) mma16(acc[mt], af[mt][ks], bfr);
+      for (int h = 0; h < 2; ++h) {
+        Frag<bf16> bfr;
+        Stage::frag(bfr, Bs, n0 + h * 32, ks, lane);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) mma16(acc[mt][h], af[mt][ks], bfr);
+      }
     }
-    const int col = c0 + n0 + (lane & 31);
-    if (col < d) {
+    const int cl = (lane & 7) * 8;  // read-back: 8 lanes per row, 8 rows per pass
+    const int col = c0 + n0 + cl;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int v = mt * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
-          if (v < V) out[(int64_t)v * d + col] = (bf16)acc[mt][i];
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          ew[((i >> 2) * 8 + g * 4 + (i & 3)) * EP + h * 32 + (lane & 31)] = acc[mt][h][i];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {
+        const int r = pass * 8 + (lane >> 3);
+        const int v = mt * 32 + r;
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(ew + r * EP + cl);
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(ew + r * EP + cl + 4);
+        if (v < V && col < d) {
+          bf16x8 o;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) { o[q] = (bf16)lo[q]; o[4 + q] = (bf16)hi[q]; }
+          *reinterpret_cast<bf16x8*>(out + (int64_t)v * d + col) = o;
         }
+      }
+      __builtin_amdgcn_wave_barrier();
     }
   }
 }
 
 unsigned g1(int64_t n) { return (unsigned)std::max<int64_t>(1, cdiv(n, 256)); }
+
+// out = (weighted column sums of W, see agg_gemv_part) + bias; part holds
+// cdiv(d, kGvRows) x A floats
+template <typename T, bool DQ>
+orbit_status gemv_cols(const char* name, const void* W, const void* x, const float* dU, const void* bias, float* out,
+                       float* part, int d, int A, int H, int dh, hipStream_t s) {
+  const int slices = (int)cdiv(d, kGvRows);
+  KernelInfo k1{name, 2.0 * d * A, (double)d * A * sizeof(T)};
+  ORBIT_TRY(launch(k1, agg_gemv_part<T, DQ>, dim3((unsigned)slices), dim3(256), 0, s, static_cast<const T*>(W),
+                   static_cast<const T*>(x), dU, part, d, A, H, dh));
+  KernelInfo k2{"agg_gemv_final", 0.0, (double)slices * A * 4};
+  return launch(k2, agg_gemv_final<T>, dim3((unsigned)cdiv(A, 256)), dim3(256), 0, s, (const float*)part, slices, A,
+                static_cast<const T*>(bias), out);
+}
+size_t gemv_part_bytes(int d, int A) { return (size_t)cdiv(d, kGvRows) * A * sizeof(float); }
 
 struct Sizes {
   int64_t T;
@@ -283,9 +327,9 @@ size_t agg_saved_bytes(const orbit_agg_desc& a) {
   return u;
 }
 
-// forward workspace: S f32 [T*V, H] | ab [T, H, Vp] | gemm split-K
+// forward workspace: S f32 [T*V, H] | ab [T, H, Vp] | query partials | gemm split-K
 // backward workspace: dzh [T, A] | dxbar [T, H, d] | da f32 [T, H, V] | ac [T*V, 2H] | dU f32 [d, H]
-//                     | dq f32 [A] | colsum | gemm split-K
+//                     | dq f32 [A] | query-gradient partials | colsum | gemm split-K
 static size_t gemm_ws_max(const Sizes& z, orbit_dtype dt) {
   // split-K partials of every product of the forward and backward passes
   const int T = (int)z.T, TV = (int)(z.T * z.V);
@@ -310,6 +354,7 @@ size_t agg_workspace_bytes(const orbit_agg_desc& a) {
   Carver f(nullptr);
   f.take<float>((size_t)z.T * z.V * z.H);
   f.take<char>((size_t)z.T * z.H * z.Vp * esz(dt));
+  f.take<char>(gemv_part_bytes(z.d, z.A));
   size_t fwd = f.used();
   Carver b(nullptr);
   b.take<char>((size_t)z.T * z.A * esz(dt));
@@ -318,6 +363,7 @@ size_t agg_workspace_bytes(const orbit_agg_desc& a) {
   b.take<char>((size_t)z.T * z.V * 2 * z.H * esz(dt));
   b.take<float>((size_t)z.d * z.H);
   b.take<float>((size_t)z.A);
+  b.take<char>(gemv_part_bytes(z.d, z.A));
   b.take<char>(std::max(colsum_workspace_bytes((int)z.T, std::max(z.d, z.A)),
                         colsum_workspace_bytes(z.B, z.L * z.d)));
   size_t bwd = b.used();
@@ -332,22 +378,19 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
   Carver w(ws);
   float* S = w.take<float>((size_t)z.T * z.V * z.H);
   void* ab = w.take<char>((size_t)z.T * z.H * z.Vp * esz(dt));
+  float* gvp = w.take<float>(gemv_part_bytes(z.d, z.A) / sizeof(float));
   void* gws = w.take<char>(0);
   const size_t gws_bytes = ws_bytes - w.used();
   const int64_t TV = z.T * z.V;
 
   // 1. q = q0 W_q + b_q;  Ut[h] = W_k^h q_h
-  KernelInfo kq{"agg_query", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   KernelInfo ku{"agg_fold_key", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   if (dt == ORBIT_BF16) {
-    ORBIT_TRY(launch(kq, agg_query<bf16>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const bf16*)p.q0,
-                     (const bf16*)p.w_q,
-                     (const bf16*)p.b_q, sv.q, z.d, z.A));
+    ORBIT_TRY((gemv_cols<bf16, false>("agg_query", p.w_q, p.q0, nullptr, p.b_q, sv.q, gvp, z.d, z.A, z.H, z.dh, s)));
     ORBIT_TRY(launch(ku, agg_fold_key<bf16>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s, (const bf16*)p.w_k,
                      (const float*)sv.q, (bf16*)sv.Ut, z.d, z.H, z.dh));
   } else {
-    ORBIT_TRY(launch(kq, agg_query<float>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const float*)p.q0,
-                     (const float*)p.w_q, (const float*)p.b_q, sv.q, z.d, z.A));
+    ORBIT_TRY((gemv_cols<float, false>("agg_query", p.w_q, p.q0, nullptr, p.b_q, sv.q, gvp, z.d, z.A, z.H, z.dh, s)));
     ORBIT_TRY(launch(ku, agg_fold_key<float>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s,
                      (const float*)p.w_k, (const float*)sv.q, (float*)sv.Ut, z.d, z.H, z.dh));
   }
@@ -419,6 +462,7 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
   void* ac = w.take<char>((size_t)z.T * z.V * 2 * z.H * esz(dt));
   float* dU = w.take<float>((size_t)z.d * z.H);
   float* dq = w.take<float>((size_t)z.A);
+  float* gvp = w.take<float>(gemv_part_bytes(z.d, z.A) / sizeof(float));
   void* cws = w.take<char>(std::max(colsum_workspace_bytes((int)z.T, std::max(z.d, z.A)),
                                     colsum_workspace_bytes(z.B, z.L * z.d)));
   void* gws = w.take<char>(0);
@@ -497,22 +541,17 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
     ORBIT_TRY(gemm(g, gws, gws_bytes, s));
   }
   // query path
-  KernelInfo kdq{"agg_dq", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   KernelInfo kou{"agg_outer", 2.0 * z.d * z.A, 8.0 * z.d * z.A};
   KernelInfo kqb{"agg_query_bwd", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   if (dt == ORBIT_BF16) {
-    ORBIT_TRY(launch(kdq, agg_dq<bf16>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const bf16*)p.w_k,
-                     (const float*)dU, dq,
-                     z.d, z.H, z.dh));
+    ORBIT_TRY((gemv_cols<bf16, true>("agg_dq", p.w_k, nullptr, dU, nullptr, dq, gvp, z.d, z.A, z.H, z.dh, s)));
     ORBIT_TRY(launch(kou, agg_outer<bf16>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
                      dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const bf16*)p.q0, (const float*)dq,
                      gr.w_k, gr.w_q, z.d, z.H, z.dh, accumulate));
     ORBIT_TRY(launch(kqb, agg_query_bwd<bf16>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s, (const bf16*)p.w_q,
                      (const float*)dq, gr.q0, gr.b_q, gr.b_k, z.d, z.A, accumulate));
   } else {
-    ORBIT_TRY(launch(kdq, agg_dq<float>, dim3((unsigned)cdiv(z.A, kGvCols)), dim3(1024), 0, s, (const float*)p.w_k,
-                     (const float*)dU,
-                     dq, z.d, z.H, z.dh));
+    ORBIT_TRY((gemv_cols<float, true>("agg_dq", p.w_k, nullptr, dU, nullptr, dq, gvp, z.d, z.A, z.H, z.dh, s)));
     ORBIT_TRY(launch(kou, agg_outer<float>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
                      dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const float*)p.q0, (const float*)dq,
                      gr.w_k, gr.w_q, z.d, z.H, z.dh, accumulate));

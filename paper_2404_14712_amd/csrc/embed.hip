@@ -149,22 +149,126 @@ __global__ void __launch_bounds__(256) patch_bwd_partial(const float* __restrict
   }
 }
 
+// bf16 pixels as two MFMA operands: x ~ hi + lo with hi = bf16(x) and
+// lo = bf16(x - hi) (relative error ~2^-16, far below the bf16 output's)
+ORBIT_DEV void split_hi_lo(const float* x, Frag<bf16>& hi, Frag<bf16>& lo) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const bf16 h = (bf16)x[j];
+    hi.v[j] = h;
+    lo.v[j] = (bf16)(x[j] - (float)h);
+  }
+}
+
+// bf16 forward on MFMA: a block takes kPfTok tokens (32 per wave) of one
+// variable and kPfCols columns. Left operand: the token's 16 pixels (hi and lo
+// parts, two products); right operand: the W_pe[v] column slice staged in LDS
+// as stored and read through transposing reads. Each wave writes 64 columns
+// at a time through a private LDS area (16 contiguous bytes per lane) with the
+// bias and variable embedding added.
+constexpr int kPfCols = 512, kPfTok = 128;
+
+__global__ void __launch_bounds__(256) patch_fwd_mfma(const float* __restrict__ img, const bf16* __restrict__ w,
+                                                      const bf16* __restrict__ bias, const bf16* __restrict__ ve,
+                                                      bf16* __restrict__ tok, int V, int Hg, int Wg, int d,
+                                                      int64_t ntok) {
+  using Stage = GemmStageMN<kPfCols, 16, 256>;
+  constexpr int P = Stage::PITCH, EP = 64 + 4;
+  __shared__ __attribute__((aligned(16))) bf16 Ws[16 * P];
+  __shared__ __attribute__((aligned(16))) float ew_all[4][32 * EP];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int v = blockIdx.y, c0 = blockIdx.x * kPfCols;
+  const int64_t t0 = (int64_t)blockIdx.z * kPfTok + wave * 32;
+  const int nw = Wg / 4, L = (Hg / 4) * nw;
+  {
+    Stage st;
+    st.load(w + (int64_t)v * 16 * d, nullptr, 0, d, c0, d, 0, 16, tid);
+    st.store(Ws, tid);
+  }
+  // pixels 8g .. 8g+7 of this lane's token: image rows 2g, 2g + 1 of the patch
+  Frag<bf16> ahi, alo;
+  {
+    float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const int64_t t = t0 + (lane & 31);
+    if (t < ntok) {
+      const int b = (int)(t / L), l = (int)(t % L);
+      const int ph = l / nw, pw = l % nw;
+      const float* row = img + (((int64_t)b * V + v) * Hg + ph * 4 + 2 * g) * Wg + pw * 4;
+      const f32x4 r0 = *reinterpret_cast<const f32x4*>(row);
+      const f32x4 r1 = *reinterpret_cast<const f32x4*>(row + Wg);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { x[q] = r0[q]; x[4 + q] = r1[q]; }
+    }
+    split_hi_lo(x, ahi, alo);
+  }
+  __syncthreads();
+  float* ew = ew_all[wave];
+  const int cl = (lane & 7) * 8;
+#pragma unroll 1
+  for (int pp = 0; pp < kPfCols / 64; ++pp) {
+    const int col = c0 + pp * 64 + cl;
+    if (c0 + pp * 64 >= d) break;
+    f32x16 acc[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[h][i] = 0.f;
+      Frag<bf16> bfr;
+      Stage::frag(bfr, Ws, pp * 64 + h * 32, 0, lane);
+      mma16(acc[h], ahi, bfr);
+      mma16(acc[h], alo, bfr);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) ew[((i >> 2) * 8 + g * 4 + (i & 3)) * EP + h * 32 + (lane & 31)] = acc[h][i];
+    __builtin_amdgcn_wave_barrier();
+    float add[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (col < d) {
+      ld8f(bias + (int64_t)v * d + col, add);
+      if (ve) {
+        float e[8];
+        ld8f(ve + (int64_t)v * d + col, e);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) add[i] += e[i];
+      }
+    }
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {
+      const int r = pass * 8 + (lane >> 3);
+      const int64_t t = t0 + r;
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(ew + r * EP + cl);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(ew + r * EP + cl + 4);
+      if (t < ntok && col < d) {
+        float o[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { o[q] = lo[q] + add[q]; o[4 + q] = hi[q] + add[4 + q]; }
+        st8f(tok + (t * V + v) * d + col, o);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 // bf16: dW_pe[v] = sum_t P[t,v]^T dtok[t,v,:] on MFMA. A block takes 256
-// columns of one variable over a slice of kPbTokens tokens, 16 tokens per
-// K-step. Left operand rows: the 16 pixels, split exactly enough into bf16
-// high and low parts (two products), plus a row of ones whose product is the
-// bias gradient; right operand: the dtok rows of the step, staged in LDS as
-// stored and read through transposing reads. Partials per token slice in the
-// layout patch_bwd_final sums.
+// columns of one variable over a slice of kPbTokens tokens, kPbStep tokens per
+// stage (two 16-deep K-steps). Left operand rows: the 16 pixels (hi and lo
+// parts, two products) plus a row of ones whose product is the bias gradient;
+// the stage's pixels are gathered into LDS pixel-major. Right operand: the
+// dtok rows of the stage, staged in LDS as stored and read through
+// transposing reads. Partials per token slice in the layout patch_bwd_final
+// sums.
 constexpr int kPbCols = 256;
 constexpr int kPbTokens = 1024;
+constexpr int kPbStep = 32;
 
 __global__ void __launch_bounds__(256) patch_bwd_mfma(const float* __restrict__ img, const bf16* __restrict__ dtok,
                                                       float* __restrict__ part, int V, int Hg, int Wg, int d,
                                                       int64_t ntok) {
-  using Stage = GemmStageMN<kPbCols, 16, 256>;
-  constexpr int P = Stage::PITCH;
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][16 * P];
+  using Stage = GemmStageMN<kPbCols, kPbStep, 256>;
+  constexpr int P = Stage::PITCH, XP = kPbStep + 4;
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][kPbStep * P];
+  __shared__ __attribute__((aligned(16))) float Px[2][16 * XP];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
   const int v = blockIdx.y, c0 = blockIdx.x * kPbCols;
   const int64_t t_begin = (int64_t)blockIdx.z * kPbTokens;
@@ -179,44 +283,63 @@ __global__ void __launch_bounds__(256) patch_bwd_mfma(const float* __restrict__ 
   Stage st;
   const bf16* X = dtok + (int64_t)v * d;
   const int64_t ld = (int64_t)V * d;
+  // pixel gather: threads 0..127 take token tid % 32 and image row tid / 32 of its patch
+  f32x4 px;
+  auto gather = [&](int64_t ts) {
+    px = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int64_t t = ts + (tid & 31);
+    if (tid < 128 && t < t_end) {
+      const int b = (int)(t / L), l = (int)(t % L);
+      const int ph = l / nw, pw = l % nw;
+      px = *reinterpret_cast<const f32x4*>(img + (((int64_t)b * V + v) * Hg + ph * 4 + (tid >> 5)) * Wg + pw * 4);
+    }
+  };
+  auto put = [&](float* S) {
+    if (tid < 128) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) S[((tid >> 5) * 4 + e) * XP + (tid & 31)] = px[e];
+    }
+  };
   // token indices of the slice are below 2^31 (checked by the caller)
   st.load(X, nullptr, 0, ld, c0, d, (int)t_begin, (int)t_end, tid);
+  gather(t_begin);
   st.store(Bs[0], tid);
+  put(Px[0]);
   __syncthreads();
-  const int nsteps = (int)((t_end - t_begin + 15) / 16);
+  const int nsteps = (int)((t_end - t_begin + kPbStep - 1) / kPbStep);
   for (int it = 0; it < nsteps; ++it) {
     const int cur = it & 1;
-    const int64_t t0 = t_begin + (int64_t)it * 16;
-    if (it + 1 < nsteps) st.load(X, nullptr, 0, ld, c0, d, (int)(t0 + 16), (int)t_end, tid);
-    float hi[8], lo[8];
+    const int64_t t0 = t_begin + (int64_t)it * kPbStep;
+    if (it + 1 < nsteps) {
+      st.load(X, nullptr, 0, ld, c0, d, (int)(t0 + kPbStep), (int)t_end, tid);
+      gather(t0 + kPbStep);
+    }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int64_t t = t0 + 8 * g + j;
-      float val = 0.f, one = 0.f;
-      if (t < t_end) {
-        if (p < 16) {
-          const int b = (int)(t / L), l = (int)(t % L);
-          const int ph = l / nw, pw = l % nw;
-          val = img[(((int64_t)b * V + v) * Hg + ph * 4 + (p >> 2)) * Wg + pw * 4 + (p & 3)];
-        } else if (p == 16) {
-          one = 1.f;
-        }
+    for (int kk = 0; kk < kPbStep / 16; ++kk) {
+      float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (p < 16) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(Px[cur] + p * XP + kk * 16 + 8 * g);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(Px[cur] + p * XP + kk * 16 + 8 * g + 4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { x[q] = a[q]; x[4 + q] = b[q]; }
+      } else if (p == 16) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = t0 + kk * 16 + 8 * g + j < t_end ? 1.f : 0.f;
       }
-      const float h = (float)(bf16)val;
-      hi[j] = p == 16 ? one : h;
-      lo[j] = val - h;
-    }
-    Frag<bf16> ahi, alo;
-    frag_from(ahi, hi);
-    frag_from(alo, lo);
+      Frag<bf16> ahi, alo;
+      split_hi_lo(x, ahi, alo);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      Frag<bf16> bfr;
-      Stage::frag(bfr, Bs[cur], wave * 64 + j * 32, 0, lane);
-      mma16(acc_hi[j], ahi, bfr);
-      mma16(acc_lo[j], alo, bfr);
+      for (int j = 0; j < 2; ++j) {
+        Frag<bf16> bfr;
+        Stage::frag(bfr, Bs[cur], wave * 64 + j * 32, kk, lane);
+        mma16(acc_hi[j], ahi, bfr);
+        mma16(acc_lo[j], alo, bfr);
+      }
     }
-    if (it + 1 < nsteps) st.store(Bs[cur ^ 1], tid);
+    if (it + 1 < nsteps) {
+      st.store(Bs[cur ^ 1], tid);
+      put(Px[cur ^ 1]);
+    }
     __syncthreads();
   }
 #pragma unroll
@@ -227,7 +350,7 @@ __global__ void __launch_bounds__(256) patch_bwd_mfma(const float* __restrict__ 
       for (int i = 0; i < 16; ++i) {
         const int r = (i >> 2) * 8 + g * 4 + (i & 3);
         if (r <= 16)
-          part[(((int64_t)blockIdx.z * V + v) * 17 + r) * d + c] = acc_hi[j][i] + (r < 16 ? acc_lo[j][i] : 0.f);
+          part[(((int64_t)blockIdx.z * V + v) * 17 + r) * d + c] = acc_hi[j][i] + acc_lo[j][i];
       }
     }
   }
@@ -265,9 +388,12 @@ orbit_status patch_embed_fwd(orbit_dtype dt, const float* img, const void* w, co
   const double toks = (double)B * L * V;
   KernelInfo ki{dt == ORBIT_BF16 ? "patch_fwd_kernel<bf16>" : "patch_fwd_kernel<f32>", toks * d * 2 * kPP,
                 toks * (kPP * 4.0 + d * (dt == ORBIT_BF16 ? 2.0 : 4.0))};
-  if (dt == ORBIT_BF16)
-    return launch(ki, patch_fwd_kernel<bf16>, grid, dim3(256), 0, s, img, (const bf16*)w, (const bf16*)b,
-                  (const bf16*)ve, (bf16*)tok, V, Hg, Wg, d);
+  if (dt == ORBIT_BF16) {
+    const int64_t ntok = (int64_t)B * L;
+    KernelInfo km{"patch_fwd_mfma", toks * d * 2 * kPP * 2, toks * (kPP * 4.0 + d * 2.0)};
+    return launch(km, patch_fwd_mfma, dim3((unsigned)cdiv(d, kPfCols), V, (unsigned)cdiv(ntok, kPfTok)), dim3(256),
+                  0, s, img, (const bf16*)w, (const bf16*)b, (const bf16*)ve, (bf16*)tok, V, Hg, Wg, d, ntok);
+  }
   return launch(ki, patch_fwd_kernel<float>, grid, dim3(256), 0, s, img, (const float*)w, (const float*)b,
                 (const float*)ve, (float*)tok, V, Hg, Wg, d);
 }

@@ -766,6 +766,51 @@ size_t gemm_workspace_bytes(const Gemm& g) {
   return s > 1 ? align_up((size_t)s * g.batch * (size_t)g.M * g.N * sizeof(float)) : 0;
 }
 
+namespace {
+
+// one product on tile configuration t with the K range cut into `splits`
+// slices (when the workspace holds their float32 partials; else one slice)
+orbit_status gemm_run(const Gemm& g, const TileCfg& t, int splits, void* ws, size_t ws_bytes, hipStream_t s) {
+  GemmKArgs a{};
+  a.A = g.A; a.B = g.B; a.B2 = g.B2; a.C = g.C;
+  a.M = g.M; a.N = g.N; a.K = g.K; a.k_split = g.B2 ? g.k_split : g.K;
+  a.lda = g.lda; a.ldb = g.ldb; a.ldc = g.ldc;
+  a.sA = g.sA; a.sB = g.sB; a.sB2 = g.sB2; a.sC = g.sC;
+  a.batch = g.batch;
+  a.splits = 1;
+  a.k_per_split = g.K;
+  a.partial = nullptr;
+  if (splits > 1 && ws && ws_bytes >= (size_t)splits * g.batch * (size_t)g.M * g.N * sizeof(float)) {
+    const int bke = bke_of(g.dtype);
+    const int64_t ksteps = cdiv(g.K, bke);
+    const int per = (int)cdiv(ksteps, splits) * bke;
+    a.splits = (int)cdiv(g.K, per);
+    a.k_per_split = per;
+    a.partial = static_cast<float*>(ws);
+  }
+  if (g.K <= 0) a.k_per_split = 0;
+  {
+    auto al = [](int64_t x) { return x % 8 == 0; };
+    auto ap = [](const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+    a.vec_ok = al(g.N) && al(g.ldc) && al(g.sC) && al(g.sBias) && al(g.ldgo) && al(g.ldgi) && al(g.ldr) &&
+               al(g.sR) && ap(g.C) && ap(g.bias) && ap(g.gelu_out) && ap(g.gelu_in) && ap(g.res);
+  }
+  a.epi.alpha = g.alpha;
+  a.epi.accumulate = g.accumulate ? 1 : 0;
+  a.epi.bias = g.bias;
+  a.epi.sBias = g.sBias;
+  a.epi.gelu_out = g.gelu_out; a.epi.ldgo = g.ldgo;
+  a.epi.gelu_in = g.gelu_in; a.epi.ldgi = g.ldgi;
+  a.epi.res = g.res; a.epi.ldr = g.ldr; a.epi.sR = g.sR; a.epi.res_row_mod = g.res_row_mod;
+  if (g.dtype == ORBIT_BF16) {
+    return g.out_f32 ? run_typed<bf16, float>(g, a, t, s) : run_typed<bf16, bf16>(g, a, t, s);
+  }
+  // float operands always produce float
+  return run_typed<float, float>(g, a, t, s);
+}
+
+}  // namespace
+
 orbit_status gemm(const Gemm& g, void* ws, size_t ws_bytes, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return ORBIT_OK;
   // K-major operands are read in 16-byte chunks along K: with K % 8 != 0 the
@@ -780,47 +825,8 @@ orbit_status gemm(const Gemm& g, void* ws, size_t ws_bytes, hipStream_t s) {
     return ORBIT_E_ARG;
   }
   const TileCfg t = pick_tile(g);
-  GemmKArgs a{};
-  a.A = g.A; a.B = g.B; a.B2 = g.B2; a.C = g.C;
-  a.M = g.M; a.N = g.N; a.K = g.K; a.k_split = g.B2 ? g.k_split : g.K;
-  a.lda = g.lda; a.ldb = g.ldb; a.ldc = g.ldc;
-  a.sA = g.sA; a.sB = g.sB; a.sB2 = g.sB2; a.sC = g.sC;
-  a.batch = g.batch;
-  a.splits = 1;
-  a.k_per_split = g.K;
-  a.partial = nullptr;
   const int splits = pick_splits(g, t);
-  if (splits > 1 && ws && ws_bytes >= gemm_workspace_bytes(g)) {
-    const int bke = bke_of(g.dtype);
-    const int64_t ksteps = cdiv(g.K, bke);
-    const int per = (int)cdiv(ksteps, splits) * bke;
-    a.splits = (int)cdiv(g.K, per);
-    a.k_per_split = per;
-    a.partial = static_cast<float*>(ws);
-  }
-  if (g.K <= 0) a.k_per_split = 0;
-  {
-    auto al = [](int64_t x) { return x % 8 == 0; };
-    auto ap = [](const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
-    a.vec_ok = al(g.N) && al(g.ldc) && al(g.sC) && al(g.sBias) && al(g.ldgo) && al(g.ldgi) && al(g.ldr) &&
-               al(g.sR) && ap(g.C) && ap(g.bias) && ap(g.gelu_out) && ap(g.gelu_in) && ap(g.res) &&
-               (g.res == nullptr || g.res_row_mod == 0 || true);
-  }
-  a.epi.alpha = g.alpha;
-  a.epi.accumulate = g.accumulate ? 1 : 0;
-  a.epi.bias = g.bias;
-  a.epi.sBias = g.sBias;
-  a.epi.gelu_out = g.gelu_out; a.epi.ldgo = g.ldgo;
-  a.epi.gelu_in = g.gelu_in; a.epi.ldgi = g.ldgi;
-  a.epi.res = g.res; a.epi.ldr = g.ldr; a.epi.sR = g.sR; a.epi.res_row_mod = g.res_row_mod;
-  if (g.dtype == ORBIT_BF16) {
-    return g.out_f32 ? run_typed<bf16, float>(g, a, t, s) : run_typed<bf16, bf16>(g, a, t, s);
-  }
-  if (!g.out_f32) {
-    // float operands always produce float
-    return run_typed<float, float>(g, a, t, s);
-  }
-  return run_typed<float, float>(g, a, t, s);
+  return gemm_run(g, t, splits > 1 && ws_bytes >= gemm_workspace_bytes(g) ? splits : 1, ws, ws_bytes, s);
 }
 
 }  // namespace orbit
