@@ -573,8 +573,9 @@ ORBIT_DEV void ld_frag_tr(Frag<bf16>& f, const bf16* base, int pitch, int lane) 
   f.v = __builtin_bit_cast(bf16x8, xy);
 }
 
+// four waves per SIMD for head_dim 64 (the kernel fits in 128 VGPRs)
 template <int DH>
-__global__ void __launch_bounds__(256) attn_fwd_tr(FwdArgs a) {
+__global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) {
   using T = bf16;
   constexpr int KT = 64;
   using LK = TileLoader<T, KT, DH, 256, true>;  // K and V rows [kv][c]
