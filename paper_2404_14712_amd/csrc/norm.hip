@@ -86,6 +86,106 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const T* __restrict__ x, in
   }
 }
 
+// Rows of up to 4096 elements: one wave per row (4 rows per block), lane l
+// taking the 16-byte chunks l, l + 64, ...; statistics by wave reductions.
+template <typename T, int PER>
+__global__ void __launch_bounds__(256) ln_fwd_wave(const T* __restrict__ x, int64_t ldx, const T* __restrict__ g,
+                                                   const T* __restrict__ b, T* __restrict__ y, int64_t ldy,
+                                                   float* mean, float* rstd, int rows, int n, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const T* xr = x + row * ldx;
+  float v[PER][8];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < PER; ++c) {
+    const int idx = (lane + c * 64) * 8;
+    if (idx < n) {
+      load8(xr + idx, v[c]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[c][i];
+    }
+  }
+  const float mu = wave_sum(s) / (float)n;
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < PER; ++c)
+    if ((lane + c * 64) * 8 < n)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float t = v[c][i] - mu;
+        q += t * t;
+      }
+  const float r = rsqrtf(wave_sum(q) / (float)n + eps);
+  T* yr = y + row * ldy;
+#pragma unroll
+  for (int c = 0; c < PER; ++c) {
+    const int idx = (lane + c * 64) * 8;
+    if (idx < n) {
+      float gg[8], bb[8], o[8];
+      load8(g + idx, gg);
+      load8(b + idx, bb);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = (v[c][i] - mu) * r * gg[i] + bb[i];
+      store8(yr + idx, o);
+    }
+  }
+  if (lane == 0) {
+    if (mean) mean[row] = mu;
+    if (rstd) rstd[row] = r;
+  }
+}
+
+template <typename T, int PER>
+__global__ void __launch_bounds__(256) ln_bwd_wave(const T* __restrict__ dy, int64_t lddy, const T* __restrict__ x,
+                                                   int64_t ldx, const float* __restrict__ mean,
+                                                   const float* __restrict__ rstd, const T* __restrict__ g,
+                                                   const T* dres, T* dx, int64_t lddx, int rows, int n) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float mu = mean[row], r = rstd[row];
+  float gh[PER][8], xh[PER][8];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int c = 0; c < PER; ++c) {
+    const int idx = (lane + c * 64) * 8;
+    if (idx < n) {
+      float d8[8], x8[8], g8[8];
+      load8(dy + row * lddy + idx, d8);
+      load8(x + row * ldx + idx, x8);
+      load8(g + idx, g8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        xh[c][i] = (x8[i] - mu) * r;
+        gh[c][i] = d8[i] * g8[i];
+        s1 += gh[c][i];
+        s2 += gh[c][i] * xh[c][i];
+      }
+    }
+  }
+  const float inv_n = 1.f / (float)n;
+  const float m1 = wave_sum(s1) * inv_n;
+  const float m2 = wave_sum(s2) * inv_n;
+#pragma unroll
+  for (int c = 0; c < PER; ++c) {
+    const int idx = (lane + c * 64) * 8;
+    if (idx < n) {
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = r * (gh[c][i] - m1 - xh[c][i] * m2);
+      if (dres) {
+        float rr[8];
+        load8(dres + row * lddx + idx, rr);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] += rr[i];
+      }
+      store8(dx + row * lddx + idx, o);
+    }
+  }
+}
+
 template <typename T, int NCH>
 __global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, int64_t lddy,
                                                      const T* __restrict__ x, int64_t ldx,
@@ -331,49 +431,64 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
   load8(qg + li * 8, gq);
   load8(kg + li * 8, gk);
   const int64_t nrows = (int64_t)T_ * 2 * H;
-  // every row group of every block runs the same number of iterations (shuffles)
+  // every row group of every block runs the same number of iterations
+  // (shuffles); each iteration takes kQkRows rows, loads first
+  constexpr int kQkRows = 4;
   const int64_t stride = (int64_t)gridDim.x * NG;
-  const int64_t iters = (nrows + stride - 1) / stride;
+  const int64_t iters = (nrows + stride * kQkRows - 1) / (stride * kQkRows);
   for (int64_t it = 0; it < iters; ++it) {
-    const int64_t row = it * stride + (int64_t)blockIdx.x * NG + grp;
-    const bool valid = row < nrows;
-    const int64_t t = valid ? row / (2 * H) : 0;
-    const int j = valid ? (int)(row % (2 * H)) : 0;
-    const int sidx = j / H, h = j % H;
-    const int64_t off_d = t * ldd + sidx * A + h * DH + li * 8;
-    const int64_t off_s = t * lds + sidx * A + h * DH + li * 8;
-    float dy[8], xv[8], xh[8], gh[8];
-    if (valid) {
-      load8(d + off_d, dy);
-      load8(src + off_s, xv);
-    } else {
+    float dy[kQkRows][8], xv[kQkRows][8];
+    int64_t off_d[kQkRows];
+    int sidx[kQkRows];
+    bool valid[kQkRows];
+    float mu[kQkRows], r[kQkRows];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) dy[i] = xv[i] = 0.f;
+    for (int u = 0; u < kQkRows; ++u) {
+      const int64_t row = (it * kQkRows + u) * stride + (int64_t)blockIdx.x * NG + grp;
+      valid[u] = row < nrows;
+      const int64_t t = valid[u] ? row / (2 * H) : 0;
+      const int j = valid[u] ? (int)(row % (2 * H)) : 0;
+      sidx[u] = j / H;
+      const int h = j % H;
+      off_d[u] = t * ldd + sidx[u] * A + h * DH + li * 8;
+      const int64_t off_s = t * lds + sidx[u] * A + h * DH + li * 8;
+      if (valid[u]) {
+        load8(d + off_d[u], dy[u]);
+        load8(src + off_s, xv[u]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) dy[u][i] = xv[u][i] = 0.f;
+      }
+      mu[u] = valid[u] ? mean[row] : 0.f;
+      r[u] = valid[u] ? rstd[row] : 0.f;
     }
-    const float mu = valid ? mean[row] : 0.f, r = valid ? rstd[row] : 0.f;
-    float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      xh[i] = (xv[i] - mu) * r;
-      gh[i] = dy[i] * (sidx ? gk[i] : gq[i]);
-      s1 += gh[i];
-      s2 += gh[i] * xh[i];
-    }
-#pragma unroll
-    for (int o = G / 2; o >= 1; o >>= 1) {
-      s1 += __shfl_xor(s1, o, 64);
-      s2 += __shfl_xor(s2, o, 64);
-    }
-    if (valid) {
-      const float m1 = s1 / (float)DH, m2 = s2 / (float)DH;
-      float o8[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o8[i] = r * (gh[i] - m1 - xh[i] * m2);
-      store8(d + off_d, o8);
+    for (int u = 0; u < kQkRows; ++u) {
+      float xh[8], gh[8];
+      float s1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        if (sidx) { ag[1][i] += dy[i] * xh[i]; ab[1][i] += dy[i]; }
-        else      { ag[0][i] += dy[i] * xh[i]; ab[0][i] += dy[i]; }
+        xh[i] = (xv[u][i] - mu[u]) * r[u];
+        gh[i] = dy[u][i] * (sidx[u] ? gk[i] : gq[i]);
+        s1 += gh[i];
+        s2 += gh[i] * xh[i];
+      }
+#pragma unroll
+      for (int o = G / 2; o >= 1; o >>= 1) {
+        s1 += __shfl_xor(s1, o, 64);
+        s2 += __shfl_xor(s2, o, 64);
+      }
+      if (valid[u]) {
+        const float m1 = s1 / (float)DH, m2 = s2 / (float)DH;
+        float o8[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o8[i] = r[u] * (gh[i] - m1 - xh[i] * m2);
+        store8(d + off_d[u], o8);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if (sidx[u]) { ag[1][i] += dy[u][i] * xh[i]; ab[1][i] += dy[u][i]; }
+          else         { ag[0][i] += dy[u][i] * xh[i]; ab[0][i] += dy[u][i]; }
+        }
       }
     }
   }
@@ -433,6 +548,16 @@ orbit_status ln_bwd_t(const void* dy, int64_t lddy, const void* x, int64_t ldx, 
 template <typename T>
 orbit_status ln_fwd_dispatch(const void* x, int64_t ldx, const void* g, const void* b, void* y, int64_t ldy,
                              float* mean, float* rstd, int rows, int n, float eps, hipStream_t s) {
+  if (n <= 4096) {
+    KernelInfo ki{sizeof(T) == 2 ? "ln_fwd_wave<bf16>" : "ln_fwd_wave<f32>", 8.0 * rows * n,
+                  2.0 * rows * n * sizeof(T)};
+    const int per = (int)cdiv(n, 512);
+    const dim3 grid((unsigned)cdiv(rows, 4));
+#define LNF(P) if (per <= P) return launch(ki, ln_fwd_wave<T, P>, grid, dim3(256), 0, s, (const T*)x, ldx, (const T*)g, \
+                                           (const T*)b, (T*)y, ldy, mean, rstd, rows, n, eps)
+    LNF(1); LNF(2); LNF(4); LNF(8);
+#undef LNF
+  }
   const int nch = (int)cdiv(n, 2048);
   if (nch <= 1) return ln_fwd_t<T, 1>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
   if (nch <= 2) return ln_fwd_t<T, 2>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
@@ -446,6 +571,16 @@ template <typename T>
 orbit_status ln_bwd_dispatch(const void* dy, int64_t lddy, const void* x, int64_t ldx, const float* mean,
                              const float* rstd, const void* g, const void* dres, void* dx, int64_t lddx,
                              int rows, int n, hipStream_t s) {
+  if (n <= 4096) {
+    KernelInfo ki{sizeof(T) == 2 ? "ln_bwd_wave<bf16>" : "ln_bwd_wave<f32>", 12.0 * rows * n,
+                  (dres ? 4.0 : 3.0) * rows * n * sizeof(T)};
+    const int per = (int)cdiv(n, 512);
+    const dim3 grid((unsigned)cdiv(rows, 4));
+#define LNB(P) if (per <= P) return launch(ki, ln_bwd_wave<T, P>, grid, dim3(256), 0, s, (const T*)dy, lddy, (const T*)x, \
+                                           ldx, mean, rstd, (const T*)g, (const T*)dres, (T*)dx, lddx, rows, n)
+    LNB(1); LNB(2); LNB(4); LNB(8);
+#undef LNB
+  }
   const int nch = (int)cdiv(n, 2048);
   if (nch <= 1) return ln_bwd_t<T, 1>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
   if (nch <= 2) return ln_bwd_t<T, 2>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
