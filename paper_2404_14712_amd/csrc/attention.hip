@@ -573,13 +573,75 @@ ORBIT_DEV void ld_frag_tr(Frag<bf16>& f, const bf16* base, int pitch, int lane) 
   f.v = __builtin_bit_cast(bf16x8, xy);
 }
 
+// ROWS consecutive rows of one head's DH-column slice of a bf16 [L][ld]
+// matrix, copied global -> registers -> LDS ([row][DH + 8]). The loads go
+// through a buffer resource whose extent ends with row L - 1, so rows at or
+// past L read as zeros without a branch; a tile's position is a scalar byte
+// offset, so advancing costs no vector instructions.
+template <int ROWS, int DH>
+struct RowTile {
+  static constexpr int CPR = DH / 8;  // 16-byte chunks per row
+  static constexpr int NCH = ROWS * CPR;
+  static constexpr int PER = (NCH + 255) / 256;  // chunks per thread
+  static constexpr int PITCH = DH + 8;
+  static_assert(NCH % 256 == 0 || NCH % 64 == 0, "whole waves per chunk round");
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __amdgpu_buffer_rsrc_t rsrc;
+  unsigned row_bytes;
+  int tid_;
+  unsigned voff[PER];
+  unsigned lofs[PER];
+  u32x4 r[PER];
+  ORBIT_DEV void init(const bf16* base, int64_t ld, int L, int tid) {
+    row_bytes = (unsigned)(ld * 2);
+    tid_ = tid;
+    const int extent = (int)(((int64_t)(L - 1) * ld + DH) * 2);
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base), 0, extent, 0x00020000);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * 256, row = c / CPR, col = c % CPR;
+      voff[i] = (unsigned)row * row_bytes + col * 16;
+      lofs[i] = (unsigned)(row * PITCH + col * 8);
+    }
+  }
+  ORBIT_DEV void load(int row0) {
+    const unsigned so = (unsigned)row0 * row_bytes;
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (NCH % 256 == 0 || tid_ + i * 256 < NCH) r[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff[i], so, 0);
+  }
+  ORBIT_DEV void store(bf16* S) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (NCH % 256 == 0 || tid_ + i * 256 < NCH) *reinterpret_cast<u32x4*>(S + lofs[i]) = r[i];
+  }
+};
+
+// sum of the 8 values of a bf16 fragment added to acc (two per instruction)
+ORBIT_DEV float frag_sum(const Frag<bf16>& f, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bf16x2 pr = {f.v[2 * j], f.v[2 * j + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+  }
+  return acc;
+}
+
+// Softmax reference point: scores are exponentiated as exp2(s - m) with m a
+// running maximum that is raised only when a new score exceeds it by more than
+// this margin (log2 units), so the output is rescaled rarely; the unnormalised
+// probabilities stay below 2^margin.
+constexpr float kMaxSlack = 8.f;
+
 // four waves per SIMD for head_dim 64 (the kernel fits in 128 VGPRs)
 template <int DH>
 __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) {
   using T = bf16;
   constexpr int KT = 64;
-  using LK = TileLoader<T, KT, DH, 256, true>;  // K and V rows [kv][c]
-  constexpr int KP = LK::PITCH;
+  using TL = RowTile<KT, DH>;  // K and V rows [kv][c]
+  constexpr int KP = TL::PITCH;
   __shared__ __attribute__((aligned(16))) T ks[2][KT * KP];
   __shared__ __attribute__((aligned(16))) T vs[2][KT * KP];
 
@@ -608,20 +670,21 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
     for (int v = 0; v < 16; ++v) o[c][v] = 0.f;
   float m = -INFINITY, lsum = 0.f;
 
-  LK lk, lv;
+  TL tk, tv;
+  tk.init(K, a.ldk, L, tid);
+  tv.init(V, a.ldv, L, tid);
   const int nt = (L + KT - 1) / KT;
-  lk.load(K, nullptr, 0, a.ldk, 0, L, 0, DH, tid);
-  lv.load(V, nullptr, 0, a.ldv, 0, L, 0, DH, tid);
-  lk.store(ks[0], tid);
-  lv.store(vs[0], tid);
+  tk.load(0);
+  tv.load(0);
+  tk.store(ks[0]);
+  tv.store(vs[0]);
   __syncthreads();
 
   auto tile = [&](int jt, auto mask) {
     const int cur = jt & 1;
     if (jt + 1 < nt) {
-      const int j1 = (jt + 1) * KT;
-      lk.load(K, nullptr, 0, a.ldk, j1, L, 0, DH, tid);
-      lv.load(V, nullptr, 0, a.ldv, j1, L, 0, DH, tid);
+      tk.load((jt + 1) * KT);
+      tv.load((jt + 1) * KT);
     }
     const T* Ks = ks[cur];
     const T* Vs = vs[cur];
@@ -650,9 +713,9 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, s[mt][v]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float mnew = fmaxf(m, mloc * a.sl2);
-    if (__ballot(mnew > m) != 0) {
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * a.sl2;
+    if (__ballot(mloc > m + kMaxSlack) != 0) {
+      const float mnew = fmaxf(m, mloc);
       const float alpha = __builtin_amdgcn_exp2f(m - mnew);
       lsum *= alpha;
 #pragma unroll
@@ -664,16 +727,14 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -m));
-        s[mt][v] = p;
-        lsum += p;
-      }
-    // O^T[c][q] += V^T[c][kv] P^T[kv][q]
+      for (int v = 0; v < 16; ++v) s[mt][v] = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -m));
+    // O^T[c][q] += V^T[c][kv] P^T[kv][q]; the row sums come from the same
+    // bf16 probabilities that enter the product
 #pragma unroll
     for (int kk = 0; kk < KT / 16; ++kk) {
       Frag<T> pf;
       acc_frag(pf, s[kk >> 1], (kk & 1) * 8);
+      lsum = frag_sum(pf, lsum);
 #pragma unroll
       for (int c = 0; c < DH / 32; ++c) {
         Frag<T> vf;
@@ -682,8 +743,8 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
       }
     }
     if (jt + 1 < nt) {
-      lk.store(ks[cur ^ 1], tid);
-      lv.store(vs[cur ^ 1], tid);
+      tk.store(ks[cur ^ 1]);
+      tv.store(vs[cur ^ 1]);
     }
     __syncthreads();
   };
@@ -727,8 +788,8 @@ template <int DH>
 __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
   using T = bf16;
   constexpr int QT = 32;
-  using LQ = TileLoader<T, QT, DH, 256, true>;  // Q and dO rows [q][c]
-  constexpr int RP = LQ::PITCH;
+  using TL = RowTile<QT, DH>;  // Q and dO rows [q][c]
+  constexpr int RP = TL::PITCH;
   __shared__ __attribute__((aligned(16))) T qs[2][QT * RP];
   __shared__ __attribute__((aligned(16))) T os[2][QT * RP];
   __shared__ float lse_s[2][QT], d_s[2][QT];
@@ -766,12 +827,14 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
     for (int v = 0; v < 16; ++v) dvt[c][v] = dkt[c][v] = 0.f;
 
   float cs = 0.f, csr = 0.f;
-  LQ lq, lo;
+  TL tq, to;
+  tq.init(Q, a.ldq, L, tid);
+  to.init(dO, a.lddo, L, tid);
   const int nq = (L + QT - 1) / QT;
-  lq.load(Q, nullptr, 0, a.ldq, 0, L, 0, DH, tid);
-  lo.load(dO, nullptr, 0, a.lddo, 0, L, 0, DH, tid);
-  lq.store(qs[0], tid);
-  lo.store(os[0], tid);
+  tq.load(0);
+  to.load(0);
+  tq.store(qs[0]);
+  to.store(os[0]);
   if (tid < QT) {
     lse_s[0][tid] = tid < L ? lse[tid] * kLog2e : INFINITY;
     d_s[0][tid] = tid < L ? Dv[tid] : 0.f;
@@ -782,8 +845,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
     float lse_n = 0.f, d_n = 0.f;
     if (it + 1 < nq) {
       const int q1 = (it + 1) * QT;
-      lq.load(Q, nullptr, 0, a.ldq, q1, L, 0, DH, tid);
-      lo.load(dO, nullptr, 0, a.lddo, q1, L, 0, DH, tid);
+      tq.load(q1);
+      to.load(q1);
       if (tid < QT) {
         lse_n = q1 + tid < L ? lse[q1 + tid] * kLog2e : INFINITY;
         d_n = q1 + tid < L ? Dv[q1 + tid] : 0.f;
@@ -816,8 +879,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
       Frag<T> pf, sf;
       acc_frag(pf, s, kk * 8);
       acc_frag(sf, dp, kk * 8);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) csr += (float)sf.v[j];
+      csr = frag_sum(sf, csr);
 #pragma unroll
       for (int c = 0; c < DH / 32; ++c) {
         Frag<T> af;
@@ -828,8 +890,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
       }
     }
     if (it + 1 < nq) {
-      lq.store(qs[cur ^ 1], tid);
-      lo.store(os[cur ^ 1], tid);
+      tq.store(qs[cur ^ 1]);
+      to.store(os[cur ^ 1]);
       if (tid < QT) {
         lse_s[cur ^ 1][tid] = lse_n;
         d_s[cur ^ 1][tid] = d_n;
@@ -866,8 +928,8 @@ template <int DH>
 __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
   using T = bf16;
   constexpr int KT = 64;
-  using LK = TileLoader<T, KT, DH, 256, true>;  // K and V rows [kv][c]
-  constexpr int KP = LK::PITCH;
+  using TL = RowTile<KT, DH>;  // K and V rows [kv][c]
+  constexpr int KP = TL::PITCH;
   __shared__ __attribute__((aligned(16))) T ks[2][KT * KP];
   __shared__ __attribute__((aligned(16))) T vs[2][KT * KP];
   __shared__ float kbar[DH];
@@ -905,20 +967,21 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
     for (int v = 0; v < 16; ++v) dqt[c][v] = 0.f;
   float rs = 0.f;
 
-  LK lk, lv;
+  TL tk, tv;
+  tk.init(K, a.ldk, L, tid);
+  tv.init(V, a.ldv, L, tid);
   const int nt = (L + KT - 1) / KT;
-  lk.load(K, nullptr, 0, a.ldk, 0, L, 0, DH, tid);
-  lv.load(V, nullptr, 0, a.ldv, 0, L, 0, DH, tid);
-  lk.store(ks[0], tid);
-  lv.store(vs[0], tid);
+  tk.load(0);
+  tv.load(0);
+  tk.store(ks[0]);
+  tv.store(vs[0]);
   __syncthreads();
 
   auto tile = [&](int jt, auto mask) {
     const int cur = jt & 1;
     if (jt + 1 < nt) {
-      const int j1 = (jt + 1) * KT;
-      lk.load(K, nullptr, 0, a.ldk, j1, L, 0, DH, tid);
-      lv.load(V, nullptr, 0, a.ldv, j1, L, 0, DH, tid);
+      tk.load((jt + 1) * KT);
+      tv.load((jt + 1) * KT);
     }
     const T* Ks = ks[cur];
     const T* Vs = vs[cur];
@@ -952,8 +1015,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
     for (int kk = 0; kk < KT / 16; ++kk) {
       Frag<T> sf;
       acc_frag(sf, dp[kk >> 1], (kk & 1) * 8);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) rs += (float)sf.v[j];
+      rs = frag_sum(sf, rs);
 #pragma unroll
       for (int c = 0; c < DH / 32; ++c) {
         Frag<T> af;
@@ -962,8 +1024,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
       }
     }
     if (jt + 1 < nt) {
-      lk.store(ks[cur ^ 1], tid);
-      lv.store(vs[cur ^ 1], tid);
+      tk.store(ks[cur ^ 1]);
+      tv.store(vs[cur ^ 1]);
     }
     __syncthreads();
   };
