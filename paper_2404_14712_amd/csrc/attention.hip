@@ -583,7 +583,9 @@ struct RowTile {
   static constexpr int CPR = DH / 8;  // 16-byte chunks per row
   static constexpr int NCH = ROWS * CPR;
   static constexpr int PER = (NCH + 255) / 256;  // chunks per thread
-  static constexpr int PITCH = DH + 8;
+  // row pitch (elements): 16-byte fragment reads of 16 consecutive rows and
+  // transposing reads of 4 k-rows x 64 bytes both hit 64 distinct banks
+  static constexpr int PITCH = DH == 128 ? DH + 24 : DH + 8;
   static_assert(NCH % 256 == 0 || NCH % 64 == 0, "whole waves per chunk round");
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
   __amdgpu_buffer_rsrc_t rsrc;
@@ -785,13 +787,17 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
 // float32, which equals the centred form sum_i bf16(dS_ij) (q_i - qbar) +
 // qbar sum_i dS_ij.
 template <int DH>
-__global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
+__global__ void __launch_bounds__(256, DH == 128 ? 2 : 1) attn_bwd_dkdv_tr(BwdArgs a) {
   using T = bf16;
   constexpr int QT = 32;
   using TL = RowTile<QT, DH>;  // Q and dO rows [q][c]
   constexpr int RP = TL::PITCH;
+  // head_dim 128: the block's V rows stay in LDS rather than in registers,
+  // which brings the kernel within the register budget of two waves per SIMD
+  constexpr bool VLDS = DH == 128;
   __shared__ __attribute__((aligned(16))) T qs[2][QT * RP];
   __shared__ __attribute__((aligned(16))) T os[2][QT * RP];
+  __shared__ __attribute__((aligned(16))) T vsh[VLDS ? 128 * RP : 8];
   __shared__ float lse_s[2][QT], d_s[2][QT];
   __shared__ float qbar[DH];
 
@@ -808,18 +814,25 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
   const float* Dv = a.D + ((int64_t)b * a.H + h) * L;
 
   const int kv = blockIdx.x * 128 + wave * 32 + (lane & 31);
-  Frag<T> kf[DH / 16], vf[DH / 16];
+  Frag<T> kf[DH / 16], vf[VLDS ? 1 : DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
     if (kv < L) {
       ld_frag(kf[kk], K + (int64_t)kv * a.ldk + kk * 16 + g * 8);
-      ld_frag(vf[kk], V + (int64_t)kv * a.ldv + kk * 16 + g * 8);
+      if constexpr (!VLDS) ld_frag(vf[kk], V + (int64_t)kv * a.ldv + kk * 16 + g * 8);
     } else {
       float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
       frag_from(kf[kk], z);
-      frag_from(vf[kk], z);
+      if constexpr (!VLDS) frag_from(vf[kk], z);
     }
   }
+  if constexpr (VLDS) {
+    RowTile<128, DH> tvb;
+    tvb.init(V, a.ldv, L, tid);
+    tvb.load(blockIdx.x * 128);
+    tvb.store(vsh);
+  }
+  const T* vrow = vsh + (wave * 32 + (lane & 31)) * RP + g * 8;
   f32x16 dvt[DH / 32], dkt[DH / 32];
 #pragma unroll
   for (int c = 0; c < DH / 32; ++c)
@@ -863,7 +876,13 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_tr(BwdArgs a) {
       ld_frag(af, Qs + (lane & 31) * RP + kk * 16 + g * 8);
       mma16(s, af, kf[kk]);
       ld_frag(af, Os + (lane & 31) * RP + kk * 16 + g * 8);
-      mma16(dp, af, vf[kk]);
+      if constexpr (VLDS) {
+        Frag<T> vk;
+        ld_frag(vk, vrow + kk * 16);
+        mma16(dp, af, vk);
+      } else {
+        mma16(dp, af, vf[kk]);
+      }
     }
     // rows: query 8*(v/4) + 4g + v%4 of the tile; column: this lane's key
 #pragma unroll
