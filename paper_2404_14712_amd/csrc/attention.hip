@@ -787,14 +787,15 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
 // float32, which equals the centred form sum_i bf16(dS_ij) (q_i - qbar) +
 // qbar sum_i dS_ij.
 template <int DH>
-__global__ void __launch_bounds__(256, DH == 128 ? 2 : 1) attn_bwd_dkdv_tr(BwdArgs a) {
+__global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? 3 : 1) attn_bwd_dkdv_tr(BwdArgs a) {
   using T = bf16;
   constexpr int QT = 32;
   using TL = RowTile<QT, DH>;  // Q and dO rows [q][c]
   constexpr int RP = TL::PITCH;
-  // head_dim 128: the block's V rows stay in LDS rather than in registers,
-  // which brings the kernel within the register budget of two waves per SIMD
-  constexpr bool VLDS = DH == 128;
+  // the block's V rows stay in LDS rather than in registers, which brings the
+  // kernel within the register budget of three waves per SIMD at head_dim 64
+  // and two at head_dim 128
+  constexpr bool VLDS = DH >= 64;
   __shared__ __attribute__((aligned(16))) T qs[2][QT * RP];
   __shared__ __attribute__((aligned(16))) T os[2][QT * RP];
   __shared__ __attribute__((aligned(16))) T vsh[VLDS ? 128 * RP : 8];
