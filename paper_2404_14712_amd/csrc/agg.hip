@@ -113,6 +113,59 @@ __global__ void __launch_bounds__(256) agg_softmax(const float* __restrict__ S, 
   }
 }
 
+// xbar[t][h][c] = sum_v a[t][h][v] x[t][v][c] (bf16) as one streaming pass over
+// the token tensor: a wave per (token, 512 columns), 8 columns per lane read as
+// 16-byte row segments (a wave reads 1 KB of a row per load); two variables
+// per step, interleaved into bf16 pairs and multiplied by the head's weight
+// pair (wave-uniform, a scalar operand) with dot2, float32 accumulation in v
+// order. ab is zero-padded to an even count, so an odd last variable pairs
+// with a zero weight.
+template <int H>
+__global__ void __launch_bounds__(256) agg_xbar(const bf16* __restrict__ ab, const bf16* __restrict__ tok,
+                                                bf16* __restrict__ xbar, int64_t T_, int V, int Vp, int d) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63;
+  const int nch = (d + 511) / 512;
+  const int item = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 4 + (int)(threadIdx.x >> 6));
+  if ((int64_t)item >= T_ * nch) return;
+  const int t = __builtin_amdgcn_readfirstlane(item / nch);
+  const int c0 = (item - t * nch) * 512 + lane * 8;
+  // the token's V rows as one buffer: loads past the last row read zeros
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16*>(tok + (int64_t)t * V * d), 0, V * d * 2, 0x00020000);
+  const unsigned* A = reinterpret_cast<const unsigned*>(ab + (int64_t)t * H * Vp);
+  const int hp = Vp / 2;
+  const unsigned voff = (unsigned)c0 * 2;
+  const unsigned row = (unsigned)d * 2;
+  float acc[H][8];
+#pragma unroll
+  for (int h = 0; h < H; ++h)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[h][j] = 0.f;
+#pragma unroll 2
+  for (int v = 0; v < V; v += 2) {
+    const u32x4 x0 = __builtin_amdgcn_raw_buffer_load_b128(rx, voff, (unsigned)v * row, 0);
+    const u32x4 x1 = __builtin_amdgcn_raw_buffer_load_b128(rx, voff, (unsigned)(v + 1) * row, 0);
+    unsigned p[8];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      p[2 * w] = __builtin_amdgcn_perm(x1[w], x0[w], 0x05040100u);
+      p[2 * w + 1] = __builtin_amdgcn_perm(x1[w], x0[w], 0x07060302u);
+    }
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const bf16x2 a2 = __builtin_bit_cast(bf16x2, A[h * hp + v / 2]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[h][j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p[j]), a2, acc[h][j], false);
+    }
+  }
+  if (c0 >= d) return;
+#pragma unroll
+  for (int h = 0; h < H; ++h) st128(xbar + ((int64_t)t * H + h) * d + c0, pack(acc[h], (bf16*)nullptr));
+}
+
 // softmax backward per (t, h): ds = a (da - sum a da) * scale.
 // ac[(t*V + v)*2H + h] = a, ac[(t*V + v)*2H + H + h] = ds   (dtype); one wave per
 // token, lanes as in agg_softmax
@@ -414,7 +467,18 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
     ORBIT_TRY(launch(ks, agg_softmax<float>, dim3((unsigned)cdiv(z.T, 4)), dim3(256), 0, s, (const float*)S, sv.a32,
                      (float*)ab, z.T, z.V, z.Vp, z.H));
   // 4. xbar_t = a_t [H, V] X_t [V, d]   (batched over tokens)
-  {
+  if (dt == ORBIT_BF16 && (z.H == 8 || z.H == 16)) {
+    const int64_t items = z.T * cdiv(z.d, 512);
+    KernelInfo kx{"agg_xbar", 2.0 * z.T * z.H * (double)z.V * z.d,
+                  (double)z.T * (z.V + z.H) * z.d * 2.0};
+    const dim3 grid((unsigned)cdiv(items, 4));
+    if (z.H == 8)
+      ORBIT_TRY(launch(kx, agg_xbar<8>, grid, dim3(256), 0, s, (const bf16*)ab, (const bf16*)tok, (bf16*)sv.xbar,
+                       z.T, z.V, z.Vp, z.d));
+    else
+      ORBIT_TRY(launch(kx, agg_xbar<16>, grid, dim3(256), 0, s, (const bf16*)ab, (const bf16*)tok, (bf16*)sv.xbar,
+                       z.T, z.V, z.Vp, z.d));
+  } else {
     Gemm g = base_gemm(dt);
     g.tag = "agg_xbar";
     g.A = ab; g.lda = z.Vp; g.a_kmajor = true; g.sA = (int64_t)z.H * z.Vp;

@@ -64,6 +64,8 @@ AGG_CASES = [
     ("bf16", 2, 33, 48, 256, 8, 32),
     ("bf16", 1, 70, 91, 512, 8, 64),      # V of the 91-variable set, A = d
     ("bf16", 1, 19, 7, 1024, 8, 64),       # column shard: A = 512 != d
+    ("bf16", 1, 24, 48, 768, 16, 32),      # 16 heads; a partial 512-column chunk
+    ("bf16", 2, 9, 91, 512, 16, 64),       # 16 heads, odd V, A = 2d
 ]
 
 
