@@ -26,10 +26,7 @@
  * Streams.    `stream` is a hipStream_t passed as void* (NULL = the null
  *             stream). Every call only enqueues work on it and returns; results
  *             are valid once the stream reaches that point. No call
- *             synchronises the device. orbit_vit_block_bwd also queues work
- *             on a second stream of the same device (created on first use,
- *             default priority), ordered after the work already on `stream`
- *             and joined back into `stream` before the call returns.
+ *             synchronises the device.
  * Gradients.  accumulate = 0 overwrites the gradient buffers, 1 adds to them.
  * Errors.     Arguments are validated before anything is enqueued; on failure
  *             the call returns ORBIT_E_ARG or ORBIT_E_UNSUPPORTED, touches no

@@ -129,14 +129,12 @@ struct BlockWs {
   float* D;    // attention backward workspace
   float *p_fc1, *p_fc2, *p_ln2, *p_proj, *p_qkv, *p_ln1;  // column-sum partials
   void* qws;
-  void* gws_w;  // GEMM workspace of the weight-gradient products (side stream)
-  size_t gws_w_bytes;
   void* gws;
   size_t gws_bytes;
 };
 
-size_t block_gemm_ws(const BlockDims& z, bool weight_grads_only) {
-  // the products of the block (forward and backward) with their shapes
+size_t block_gemm_ws(const BlockDims& z) {
+  // every product of the block (forward and backward) with its shapes
   Gemm g;
   g.dtype = z.dt;
   size_t m = 0;
@@ -147,7 +145,6 @@ size_t block_gemm_ws(const BlockDims& z, bool weight_grads_only) {
       {z.F, z.d, T, 0, 0},     {T, z.F, z.d, 1, 1}, {z.d, z.F, T, 0, 0}, {T, z.d, z.F, 1, 1},
       {z.A, z.d, T, 0, 0},     {T, z.A, z.d, 1, 1}, {z.d, 3 * z.A, T, 0, 0}, {T, z.d, 3 * z.A, 1, 1}};
   for (auto& sh : shapes) {
-    if (weight_grads_only && sh[3]) continue;
     g.M = sh[0]; g.N = sh[1]; g.K = sh[2]; g.a_kmajor = sh[3]; g.b_kmajor = sh[4];
     m = std::max(m, gemm_workspace_bytes(g));
   }
@@ -174,9 +171,7 @@ size_t block_ws_layout(const BlockDims& z, void* base, size_t bytes, BlockWs* w,
   t.p_qkv = c.take<float>(colsum_part_bytes(T, 3 * z.A, false) / sizeof(float));
   t.p_ln1 = c.take<float>(colsum_part_bytes(T, z.d, true) / sizeof(float));
   t.qws = c.take<char>(qk_norm_bwd_workspace_bytes(z.dh));
-  t.gws_w_bytes = block_gemm_ws(z, true);
-  t.gws_w = c.take<char>(t.gws_w_bytes);
-  const size_t g = block_gemm_ws(z, false);
+  const size_t g = block_gemm_ws(z);
   t.gws = c.take<char>(g);
   const size_t used = c.used();
   t.gws_bytes = base ? (bytes > used - g ? bytes - (used - g) : 0) : g;
@@ -306,27 +301,15 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
   const orbit_dtype dt = z.dt;
   const size_t e = esz(dt);
   const bool acc = accumulate != 0;
-  // The weight-gradient products run on a side stream, each started once its
-  // inputs exist on the caller's stream, and overlap the input-gradient chain;
-  // the call joins the side stream before it returns.
-  SideStream* side = nullptr;
-  ORBIT_TRY(side_stream(&side));
-  const hipStream_t sw = side->s;
-  struct Join {  // also on an early error return: nothing of the call outlives it
-    SideStream* side; hipStream_t s; bool done = false;
-    ~Join() { if (!done) (void)side->join(s); }
-  } join{side, s};
 
   // feed-forward sub-layer
-  ORBIT_TRY(side->fork(s));
   {
     Gemm g; g.dtype = dt; g.tag = "fc2_dw";
     g.A = sv.g; g.lda = z.F; g.a_kmajor = false; g.B = dy; g.ldb = z.d; g.b_kmajor = false;
     g.C = gr->w_fc2; g.ldc = z.d; g.out_f32 = true; g.accumulate = acc;
     g.M = z.F; g.N = z.d; g.K = T;
-    ORBIT_TRY(gemm(g, w.gws_w, w.gws_w_bytes, sw));
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(side->mark());  // dy has been read (dx may alias it)
   ColFinal fin;  // parameter-gradient column sums, finished together at the end
   {
     Gemm g; g.dtype = dt; g.tag = "fc2_dx";
@@ -334,13 +317,12 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.C = w.du; g.ldc = z.F; g.M = T; g.N = z.F; g.K = z.d; g.gelu_in = sv.u; g.ldgi = z.F;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(side->fork(s));
   {
     Gemm g; g.dtype = dt; g.tag = "fc1_dw";
     g.A = sv.h2; g.lda = z.d; g.a_kmajor = false; g.B = w.du; g.ldb = z.F; g.b_kmajor = false;
     g.C = gr->w_fc1; g.ldc = z.F; g.out_f32 = true; g.accumulate = acc;
     g.M = z.d; g.N = z.F; g.K = T;
-    ORBIT_TRY(gemm(g, w.gws_w, w.gws_w_bytes, sw));
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   {
     ColJob j[2];
@@ -367,13 +349,12 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     fin.add_job(j[1], T);
   }
   // attention sub-layer
-  ORBIT_TRY(side->fork(s));
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dw";
     g.A = sv.o; g.lda = z.A; g.a_kmajor = false; g.B = w.dx1; g.ldb = z.d; g.b_kmajor = false;
     g.C = gr->w_proj; g.ldc = z.d; g.out_f32 = true; g.accumulate = acc;
     g.M = z.A; g.N = z.d; g.K = T;
-    ORBIT_TRY(gemm(g, w.gws_w, w.gws_w_bytes, sw));
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dx";
@@ -403,13 +384,12 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(fill_f32(gr->kn_g, z.dh, 0.f, s));
     ORBIT_TRY(fill_f32(gr->kn_b, z.dh, 0.f, s));
   }
-  ORBIT_TRY(side->fork(s));
   {
     Gemm g; g.dtype = dt; g.tag = "qkv_dw";
     g.A = sv.h1; g.lda = z.d; g.a_kmajor = false; g.B = w.dqkv; g.ldb = 3 * z.A; g.b_kmajor = false;
     g.C = gr->w_qkv; g.ldc = 3 * z.A; g.out_f32 = true; g.accumulate = acc;
     g.M = z.d; g.N = 3 * z.A; g.K = T;
-    ORBIT_TRY(gemm(g, w.gws_w, w.gws_w_bytes, sw));
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   {
     Gemm g; g.dtype = dt; g.tag = "qkv_dx";
@@ -417,7 +397,6 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.C = w.dh; g.ldc = z.d; g.M = T; g.N = z.d; g.K = 3 * z.A;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(side->wait_mark(s));
   ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, x, z.d, sv.mu1, sv.r1, p->ln1_g, w.dx1, dx, z.d, T, z.d, s));
   {
     ColJob j[2];
@@ -428,8 +407,6 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     fin.add_job(j[0], T);
     fin.add_job(j[1], T);
   }
-  join.done = true;
-  ORBIT_TRY(side->join(s));
   return fin.run(accumulate, s);
 }
 

@@ -147,23 +147,6 @@ struct KernelInfo {
   double flops;       // algorithmic flops of this launch
   double bytes;       // algorithmic HBM bytes of this launch
 };
-// A second stream of the current device for work within one call that may
-// overlap the caller's stream. fork(): work queued on the side stream after it
-// waits for everything queued on `main` so far; join(): `main` waits for
-// everything queued on the side stream so far. A call joins before it returns,
-// so its results are complete when the caller's stream reaches them.
-// mark() / wait_mark(): `main` waits only for the side-stream work queued
-// before the last mark().
-struct SideStream {
-  hipStream_t s;
-  hipEvent_t fork_ev, join_ev, mark_ev;
-  orbit_status fork(hipStream_t main);
-  orbit_status join(hipStream_t main);
-  orbit_status mark();
-  orbit_status wait_mark(hipStream_t main);
-};
-orbit_status side_stream(SideStream** out);
-
 bool timing_on();
 void timing_begin(hipStream_t s, const KernelInfo& k);
 void timing_end(hipStream_t s);

@@ -25,71 +25,6 @@ void set_error(const char* fmt, ...) {
 void clear_error() { g_err[0] = 0; }
 
 // ---------------------------------------------------------------------------
-// side streams: one per device, default priority, created on first use
-// ---------------------------------------------------------------------------
-namespace {
-constexpr int kMaxDevices = 64;
-SideStream g_side[kMaxDevices];
-std::once_flag g_side_once[kMaxDevices];
-orbit_status g_side_status[kMaxDevices];
-}  // namespace
-
-orbit_status side_stream(SideStream** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
-    set_error("side stream: no usable current device");
-    return ORBIT_E_DEVICE;
-  }
-  std::call_once(g_side_once[dev], [dev] {
-    SideStream& x = g_side[dev];
-    g_side_status[dev] = ORBIT_OK;
-    if (hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking) != hipSuccess ||
-        hipEventCreateWithFlags(&x.fork_ev, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&x.join_ev, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&x.mark_ev, hipEventDisableTiming) != hipSuccess)
-      g_side_status[dev] = ORBIT_E_DEVICE;
-  });
-  if (g_side_status[dev] != ORBIT_OK) {
-    set_error("side stream: creating the stream or its events failed on device %d", dev);
-    return g_side_status[dev];
-  }
-  *out = &g_side[dev];
-  return ORBIT_OK;
-}
-
-orbit_status SideStream::fork(hipStream_t main) {
-  if (hipEventRecord(fork_ev, main) != hipSuccess || hipStreamWaitEvent(s, fork_ev, 0) != hipSuccess) {
-    set_error("side stream: fork failed");
-    return ORBIT_E_DEVICE;
-  }
-  return ORBIT_OK;
-}
-
-orbit_status SideStream::join(hipStream_t main) {
-  if (hipEventRecord(join_ev, s) != hipSuccess || hipStreamWaitEvent(main, join_ev, 0) != hipSuccess) {
-    set_error("side stream: join failed");
-    return ORBIT_E_DEVICE;
-  }
-  return ORBIT_OK;
-}
-
-orbit_status SideStream::mark() {
-  if (hipEventRecord(mark_ev, s) != hipSuccess) {
-    set_error("side stream: mark failed");
-    return ORBIT_E_DEVICE;
-  }
-  return ORBIT_OK;
-}
-
-orbit_status SideStream::wait_mark(hipStream_t main) {
-  if (hipStreamWaitEvent(main, mark_ev, 0) != hipSuccess) {
-    set_error("side stream: wait failed");
-    return ORBIT_E_DEVICE;
-  }
-  return ORBIT_OK;
-}
-
-// ---------------------------------------------------------------------------
 // timing
 // ---------------------------------------------------------------------------
 namespace {
