@@ -284,6 +284,41 @@ def _check_model(vp, loss, inputs, c, tol):
     print("largest errors (err, floor):", [(n, f"{e:.2e}", f"{fl:.2e}") for (e, fl), n in worst[:6]])
 
 
+def test_graph_replay_matches_eager(lib):
+    """A captured HIP graph of the whole pass (the block backward's side stream
+    included) replays bit-identically to eager launches: three replays, each
+    after eager work that overwrites every output."""
+    import torch
+    c = synth.small_config(2, B=2, L=64, grid=(32, 32), V=6, d=256, blocks=2, heads=4, head_dim=64, mlp=512,
+                           agg_heads=8, agg_head_dim=32, sigma=0.05)
+    vp, loss, inputs = _run_model(lib, c)
+    img, tgt = dev(inputs[0], "f32"), dev(inputs[1], "f32")
+
+    def outputs():
+        out = [vp.loss, vp.pred, vp.dtok]
+        for grp in ("embed", "agg", "head"):
+            out += [t for t in vp.grads[grp].values()]
+        for gb in vp.grads["blocks"]:
+            out += list(gb.values())
+        return out
+
+    ref = [t.clone() for t in outputs()]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        vp.forward_backward({"img": img, "tgt": tgt})
+    torch.cuda.synchronize()
+    for r in range(3):
+        for t in outputs():
+            t.fill_(float("nan") if t.is_floating_point() else 0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (t, e) in enumerate(zip(outputs(), ref)):
+            assert torch.equal(t, e), f"replay {r}: output {i} differs from the eager pass"
+        vp.forward_backward({"img": img, "tgt": tgt})  # eager work between replays
+        torch.cuda.synchronize()
+
+
 def test_full_model_tiny_fp32(lib):
     """The tiny configuration exactly: 2 x 4 variables on 32x64, d=128, 2 blocks, fp32."""
     c = synth.CONFIGS[1]
