@@ -652,8 +652,8 @@ struct Choice { TileCfg t; int splits; };
 Choice pick_bf16(const Gemm& g) {
   // TFLOP/s per layout; blocks per CU; fraction of the rate with one block per CU
   struct Cand { TileCfg t; double fwd, dx, dw; int slots; double eff1; };
-  const Cand cands[] = {{kDma, 1250.0, 1300.0, 1290.0, 1, 1.0},
-                        {kDmaHalf, 1070.0, 1030.0, 1140.0, 2, 0.67},
+  const Cand cands[] = {{kDma, 1250.0, 1053.0, 1290.0, 1, 1.0},
+                        {kDmaHalf, 1070.0, 1030.0, 1197.0, 2, 0.87},
                         {kT256, 1000.0, 1050.0, 960.0, 1, 1.0},
                         {kT256x128, 820.0, 830.0, 790.0, 1, 1.0},
                         {kT128x256, 800.0, 860.0, 755.0, 1, 1.0},
