@@ -232,9 +232,9 @@ __global__ void __launch_bounds__(256) agg_query_bwd(const T* __restrict__ wq, c
 // as stored (rows contiguous) and read through transposing LDS reads; the
 // left-hand rows (2H contiguous values per variable) are MFMA fragments read
 // straight from HBM. MT = ceil(V / 32) row tiles, KS = 2H / 16 K-steps. Each
-// wave produces 64 columns at a time and writes them through a private LDS
-// area, so that every lane stores 16 contiguous bytes (a wave covers 8 rows x
-// 128 bytes per store).
+// wave produces 64 columns at a time and writes them, rounded to bf16, through
+// a private LDS area, so that every lane stores 16 contiguous bytes (a wave
+// covers 8 rows x 128 bytes per store).
 constexpr int kDtokCols = 512;
 template <int MT, int KS>
 __global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, const bf16* __restrict__ dxbar,
@@ -242,9 +242,9 @@ __global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, con
                                                 int H) {
   using Stage = GemmStageMN<kDtokCols, 16 * KS, 256>;
   constexpr int P = Stage::PITCH;
-  constexpr int EP = 64 + 4;  // staging pitch (floats)
+  constexpr int EP = 64 + 8;  // staging pitch (bf16; results are rounded before staging)
   __shared__ __attribute__((aligned(16))) bf16 Bs[16 * KS * P];
-  __shared__ __attribute__((aligned(16))) float ew_all[4][32 * EP];
+  __shared__ __attribute__((aligned(16))) bf16 ew_all[4][32 * EP];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
   const int64_t t = blockIdx.y;
   const int c0 = blockIdx.x * kDtokCols;
@@ -272,7 +272,7 @@ __global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, con
   }
   __syncthreads();
   bf16* out = dtok + t * V * d;
-  float* ew = ew_all[wave];
+  bf16* ew = ew_all[wave];
 #pragma unroll 1
   for (int j = 0; j < kDtokCols / 256; ++j) {
     const int n0 = wave * (kDtokCols / 4) + j * 64;
@@ -301,20 +301,14 @@ __global__ void __launch_bounds__(256) agg_dtok(const bf16* __restrict__ ac, con
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          ew[((i >> 2) * 8 + g * 4 + (i & 3)) * EP + h * 32 + (lane & 31)] = acc[mt][h][i];
+          ew[((i >> 2) * 8 + g * 4 + (i & 3)) * EP + h * 32 + (lane & 31)] = (bf16)acc[mt][h][i];
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int pass = 0; pass < 4; ++pass) {
         const int r = pass * 8 + (lane >> 3);
         const int v = mt * 32 + r;
-        const f32x4 lo = *reinterpret_cast<const f32x4*>(ew + r * EP + cl);
-        const f32x4 hi = *reinterpret_cast<const f32x4*>(ew + r * EP + cl + 4);
-        if (v < V && col < d) {
-          bf16x8 o;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) { o[q] = (bf16)lo[q]; o[4 + q] = (bf16)hi[q]; }
-          *reinterpret_cast<bf16x8*>(out + (int64_t)v * d + col) = o;
-        }
+        const bf16x8 o = *reinterpret_cast<const bf16x8*>(ew + r * EP + cl);
+        if (v < V && col < d) *reinterpret_cast<bf16x8*>(out + (int64_t)v * d + col) = o;
       }
       __builtin_amdgcn_wave_barrier();
     }
