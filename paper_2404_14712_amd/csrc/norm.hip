@@ -375,13 +375,16 @@ __global__ void __launch_bounds__(256) qkln_fwd_kernel(const T* __restrict__ src
                                                        float eps) {
   constexpr int G = DH / 8;
   const int li = threadIdx.x % G;
-  const int64_t row = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;
-  const bool valid = row < (int64_t)T_ * 2 * H;
-  const int64_t t = valid ? row / (2 * H) : 0;
-  const int j = valid ? (int)(row % (2 * H)) : 0;
-  const int sidx = j / H, h = j % H;
+  // row (t, j): head slot j < 2H of token t (q heads, then k heads), at
+  // column j * DH of the token's [q | k] columns; rows < 2^31 (host check)
+  const unsigned row = blockIdx.x * (256u / G) + threadIdx.x / G;
+  const unsigned nr = 2u * H;
+  const bool valid = row < (unsigned)T_ * nr;
+  const unsigned t = valid ? row / nr : 0u;
+  const unsigned j = valid ? row - t * nr : 0u;
+  const int sidx = (int)j >= H;
   float v[8];
-  if (valid) load8(src + t * lds + sidx * A + h * DH + li * 8, v);
+  if (valid) load8(src + (int64_t)t * lds + j * DH + li * 8, v);
   else
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = 0.f;
@@ -403,7 +406,7 @@ __global__ void __launch_bounds__(256) qkln_fwd_kernel(const T* __restrict__ src
   load8((sidx ? kb : qb) + li * 8, bb);
 #pragma unroll
   for (int i = 0; i < 8; ++i) y[i] = (v[i] - mu) * r * gg[i] + bb[i];
-  store8(dst + t * ldd + sidx * A + h * DH + li * 8, y);
+  store8(dst + (int64_t)t * ldd + j * DH + li * 8, y);
   if (li == 0) {
     mean[row] = mu;
     rstd[row] = r;
@@ -430,13 +433,19 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
   float gq[8], gk[8];
   load8(qg + li * 8, gq);
   load8(kg + li * 8, gk);
-  const int64_t nrows = (int64_t)T_ * 2 * H;
+  // rows (t, j) as in the forward; a row group walks rows base, base +
+  // stride, ... keeping (t, j) by carries (one division at the start)
+  const unsigned nr = 2u * H;
+  const unsigned nrows = (unsigned)T_ * nr;
   // every row group of every block runs the same number of iterations
   // (shuffles); each iteration takes kQkRows rows, loads first
   constexpr int kQkRows = 4;
-  const int64_t stride = (int64_t)gridDim.x * NG;
-  const int64_t iters = (nrows + stride * kQkRows - 1) / (stride * kQkRows);
-  for (int64_t it = 0; it < iters; ++it) {
+  const unsigned stride = gridDim.x * (unsigned)NG;
+  const unsigned iters = (nrows + stride * kQkRows - 1) / (stride * kQkRows);
+  const unsigned st = stride / nr, sj = stride - st * nr;
+  unsigned row = blockIdx.x * (unsigned)NG + grp;
+  unsigned tc = row / nr, jc = row - tc * nr;
+  for (unsigned it = 0; it < iters; ++it) {
     float dy[kQkRows][8], xv[kQkRows][8];
     int64_t off_d[kQkRows];
     int sidx[kQkRows];
@@ -444,14 +453,15 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
     float mu[kQkRows], r[kQkRows];
 #pragma unroll
     for (int u = 0; u < kQkRows; ++u) {
-      const int64_t row = (it * kQkRows + u) * stride + (int64_t)blockIdx.x * NG + grp;
       valid[u] = row < nrows;
-      const int64_t t = valid[u] ? row / (2 * H) : 0;
-      const int j = valid[u] ? (int)(row % (2 * H)) : 0;
-      sidx[u] = j / H;
-      const int h = j % H;
-      off_d[u] = t * ldd + sidx[u] * A + h * DH + li * 8;
-      const int64_t off_s = t * lds + sidx[u] * A + h * DH + li * 8;
+      sidx[u] = (int)jc >= H;
+      off_d[u] = (int64_t)tc * ldd + jc * DH + li * 8;
+      const int64_t off_s = (int64_t)tc * lds + jc * DH + li * 8;
+      const unsigned rcur = row;
+      row += stride;
+      jc += sj;
+      tc += st;
+      if (jc >= nr) { jc -= nr; ++tc; }
       if (valid[u]) {
         load8(d + off_d[u], dy[u]);
         load8(src + off_s, xv[u]);
@@ -459,8 +469,8 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
 #pragma unroll
         for (int i = 0; i < 8; ++i) dy[u][i] = xv[u][i] = 0.f;
       }
-      mu[u] = valid[u] ? mean[row] : 0.f;
-      r[u] = valid[u] ? rstd[row] : 0.f;
+      mu[u] = valid[u] ? mean[rcur] : 0.f;
+      r[u] = valid[u] ? rstd[rcur] : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < kQkRows; ++u) {
@@ -743,6 +753,10 @@ orbit_status colsum_f32(const float* dy, int64_t lddy, int rows, int n, float* o
 orbit_status qk_norm_fwd(orbit_dtype dt, const void* src, int64_t lds, void* dst, int64_t ldd, const void* qg,
                          const void* qb, const void* kg, const void* kb, float* mean, float* rstd, int T_, int H,
                          int dh, float eps, hipStream_t s) {
+  if ((int64_t)T_ * 2 * H >= ((int64_t)1 << 31)) {
+    set_error("qk_norm: %d tokens x %d heads exceed 2^31 head rows", T_, H);
+    return ORBIT_E_UNSUPPORTED;
+  }
 #define QKF(TT, D) return qk_fwd_t<TT, D>(src, lds, dst, ldd, qg, qb, kg, kb, mean, rstd, T_, H, eps, s)
   if (dt == ORBIT_BF16) {
     if (dh == 32) QKF(bf16, 32);
@@ -764,6 +778,10 @@ orbit_status qk_norm_bwd(orbit_dtype dt, void* d, int64_t ldd, const void* src, 
                          const float* rstd, const void* qg, const void* kg, float* dqg, float* dqb, float* dkg,
                          float* dkb, int accumulate, int T_, int H, int dh, void* ws, ColFinal* fin,
                          hipStream_t s) {
+  if ((int64_t)T_ * 2 * H >= ((int64_t)1 << 31)) {
+    set_error("qk_norm: %d tokens x %d heads exceed 2^31 head rows", T_, H);
+    return ORBIT_E_UNSUPPORTED;
+  }
 #define QKB(TT, D) \
   return qk_bwd_t<TT, D>(d, ldd, src, lds, mean, rstd, qg, kg, dqg, dqb, dkg, dkb, accumulate, T_, H, ws, fin, s)
   if (dt == ORBIT_BF16) {
