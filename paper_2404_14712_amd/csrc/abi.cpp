@@ -67,6 +67,12 @@ orbit_status block_dims(const char* fn, const orbit_block_desc* desc, BlockDims*
   REQ(d.eps > 0.f, ORBIT_E_ARG, "%s: eps must be positive", fn);
   REQ((int64_t)d.B * d.L < (1ll << 31) && (int64_t)d.heads * d.head_dim * 3 < (1ll << 31), ORBIT_E_UNSUPPORTED,
       "%s: sizes too large", fn);
+  // attention addresses a (sample, head) slice of the [L, 3A] projections with
+  // 32-bit byte offsets; QK-LayerNorm and the attention preprocess index
+  // (token, head) rows in 32 bits
+  REQ((int64_t)d.L * d.heads * d.head_dim * 3 * 4 < (1ll << 31) && (int64_t)d.B * d.L * d.heads * 2 < (1ll << 31),
+      ORBIT_E_UNSUPPORTED, "%s: L=%d with %d heads of %d exceeds the 32-bit attention slice offsets", fn, d.L,
+      d.heads, d.head_dim);
   o->B = d.B; o->L = d.L; o->d = d.d; o->H = d.heads; o->dh = d.head_dim; o->A = d.heads * d.head_dim;
   o->F = d.mlp; o->T = (int64_t)d.B * d.L; o->qk = d.qk_norm; o->eps = d.eps; o->dt = (orbit_dtype)d.dtype;
   return ORBIT_OK;

@@ -223,25 +223,28 @@ __global__ void __launch_bounds__(256) attn_bwd_pre(const OT* __restrict__ o, in
                                                     int64_t lddo, float* __restrict__ D, int B, int H, int L) {
   constexpr int G = DH / 8;
   const int li = threadIdx.x % G;
-  const int64_t row = (int64_t)blockIdx.x * (256 / G) + threadIdx.x / G;  // (t, h)
-  const bool valid = row < (int64_t)B * L * H;
-  const int64_t t = valid ? row / H : 0;
-  const int h = valid ? (int)(row % H) : 0;
+  // row (t, h), 32-bit (the host keeps B * L * H below 2^31)
+  const unsigned row = blockIdx.x * (256u / G) + threadIdx.x / G;
+  const bool valid = row < (unsigned)B * L * H;
+  const unsigned t = valid ? row / (unsigned)H : 0u;
+  const int h = (int)(row - t * (unsigned)H);
   float s = 0.f;
   if (valid) {
     float a8[8], b8[8];
-    unpack(ld128(o + t * ldo + h * DH + li * 8), a8, (OT*)nullptr);
-    unpack(ld128(dO + t * lddo + h * DH + li * 8), b8, (T*)nullptr);
-    if constexpr (sizeof(OT) == 4) unpack(ld128(o + t * ldo + h * DH + li * 8 + 4), a8 + 4, (OT*)nullptr);
-    if constexpr (sizeof(T) == 4) unpack(ld128(dO + t * lddo + h * DH + li * 8 + 4), b8 + 4, (T*)nullptr);
+    const OT* op = o + (int64_t)t * ldo + h * DH + li * 8;
+    const T* dp = dO + (int64_t)t * lddo + h * DH + li * 8;
+    unpack(ld128(op), a8, (OT*)nullptr);
+    unpack(ld128(dp), b8, (T*)nullptr);
+    if constexpr (sizeof(OT) == 4) unpack(ld128(op + 4), a8 + 4, (OT*)nullptr);
+    if constexpr (sizeof(T) == 4) unpack(ld128(dp + 4), b8 + 4, (T*)nullptr);
 #pragma unroll
     for (int i = 0; i < 8; ++i) s += a8[i] * b8[i];
   }
 #pragma unroll
   for (int off = G / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
   if (valid && li == 0) {
-    const int64_t bb = t / L, l = t % L;
-    D[(bb * H + h) * L + l] = s;
+    const unsigned bb = t / (unsigned)L, l = t - bb * (unsigned)L;
+    D[((int64_t)bb * H + h) * L + l] = s;
   }
 }
 
@@ -1069,8 +1072,19 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
   }
 }
 
+// the bf16 kernels address one (sample, head) slice of q, k, v (and dO) with
+// 32-bit byte offsets, and the backward preprocess indexes head rows in 32 bits
+bool slices_fit(const AttnIO& io, int64_t ld_extra) {
+  const int64_t ld = std::max(std::max(io.ldq, io.ldk), std::max(io.ldv, ld_extra));
+  return (int64_t)io.L * ld * 4 < ((int64_t)1 << 31) && (int64_t)io.B * io.L * io.H < ((int64_t)1 << 31);
+}
+
 template <typename T, int DH>
 orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32, hipStream_t s) {
+  if (!slices_fit(io, 0)) {
+    set_error("attention: sequence length %d x row stride too large for 32-bit slice offsets", io.L);
+    return ORBIT_E_UNSUPPORTED;
+  }
   FwdArgs a{io.q, io.k, io.v, o, lse, o32, io.ldq, io.ldk, io.ldv, ldo, ldo32, io.H, io.L, kLog2e / sqrtf((float)DH)};
   const double bh = (double)io.B * io.H;
   KernelInfo ki{sizeof(T) == 2 ? "attn_fwd_kernel<bf16>" : "attn_fwd_kernel<f32>",
@@ -1083,6 +1097,10 @@ orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o3
 template <typename T, int DH>
 orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, const float* lse, const void* dO,
                    int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg, float* D, hipStream_t s) {
+  if (!slices_fit(io, lddo)) {
+    set_error("attention: sequence length %d x row stride too large for 32-bit slice offsets", io.L);
+    return ORBIT_E_UNSUPPORTED;
+  }
   const double bh = (double)io.B * io.H;
   const int64_t rows = (int64_t)io.B * io.L * io.H;
   KernelInfo kp{sizeof(T) == 2 ? "attn_bwd_pre<bf16>" : "attn_bwd_pre<f32>", 2.0 * rows * DH,

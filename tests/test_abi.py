@@ -70,6 +70,10 @@ def test_block_fwd_validation(lib):
     assert _call_block_fwd(lib, d, y=0x1000) == L.ORBIT_E_ARG and "alias" in lib.last_error()
     assert _call_block_fwd(lib, d, ws_bytes=16) == L.ORBIT_E_ARG and "workspace" in lib.last_error()
     assert _call_block_fwd(lib, _bdesc(head_dim=96)) == L.ORBIT_E_UNSUPPORTED
+    # the attention's 32-bit slice offsets: L x 3A bytes must stay well below 2^31
+    big = _bdesc(L=1 << 17, heads=16, head_dim=128)
+    assert lib.orbit_vit_block_workspace_bytes(big) == 0 and "32-bit" in lib.last_error()
+    assert _call_block_fwd(lib, big) == L.ORBIT_E_UNSUPPORTED
     bad = L.BlockParams(*[0x4000 + 0x100 * i for i in range(16)])
     bad.w_fc1 = None
     assert _call_block_fwd(lib, d, params=bad) == L.ORBIT_E_ARG and "w_fc1" in lib.last_error()
