@@ -789,10 +789,10 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
 // back exactly: dK_j += qbar (sum_i dS_ij - sum_i bf16(dS_ij)), both sums in
 // float32, which equals the centred form sum_i bf16(dS_ij) (q_i - qbar) +
 // qbar sum_i dS_ij.
-template <int DH>
-__global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? 3 : 1) attn_bwd_dkdv_tr(BwdArgs a) {
+template <int DH, int QS = 1>
+__global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 : 2) : 1) attn_bwd_dkdv_tr(BwdArgs a) {
   using T = bf16;
-  constexpr int QT = 32;
+  constexpr int QT = 32 * QS;  // queries per LDS tile: QS sub-tiles of 32 per barrier
   using TL = RowTile<QT, DH>;  // Q and dO rows [q][c]
   constexpr int RP = TL::PITCH;
   // the block's V rows stay in LDS rather than in registers, which brings the
@@ -869,47 +869,55 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? 3 : 1) attn_bw
         d_n = q1 + tid < L ? Dv[q1 + tid] : 0.f;
       }
     }
-    const T* Qs = qs[cur];
-    const T* Os = os[cur];
-    f32x16 s, dp;
+    f32x16 s[QS], dp[QS];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+    for (int q = 0; q < QS; ++q) {
+      const T* Qs = qs[cur] + q * 32 * RP;
+      const T* Os = os[cur] + q * 32 * RP;
 #pragma unroll
-    for (int kk = 0; kk < DH / 16; ++kk) {
-      Frag<T> af;
-      ld_frag(af, Qs + (lane & 31) * RP + kk * 16 + g * 8);
-      mma16(s, af, kf[kk]);
-      ld_frag(af, Os + (lane & 31) * RP + kk * 16 + g * 8);
-      if constexpr (VLDS) {
-        Frag<T> vk;
-        ld_frag(vk, vrow + kk * 16);
-        mma16(dp, af, vk);
-      } else {
-        mma16(dp, af, vf[kk]);
+      for (int v = 0; v < 16; ++v) s[q][v] = dp[q][v] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DH / 16; ++kk) {
+        Frag<T> af;
+        ld_frag(af, Qs + (lane & 31) * RP + kk * 16 + g * 8);
+        mma16(s[q], af, kf[kk]);
+        ld_frag(af, Os + (lane & 31) * RP + kk * 16 + g * 8);
+        if constexpr (VLDS) {
+          Frag<T> vk;
+          ld_frag(vk, vrow + kk * 16);
+          mma16(dp[q], af, vk);
+        } else {
+          mma16(dp[q], af, vf[kk]);
+        }
       }
     }
-    // rows: query 8*(v/4) + 4g + v%4 of the tile; column: this lane's key
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int qr = (v >> 2) * 8 + g * 4 + (v & 3);
-      const float p = __builtin_amdgcn_exp2f(fmaf(s[v], a.sl2, -lse_s[cur][qr]));
-      s[v] = p;
-      dp[v] = p * (dp[v] - d_s[cur][qr]);
-      cs += dp[v];
-    }
+    for (int q = 0; q < QS; ++q) {
+      const T* Qs = qs[cur] + q * 32 * RP;
+      const T* Os = os[cur] + q * 32 * RP;
+      // rows: query 8*(v/4) + 4g + v%4 of the sub-tile; column: this lane's key
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      Frag<T> pf, sf;
-      acc_frag(pf, s, kk * 8);
-      acc_frag(sf, dp, kk * 8);
-      csr = frag_sum(sf, csr);
+      for (int v = 0; v < 16; ++v) {
+        const int qr = q * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[q][v], a.sl2, -lse_s[cur][qr]));
+        s[q][v] = p;
+        dp[q][v] = p * (dp[q][v] - d_s[cur][qr]);
+        cs += dp[q][v];
+      }
 #pragma unroll
-      for (int c = 0; c < DH / 32; ++c) {
-        Frag<T> af;
-        ld_frag_tr(af, Os + kk * 16 * RP + c * 32, RP, lane);
-        mma16(dvt[c], af, pf);
-        ld_frag_tr(af, Qs + kk * 16 * RP + c * 32, RP, lane);
-        mma16(dkt[c], af, sf);
+      for (int kk = 0; kk < 2; ++kk) {
+        Frag<T> pf, sf;
+        acc_frag(pf, s[q], kk * 8);
+        acc_frag(sf, dp[q], kk * 8);
+        csr = frag_sum(sf, csr);
+#pragma unroll
+        for (int c = 0; c < DH / 32; ++c) {
+          Frag<T> af;
+          ld_frag_tr(af, Os + kk * 16 * RP + c * 32, RP, lane);
+          mma16(dvt[c], af, pf);
+          ld_frag_tr(af, Qs + kk * 16 * RP + c * 32, RP, lane);
+          mma16(dkt[c], af, sf);
+        }
       }
     }
     if (it + 1 < nq) {
@@ -1137,7 +1145,7 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
                 6.0 * bh * io.L * DH * sizeof(T)};
   const dim3 grid((unsigned)cdiv(io.L, 128), io.H, io.B);
   if constexpr (sizeof(T) == 2) {
-    ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH>, grid, dim3(256), 0, s, a));
+    ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH, DH == 64 ? 2 : 1>, grid, dim3(256), 0, s, a));
   } else {
     ORBIT_TRY(launch(k1, attn_bwd_dkdv<T, DH>, grid, dim3(256), 0, s, a));
   }
