@@ -789,8 +789,12 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
 // back exactly: dK_j += qbar (sum_i dS_ij - sum_i bf16(dS_ij)), both sums in
 // float32, which equals the centred form sum_i bf16(dS_ij) (q_i - qbar) +
 // qbar sum_i dS_ij.
-template <int DH, int QS = 1>
-__global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 : 2) : 1) attn_bwd_dkdv_tr(BwdArgs a) {
+// QG = 2 (grids of at most one block per CU): two groups of 4 waves share the
+// block's 128 keys and take alternate query tiles; group 1's dK, dV partials
+// are added to group 0's through LDS at the end (fixed order).
+template <int DH, int QS = 1, int QG = 1>
+__global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 : 2) : 1)
+attn_bwd_dkdv_tr(BwdArgs a) {
   using T = bf16;
   constexpr int QT = 32 * QS;  // queries per LDS tile: QS sub-tiles of 32 per barrier
   using TL = RowTile<QT, DH>;  // Q and dO rows [q][c]
@@ -799,17 +803,23 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 :
   // kernel within the register budget of three waves per SIMD at head_dim 64
   // and two at head_dim 128
   constexpr bool VLDS = DH >= 64;
-  __shared__ __attribute__((aligned(16))) T qs[2][QT * RP];
-  __shared__ __attribute__((aligned(16))) T os[2][QT * RP];
+  __shared__ __attribute__((aligned(16))) T qs_all[QG][2][QT * RP];
+  __shared__ __attribute__((aligned(16))) T os_all[QG][2][QT * RP];
   __shared__ __attribute__((aligned(16))) T vsh[VLDS ? 128 * RP : 8];
-  __shared__ float lse_s[2][QT], d_s[2][QT];
+  __shared__ float lse_all[QG][2][QT], d_all[QG][2][QT];
   __shared__ float qbar[DH];
 
-  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int lane = threadIdx.x & 63, g = lane >> 5;
+  const int grp = QG == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8);
+  const int tid = threadIdx.x & 255, wave = tid >> 6;
+  auto& qs = qs_all[grp];
+  auto& os = os_all[grp];
+  auto& lse_s = lse_all[grp];
+  auto& d_s = d_all[grp];
   const int h = blockIdx.y, b = blockIdx.z;
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
-  if (tid < DH) qbar[tid] = a.qsum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
+  if (grp == 0 && tid < DH) qbar[tid] = a.qsum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
   const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
   const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
@@ -830,7 +840,7 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 :
       if constexpr (!VLDS) frag_from(vf[kk], z);
     }
   }
-  if constexpr (VLDS) {
+  if (VLDS && grp == 0) {
     RowTile<128, DH> tvb;
     tvb.init(V, a.ldv, L, tid);
     tvb.load(blockIdx.x * 128);
@@ -848,20 +858,27 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 :
   tq.init(Q, a.ldq, L, tid);
   to.init(dO, a.lddo, L, tid);
   const int nq = (L + QT - 1) / QT;
-  tq.load(0);
-  to.load(0);
-  tq.store(qs[0]);
-  to.store(os[0]);
-  if (tid < QT) {
-    lse_s[0][tid] = tid < L ? lse[tid] * kLog2e : INFINITY;
-    d_s[0][tid] = tid < L ? Dv[tid] : 0.f;
+  // group grp takes query tiles grp, grp + QG, ...; every group runs the same
+  // number of iterations (shared barriers), past its last tile without work
+  const int iters = (nq + QG - 1) / QG;
+  {
+    const int q0 = grp * QT;
+    tq.load(q0);
+    to.load(q0);
+    tq.store(qs[0]);
+    to.store(os[0]);
+    if (tid < QT) {
+      lse_s[0][tid] = q0 + tid < L ? lse[q0 + tid] * kLog2e : INFINITY;
+      d_s[0][tid] = q0 + tid < L ? Dv[q0 + tid] : 0.f;
+    }
   }
   __syncthreads();
-  for (int it = 0; it < nq; ++it) {
-    const int cur = it & 1;
+  for (int i = 0; i < iters; ++i) {
+    const int it = i * QG + grp;
+    const int cur = i & 1;
     float lse_n = 0.f, d_n = 0.f;
-    if (it + 1 < nq) {
-      const int q1 = (it + 1) * QT;
+    if (it + QG < nq) {
+      const int q1 = (it + QG) * QT;
       tq.load(q1);
       to.load(q1);
       if (tid < QT) {
@@ -869,6 +886,7 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 :
         d_n = q1 + tid < L ? Dv[q1 + tid] : 0.f;
       }
     }
+    if (QG == 1 || it < nq) {
     f32x16 s[QS], dp[QS];
 #pragma unroll
     for (int q = 0; q < QS; ++q) {
@@ -920,7 +938,8 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 :
         }
       }
     }
-    if (it + 1 < nq) {
+    }
+    if (it + QG < nq) {
       tq.store(qs[cur ^ 1]);
       to.store(os[cur ^ 1]);
       if (tid < QT) {
@@ -933,6 +952,53 @@ __global__ void __launch_bounds__(256, DH == 128 ? 2 : DH == 64 ? (QS == 1 ? 3 :
 
   cs += __shfl_xor(cs, 32, 64);
   csr += __shfl_xor(csr, 32, 64);
+  if constexpr (QG == 2) {
+    // group 1 hands its partials to group 0 through the idle tile areas (the
+    // Q tiles, the dO tiles and the V rows: separate arrays, each holds 32
+    // floats per thread), dV^T first, then dK^T and the remainder sums;
+    // group 0 adds them in that fixed order
+    static_assert(VLDS, "the exchange uses the V-row area");
+    constexpr int C = DH / 32, CPR = (C + 1) / 2;
+    static_assert(CPR * 16 * 256 * 4 <= (int)sizeof(qs_all) && CPR * 16 * 256 * 4 <= (int)sizeof(os_all) &&
+                      2 * 256 * 4 <= (int)sizeof(vsh),
+                  "exchange areas");
+    float* region[3] = {reinterpret_cast<float*>(&qs_all[0][0][0]), reinterpret_cast<float*>(&os_all[0][0][0]),
+                        reinterpret_cast<float*>(vsh)};
+    auto slot = [&](int c, int v) -> float& {
+      return region[c / CPR][(wave * CPR * 16 + (c % CPR) * 16 + v) * 64 + lane];
+    };
+    if (grp == 1) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) slot(c, v) = dvt[c][v];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dvt[c][v] += slot(c, v);
+    }
+    __syncthreads();
+    float* rs = region[2] + wave * 2 * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) slot(c, v) = dkt[c][v];
+      rs[0] = cs;
+      rs[64] = csr;
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dkt[c][v] += slot(c, v);
+    cs += rs[0];
+    csr += rs[64];
+  }
   const float corr = cs - csr;
   if (kv < L) {
     T* dK = static_cast<T*>(a.dk) + (row0 + kv) * a.ldg + h * DH;
@@ -1145,7 +1211,16 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
                 6.0 * bh * io.L * DH * sizeof(T)};
   const dim3 grid((unsigned)cdiv(io.L, 128), io.H, io.B);
   if constexpr (sizeof(T) == 2) {
-    ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH, DH == 64 ? 2 : 1>, grid, dim3(256), 0, s, a));
+    // at most one block per CU (few sample x head pairs): two wave groups per
+    // block split the queries, so each SIMD still runs two waves
+    const bool few = (int64_t)grid.x * grid.y * grid.z <= 256;
+    if constexpr (DH == 128) {
+      if (few) ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH, 1, 2>, grid, dim3(512), 0, s, a));
+      else ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH, 1>, grid, dim3(256), 0, s, a));
+    } else {
+      (void)few;
+      ORBIT_TRY(launch(k1, attn_bwd_dkdv_tr<DH, DH == 64 ? 2 : 1>, grid, dim3(256), 0, s, a));
+    }
   } else {
     ORBIT_TRY(launch(k1, attn_bwd_dkdv<T, DH>, grid, dim3(256), 0, s, a));
   }
