@@ -1021,21 +1021,28 @@ attn_bwd_dkdv_tr(BwdArgs a) {
 // dQ_i = sum_j dS_ij k_j = sum_j dS_ij (k_j - kbar) since sum_j dS_ij = 0; the
 // product runs on the uncentred keys and kbar sum_j bf16(dS_ij) (float32) is
 // subtracted, which equals the centred form sum_j bf16(dS_ij) (k_j - kbar).
-template <int DH>
-__global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
+// QG = 2 (grids of at most one block per CU): two groups of 4 waves share the
+// block's 128 queries and take alternate key tiles; group 1's dQ partials are
+// added to group 0's through LDS at the end (fixed order).
+template <int DH, int QG = 1>
+__global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdArgs a) {
   using T = bf16;
   constexpr int KT = 64;
   using TL = RowTile<KT, DH>;  // K and V rows [kv][c]
   constexpr int KP = TL::PITCH;
-  __shared__ __attribute__((aligned(16))) T ks[2][KT * KP];
-  __shared__ __attribute__((aligned(16))) T vs[2][KT * KP];
+  __shared__ __attribute__((aligned(16))) T ks_all[QG][2][KT * KP];
+  __shared__ __attribute__((aligned(16))) T vs_all[QG][2][KT * KP];
   __shared__ float kbar[DH];
 
-  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
+  const int lane = threadIdx.x & 63, g = lane >> 5;
+  const int grp = QG == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8);
+  const int tid = threadIdx.x & 255, wave = tid >> 6;
+  auto& ks = ks_all[grp];
+  auto& vs = vs_all[grp];
   const int h = blockIdx.y, b = blockIdx.z;
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
-  if (tid < DH) kbar[tid] = a.ksum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
+  if (grp == 0 && tid < DH) kbar[tid] = a.ksum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
   const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
   const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
@@ -1068,17 +1075,18 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
   tk.init(K, a.ldk, L, tid);
   tv.init(V, a.ldv, L, tid);
   const int nt = (L + KT - 1) / KT;
-  tk.load(0);
-  tv.load(0);
+  // group grp takes key tiles grp, grp + QG, ...; both groups run the same
+  // number of iterations (shared barriers)
+  tk.load(grp * KT);
+  tv.load(grp * KT);
   tk.store(ks[0]);
   tv.store(vs[0]);
   __syncthreads();
 
-  auto tile = [&](int jt, auto mask) {
-    const int cur = jt & 1;
-    if (jt + 1 < nt) {
-      tk.load((jt + 1) * KT);
-      tv.load((jt + 1) * KT);
+  auto tile = [&](int jt, int cur, auto mask) {
+    if (jt + QG < nt) {
+      tk.load((jt + QG) * KT);
+      tv.load((jt + QG) * KT);
     }
     const T* Ks = ks[cur];
     const T* Vs = vs[cur];
@@ -1120,17 +1128,51 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_tr(BwdArgs a) {
         mma16(dqt[c], af, sf);
       }
     }
-    if (jt + 1 < nt) {
+    if (jt + QG < nt) {
       tk.store(ks[cur ^ 1]);
       tv.store(vs[cur ^ 1]);
     }
     __syncthreads();
   };
   const int nfull = L / KT;
-  for (int jt = 0; jt < nfull; ++jt) tile(jt, std::false_type{});
-  if (nfull < nt) tile(nfull, std::true_type{});
+  if constexpr (QG == 1) {
+    for (int jt = 0; jt < nfull; ++jt) tile(jt, jt & 1, std::false_type{});
+    if (nfull < nt) tile(nfull, nfull & 1, std::true_type{});
+  } else {
+    // pairs of full tiles, then at most two more tiles (one may be partial;
+    // a group past its last tile only joins the barrier)
+    const int pairs = nfull / QG;
+    for (int i = 0; i < pairs; ++i) tile(i * QG + grp, i & 1, std::false_type{});
+    for (int i = pairs; i < (nt + QG - 1) / QG; ++i) {
+      const int jt = i * QG + grp;
+      if (jt < nt) tile(jt, i & 1, std::true_type{});
+      else __syncthreads();
+    }
+  }
 
   rs += __shfl_xor(rs, 32, 64);
+  if constexpr (QG == 2) {
+    // group 1's dQ^T partials and remainder sum to group 0 through the idle
+    // K-tile area (dQ^T) and V-tile area (sums)
+    constexpr int C = DH / 32;
+    static_assert(C * 16 * 256 * 4 <= (int)sizeof(ks_all) && 256 * 4 <= (int)sizeof(vs_all), "exchange areas");
+    float* rq = reinterpret_cast<float*>(&ks_all[0][0][0]) + wave * C * 16 * 64 + lane;
+    float* rr = reinterpret_cast<float*>(&vs_all[0][0][0]) + wave * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) rq[(c * 16 + v) * 64] = dqt[c][v];
+      rr[0] = rs;
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dqt[c][v] += rq[(c * 16 + v) * 64];
+    rs += rr[0];
+  }
   if (qi < L) {
     T* dQ = static_cast<T*>(a.dq) + (row0 + qi) * a.ldg + h * DH;
 #pragma unroll
@@ -1226,6 +1268,9 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
   }
   KernelInfo k2{sizeof(T) == 2 ? "attn_bwd_dq<bf16>" : "attn_bwd_dq<f32>", 2 * fl * 0.4,
                 5.0 * bh * io.L * DH * sizeof(T)};
+  if constexpr (sizeof(T) == 2 && DH == 128) {
+    if ((int64_t)grid.x * grid.y * grid.z <= 256) return launch(k2, attn_bwd_dq_tr<DH, 2>, grid, dim3(512), 0, s, a);
+  }
   if constexpr (sizeof(T) == 2) return launch(k2, attn_bwd_dq_tr<DH>, grid, dim3(256), 0, s, a);
   return launch(k2, attn_bwd_dq<T, DH>, grid, dim3(256), 0, s, a);
 }
