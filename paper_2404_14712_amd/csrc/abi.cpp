@@ -308,15 +308,31 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
   const size_t e = esz(dt);
   const bool acc = accumulate != 0;
 
+  ColFinal fin;  // parameter-gradient column sums, finished together at the end
+  // a bias gradient is the column sum of its weight-gradient product's B
+  // operand: taken from that product where its kernel forms it, else from a
+  // column-sum job
+  auto dw_bias = [&](Gemm& g, float* part, float* out) -> bool {
+    g.bsum_max_parts = colsum_chunks(T);
+    const int parts = gemm_bsum_parts(g);
+    if (parts <= 0 || parts > colsum_chunks(T)) return false;
+    g.bsum = part;
+    fin.add(part, g.N, parts, g.N, out);
+    return true;
+  };
+  auto bias_job = [](ColJob& j, const void* src, int64_t n, float* part, float* out) {
+    j.src = src; j.ld = n; j.n = (int)n; j.part = part; j.out_sum = out;
+  };
   // feed-forward sub-layer
+  bool fused_fc2, fused_fc1;
   {
     Gemm g; g.dtype = dt; g.tag = "fc2_dw";
     g.A = sv.g; g.lda = z.F; g.a_kmajor = false; g.B = dy; g.ldb = z.d; g.b_kmajor = false;
     g.C = gr->w_fc2; g.ldc = z.d; g.out_f32 = true; g.accumulate = acc;
     g.M = z.F; g.N = z.d; g.K = T;
+    fused_fc2 = dw_bias(g, w.p_fc2, gr->b_fc2);
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ColFinal fin;  // parameter-gradient column sums, finished together at the end
   {
     Gemm g; g.dtype = dt; g.tag = "fc2_dx";
     g.A = dy; g.lda = z.d; g.B = p->w_fc2; g.ldb = z.d; g.b_kmajor = true;
@@ -328,15 +344,16 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.A = sv.h2; g.lda = z.d; g.a_kmajor = false; g.B = w.du; g.ldb = z.F; g.b_kmajor = false;
     g.C = gr->w_fc1; g.ldc = z.F; g.out_f32 = true; g.accumulate = acc;
     g.M = z.d; g.N = z.F; g.K = T;
+    fused_fc1 = dw_bias(g, w.p_fc1, gr->b_fc1);
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   {
     ColJob j[2];
-    j[0].src = w.du; j[0].ld = z.F; j[0].n = z.F; j[0].part = w.p_fc1; j[0].out_sum = gr->b_fc1;
-    j[1].src = dy; j[1].ld = z.d; j[1].n = z.d; j[1].part = w.p_fc2; j[1].out_sum = gr->b_fc2;
-    ORBIT_TRY(colsum_partials(dt, j, 2, T, s));
-    fin.add_job(j[0], T);
-    fin.add_job(j[1], T);
+    int nj = 0;
+    if (!fused_fc1) bias_job(j[nj++], w.du, z.F, w.p_fc1, gr->b_fc1);
+    if (!fused_fc2) bias_job(j[nj++], dy, z.d, w.p_fc2, gr->b_fc2);
+    if (nj) ORBIT_TRY(colsum_partials(dt, j, nj, T, s));
+    for (int i = 0; i < nj; ++i) fin.add_job(j[i], T);
   }
   {
     Gemm g; g.dtype = dt; g.tag = "fc1_dx";
@@ -345,23 +362,25 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, sv.x1, z.d, sv.mu2, sv.r2, p->ln2_g, dy, w.dx1, z.d, T, z.d, s));
-  {
-    ColJob j[2];
-    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = sv.x1; j[0].ldx = z.d; j[0].mean = sv.mu2;
-    j[0].rstd = sv.r2; j[0].part = w.p_ln2; j[0].out_sum = gr->ln2_b; j[0].out_xsum = gr->ln2_g;
-    j[1].src = w.dx1; j[1].ld = z.d; j[1].n = z.d; j[1].part = w.p_proj; j[1].out_sum = gr->b_proj;
-    ORBIT_TRY(colsum_partials(dt, j, 2, T, s));
-    fin.add_job(j[0], T);
-    fin.add_job(j[1], T);
-  }
-  // attention sub-layer
+  bool fused_proj;
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dw";
     g.A = sv.o; g.lda = z.A; g.a_kmajor = false; g.B = w.dx1; g.ldb = z.d; g.b_kmajor = false;
     g.C = gr->w_proj; g.ldc = z.d; g.out_f32 = true; g.accumulate = acc;
     g.M = z.A; g.N = z.d; g.K = T;
+    fused_proj = dw_bias(g, w.p_proj, gr->b_proj);
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
+  {
+    ColJob j[2];
+    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = sv.x1; j[0].ldx = z.d; j[0].mean = sv.mu2;
+    j[0].rstd = sv.r2; j[0].part = w.p_ln2; j[0].out_sum = gr->ln2_b; j[0].out_xsum = gr->ln2_g;
+    int nj = 1;
+    if (!fused_proj) bias_job(j[nj++], w.dx1, z.d, w.p_proj, gr->b_proj);
+    ORBIT_TRY(colsum_partials(dt, j, nj, T, s));
+    for (int i = 0; i < nj; ++i) fin.add_job(j[i], T);
+  }
+  // attention sub-layer
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dx";
     g.A = w.dx1; g.lda = z.d; g.B = p->w_proj; g.ldb = z.d; g.b_kmajor = true;
@@ -390,11 +409,13 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(fill_f32(gr->kn_g, z.dh, 0.f, s));
     ORBIT_TRY(fill_f32(gr->kn_b, z.dh, 0.f, s));
   }
+  bool fused_qkv;
   {
     Gemm g; g.dtype = dt; g.tag = "qkv_dw";
     g.A = sv.h1; g.lda = z.d; g.a_kmajor = false; g.B = w.dqkv; g.ldb = 3 * z.A; g.b_kmajor = false;
     g.C = gr->w_qkv; g.ldc = 3 * z.A; g.out_f32 = true; g.accumulate = acc;
     g.M = z.d; g.N = 3 * z.A; g.K = T;
+    fused_qkv = dw_bias(g, w.p_qkv, gr->b_qkv);
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   {
@@ -406,12 +427,12 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
   ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, x, z.d, sv.mu1, sv.r1, p->ln1_g, w.dx1, dx, z.d, T, z.d, s));
   {
     ColJob j[2];
-    j[0].src = w.dqkv; j[0].ld = 3 * z.A; j[0].n = 3 * z.A; j[0].part = w.p_qkv; j[0].out_sum = gr->b_qkv;
-    j[1].src = w.dh; j[1].ld = z.d; j[1].n = z.d; j[1].x = x; j[1].ldx = z.d; j[1].mean = sv.mu1;
-    j[1].rstd = sv.r1; j[1].part = w.p_ln1; j[1].out_sum = gr->ln1_b; j[1].out_xsum = gr->ln1_g;
-    ORBIT_TRY(colsum_partials(dt, j, 2, T, s));
-    fin.add_job(j[0], T);
-    fin.add_job(j[1], T);
+    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = x; j[0].ldx = z.d; j[0].mean = sv.mu1;
+    j[0].rstd = sv.r1; j[0].part = w.p_ln1; j[0].out_sum = gr->ln1_b; j[0].out_xsum = gr->ln1_g;
+    int nj = 1;
+    if (!fused_qkv) bias_job(j[nj++], w.dqkv, 3 * z.A, w.p_qkv, gr->b_qkv);
+    ORBIT_TRY(colsum_partials(dt, j, nj, T, s));
+    for (int i = 0; i < nj; ++i) fin.add_job(j[i], T);
   }
   return fin.run(accumulate, s);
 }

@@ -26,12 +26,21 @@ struct Gemm {
   const void* res = nullptr; int64_t ldr = 0; int64_t sR = 0;
   int res_row_mod = 0;                           // v += res[(m % mod or m), n]
   bool out_f32 = false;                          // C is float32 (else dtype)
+  // weight-gradient products only (A M-major, B N-major): also the column sums
+  // of B over the K range (a bias gradient) as float32 partials, partial p of
+  // column n of batch b at bsum[(p * batch + b) * N + n] for p < gemm_bsum_parts(g)
+  // (at most bsum_max_parts partials)
+  float* bsum = nullptr;
+  int bsum_max_parts = 1;
   orbit_dtype dtype = ORBIT_BF16;                // operand type of A and B
   const char* tag = "gemm";                      // name prefix for timing
 };
 
 // bytes of float32 split-K partials the product may use (0 if none)
 size_t gemm_workspace_bytes(const Gemm& g);
+// number of column-sum partials gemm() writes for g.bsum (0: the product's
+// kernel does not form them, and g.bsum must be NULL)
+int gemm_bsum_parts(const Gemm& g);
 orbit_status gemm(const Gemm& g, void* ws, size_t ws_bytes, hipStream_t s);
 
 }  // namespace orbit

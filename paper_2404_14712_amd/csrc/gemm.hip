@@ -46,6 +46,8 @@ struct GemmKArgs {
   int batch, splits, k_per_split;
   int vec_ok;      // N, ldc, batch strides and epilogue operands allow 16-byte access
   float* partial;  // splits > 1: float32 partials [splits][batch][M][N]
+  float* bsum;     // column sums of B: [splits][bs_groups][batch][N] (A M-major, B N-major)
+  int bs_groups;   // tile rows that form them, each from a strided subset of the K slices
   Epi epi;
 };
 
@@ -492,6 +494,32 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
     }
     if (!grp) __builtin_amdgcn_s_barrier();
   } else {
+  // weight gradients: the column sums of B (a bias gradient) are formed by the
+  // first bs_groups tile rows, tile row i from the K slices kt = i (mod
+  // bs_groups), so that no block carries much of the extra work; the waves of
+  // a block's first wave row hold every column of B in their fragments, each
+  // lane 8 k of one column per fragment
+  constexpr bool kCanBs = !AK && !BKM;
+  const bool bs_on = kCanBs && g.bsum != nullptr && tile_m < g.bs_groups && wm == 0;
+  int bs_next = tile_m;
+  bool bs_now = false;
+  float bs[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) bs[j] = 0.f;
+  auto bsum_add = [&](const bf16x8* f) {
+    if constexpr (kCanBs) {
+      if (bs_now) {
+        const bf16x2 one = {(bf16)1.f, (bf16)1.f};
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const bf16x2 pr = {f[j][2 * q], f[j][2 * q + 1]};
+            bs[j] = __builtin_amdgcn_fdot2_f32_bf16(pr, one, bs[j], false);
+          }
+      }
+    }
+  };
 #pragma unroll
   for (int i = 0; i < TM; ++i) ra.read(fa[0][i], smem, i, 0);
 #pragma unroll
@@ -503,6 +531,10 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
     // the slot of stage kt + NS - 1 held stage kt - 1, which every wave finished
     // reading before the barrier that ended the previous iteration
     if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    if constexpr (kCanBs) {
+      bs_now = bs_on && kt == bs_next;
+      if (bs_now) bs_next += g.bs_groups;
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) ra.read(fa[1][i], cur, i, 1);
 #pragma unroll
@@ -511,6 +543,7 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
+    bsum_add(fb[0]);
     // stage kt + 1 landed (copies of the stages after it may still be in flight)
     wait_stage<NLS, NS>(min(nk - kt - 2, NS - 2));
     __syncthreads();
@@ -525,6 +558,17 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][i], fb[1][j], acc[i][j], 0, 0, 0);
+    bsum_add(fb[1]);
+  }
+  if (bs_on) {
+    // lanes l and l + 32 hold the two k halves of column l & 31
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const float t = bs[j] + __shfl_xor(bs[j], 32, 64);
+      const int c = n0 + wn * TN * 32 + j * 32 + lane;
+      const int64_t part = (int64_t)split * g.bs_groups + tile_m;
+      if (lane < 32 && c < g.N) g.bsum[(part * g.batch + bz) * g.N + c] = t;
+    }
   }
   }
   wait_vmcnt<0>();
@@ -698,6 +742,15 @@ TileCfg pick_tile(const Gemm& g) {
   return kBig;
 }
 
+// K ranges actually launched for a requested split count: whole 64-deep steps
+// per range, so fewer ranges than requested can cover K
+int used_splits(const Gemm& g, int splits) {
+  if (splits <= 1 || g.K <= 0) return 1;
+  const int bke = bke_of(g.dtype);
+  const int per = (int)cdiv(cdiv(g.K, bke), splits) * bke;
+  return (int)cdiv(g.K, per);
+}
+
 int pick_splits(const Gemm& g, const TileCfg& t) {
   if (g.dtype == ORBIT_BF16 && g.K >= 256 && g.M >= 128 && g.N >= 128 && t == pick_bf16(g).t)
     return pick_bf16(g).splits;
@@ -810,6 +863,21 @@ orbit_status run_typed(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream_
 
 }  // namespace
 
+// tile rows that form the column sums of B: as many as the partial budget
+// allows per K range, at most every tile row
+static int bsum_groups(const Gemm& g, const TileCfg& t, int splits) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(cdiv(g.M, t.BM), g.bsum_max_parts / splits));
+}
+
+int gemm_bsum_parts(const Gemm& g) {
+  if (g.dtype != ORBIT_BF16 || g.a_kmajor || g.b_kmajor || g.M <= 0 || g.N <= 0 || g.K < DBK) return 0;
+  const TileCfg t = pick_tile(g);
+  if (!t.dma || !dma_ok(g)) return 0;
+  const int sp = used_splits(g, pick_splits(g, t));
+  if (sp > g.bsum_max_parts) return 0;
+  return sp * bsum_groups(g, t, sp);
+}
+
 size_t gemm_workspace_bytes(const Gemm& g) {
   const TileCfg t = pick_tile(g);
   const int s = pick_splits(g, t);
@@ -830,6 +898,8 @@ orbit_status gemm_run(const Gemm& g, const TileCfg& t, int splits, void* ws, siz
   a.splits = 1;
   a.k_per_split = g.K;
   a.partial = nullptr;
+  a.bsum = g.bsum;
+  a.bs_groups = 1;
   if (splits > 1 && ws && ws_bytes >= (size_t)splits * g.batch * (size_t)g.M * g.N * sizeof(float)) {
     const int bke = bke_of(g.dtype);
     const int64_t ksteps = cdiv(g.K, bke);
@@ -839,6 +909,7 @@ orbit_status gemm_run(const Gemm& g, const TileCfg& t, int splits, void* ws, siz
     a.partial = static_cast<float*>(ws);
   }
   if (g.K <= 0) a.k_per_split = 0;
+  if (g.bsum) a.bs_groups = bsum_groups(g, t, a.splits);
   {
     auto al = [](int64_t x) { return x % 8 == 0; };
     auto ap = [](const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
@@ -876,6 +947,18 @@ orbit_status gemm(const Gemm& g, void* ws, size_t ws_bytes, hipStream_t s) {
   }
   const TileCfg t = pick_tile(g);
   const int splits = pick_splits(g, t);
+  if (g.bsum) {
+    // the column sums come from gemm_dma_kernel's M-major-A, N-major-B form,
+    // one partial per K split
+    if (gemm_bsum_parts(g) == 0) {
+      set_error("gemm: column sums of B are formed only by bf16 weight-gradient products on the DMA kernel");
+      return ORBIT_E_UNSUPPORTED;
+    }
+    if (splits > 1 && ws_bytes < gemm_workspace_bytes(g)) {
+      set_error("gemm: a product with column sums needs its split-K workspace (%zu bytes)", gemm_workspace_bytes(g));
+      return ORBIT_E_ARG;
+    }
+  }
   return gemm_run(g, t, splits > 1 && ws_bytes >= gemm_workspace_bytes(g) ? splits : 1, ws, ws_bytes, s);
 }
 

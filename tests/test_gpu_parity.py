@@ -114,6 +114,10 @@ BLOCK_CASES = [
     ("bf16", 1, 257, 512, 4, 128, 1032, 1),
     ("bf16", 2, 33, 384, 3, 32, 256, 0),
     ("bf16", 1, 150, 1024, 2, 128, 512, 1),   # shard: A = 256 != d, local MLP width
+    # token counts whose weight-gradient products run on the DMA kernel, which
+    # also forms the bias gradients: one K range, then split-K partials
+    ("bf16", 2, 256, 512, 4, 64, 1024, 1),
+    ("bf16", 1, 2048, 256, 4, 64, 512, 0),
 ]
 
 
