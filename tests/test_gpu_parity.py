@@ -118,6 +118,7 @@ BLOCK_CASES = [
     # also forms the bias gradients: one K range, then split-K partials
     ("bf16", 2, 256, 512, 4, 64, 1024, 1),
     ("bf16", 1, 2048, 256, 4, 64, 512, 0),
+    ("bf16", 1, 1024, 264, 2, 64, 520, 1),    # ragged column tiles of the bias sums
 ]
 
 
