@@ -269,15 +269,25 @@ def main():
     lib.orbit_timing_enable(1)
     lib.orbit_timing_filter(dominant)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(a.steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
+    ev[0].record()
+    for i in range(a.steps):
         step()
-    e1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / a.steps
+    ms = ev[0].elapsed_time(ev[-1]) / a.steps
+    per_step = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(a.steps))
     dk = lib.orbit_timing_summary(dominant)
     lib.orbit_timing_enable(0)
+
+    # one more (untimed) step with events at the block-stack boundaries: the
+    # share of the step in the transformer blocks, forward and backward
+    marks = []
+    vp.forward_backward(inputs, marks=marks)
+    torch.cuda.synchronize()
+    me = dict(marks)
+    blocks_ms = (me["blocks_fwd"].elapsed_time(me["blocks_fwd_end"]) +
+                 me["blocks_bwd"].elapsed_time(me["blocks_bwd_end"]))
 
     tflops = flops["total"] / (ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -315,6 +325,12 @@ def main():
         "samples_per_s": round(samples, 2),
         "tokens_per_s": round(c.B * c.L / (ms * 1e-3), 1),
         "flops_per_step": flops,
+        "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
+        "ms_per_step_min": round(per_step[0], 4),
+        "blocks": {"ms": round(blocks_ms, 4), "tflops": round(flops["blocks"] / (blocks_ms * 1e-3) / 1e12, 2),
+                   "pct_peak": round(100 * flops["blocks"] / (blocks_ms * 1e-3) / 1e12 / peak, 2),
+                   "note": "transformer blocks only (forward + backward), one untimed step with events at the "
+                           "block-stack boundaries"},
         "kernel_ms_per_step": round(step_kernel_ms, 4),
         "top_kernels_ms": [[n, round(t, 4)] for n, t in breakdown],
         "roofline": roof,

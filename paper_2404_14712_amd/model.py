@@ -107,10 +107,20 @@ class ViTPass:
         self.ws = torch.empty(ws, dtype=torch.uint8, device=self.dev)
 
     # ------------------------------------------------------------------------
-    def forward_backward(self, inputs: Dict[str, torch.Tensor], accumulate: int = 0):
+    def forward_backward(self, inputs: Dict[str, torch.Tensor], accumulate: int = 0, marks=None):
         """inputs: full -> img, tgt; blocks -> x, dy; agg_blocks -> tok, dy.
-        Returns the loss tensor (full) or the input gradient."""
+        Returns the loss tensor (full) or the input gradient. With a list for
+        `marks`, appends (phase boundary, recorded timing event) pairs on the
+        current stream: blocks_fwd / blocks_fwd_end around the block forwards,
+        blocks_bwd / blocks_bwd_end around the block backwards."""
         z, lib, P, G = self.z, self.lib, self.params, self.grads
+
+        def mark(name):
+            if marks is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks.append((name, e))
+
         if z.mode == "full":
             e = P["embed"]
             lib.orbit_patch_embed(self.edesc, inputs["img"], e["w_pe"], e["b_pe"], e.get("ve"), self.tok)
@@ -119,8 +129,10 @@ class ViTPass:
             lib.orbit_var_aggregate(self.adesc, inputs["tok"], P["agg"], self.xs[0], self.asaved, self.ws)
         else:
             self.xs[0] = inputs["x"]
+        mark("blocks_fwd")
         for i in range(z.blocks):
             lib.orbit_vit_block_fwd(self.bdesc, P["blocks"][i], self.xs[i], self.xs[i + 1], self.saved[i], self.ws)
+        mark("blocks_fwd_end")
         if z.mode == "full":
             lib.orbit_head_fwd(self.hdesc, self.xs[-1], P["head"], self.pred, self.hsaved, self.ws)
             lib.orbit_mse_loss(self.pred, inputs["tgt"], self.pred.numel(), 1.0, self.loss, self.dpred, self.ws)
@@ -130,11 +142,13 @@ class ViTPass:
         else:
             dy = inputs["dy"]
         bufs = [self.dxb, self.dxa]
+        mark("blocks_bwd")
         for i in range(z.blocks - 1, -1, -1):
             dx = bufs[i % 2] if dy is not bufs[i % 2] else bufs[(i + 1) % 2]
             lib.orbit_vit_block_bwd(self.bdesc, P["blocks"][i], self.xs[i], self.saved[i], dy, dx, G["blocks"][i],
                                     accumulate, self.ws)
             dy = dx
+        mark("blocks_bwd_end")
         self.dx = dy
         if z.mode in ("full", "agg_blocks"):
             tok = self.tok if z.mode == "full" else inputs["tok"]
