@@ -634,6 +634,26 @@ ORBIT_DEV float frag_sum(const Frag<bf16>& f, float acc) {
   return acc;
 }
 
+// (query or key block, head, sample) of this block, arranged so that all the
+// blocks of one (sample, head) run on one XCD and share its L2 for the K/V
+// (or Q/dO) tiles they all stream: hardware block ids go round-robin over the
+// 8 XCDs, so XCD x takes the (sample, head) pairs x, x + 8, ... in turn. Grids
+// whose pair count is not a multiple of 8 keep the plain order.
+ORBIT_DEV void attn_block_coords(int& xb, int& h, int& b) {
+  const unsigned nx = gridDim.x, ny = gridDim.y, pairs = gridDim.y * gridDim.z;
+  if (pairs % 8 == 0) {
+    const unsigned lb = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+    const unsigned i = lb / 8, ph = (i / nx) * 8 + lb % 8;
+    xb = (int)(i % nx);
+    h = (int)(ph % ny);
+    b = (int)(ph / ny);
+  } else {
+    xb = blockIdx.x;
+    h = blockIdx.y;
+    b = blockIdx.z;
+  }
+}
+
 // Softmax reference point: scores are exponentiated as exp2(s - m) with m a
 // running maximum that is raised only when a new score exceeds it by more than
 // this margin (log2 units), so the output is rescaled rarely; the unnormalised
@@ -651,14 +671,15 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
   __shared__ __attribute__((aligned(16))) T vs[2][KT * KP];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, wave = tid >> 6;
-  const int h = blockIdx.y, b = blockIdx.z;
+  int xb, h, b;
+  attn_block_coords(xb, h, b);
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
   const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
   const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
 
-  const int qi = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  const int qi = xb * 128 + wave * 32 + (lane & 31);
   Frag<T> qf[DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
@@ -816,7 +837,8 @@ attn_bwd_dkdv_tr(BwdArgs a) {
   auto& os = os_all[grp];
   auto& lse_s = lse_all[grp];
   auto& d_s = d_all[grp];
-  const int h = blockIdx.y, b = blockIdx.z;
+  int xb, h, b;
+  attn_block_coords(xb, h, b);
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
   if (grp == 0 && tid < DH) qbar[tid] = a.qsum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
@@ -827,7 +849,7 @@ attn_bwd_dkdv_tr(BwdArgs a) {
   const float* lse = a.lse + ((int64_t)b * a.H + h) * L;
   const float* Dv = a.D + ((int64_t)b * a.H + h) * L;
 
-  const int kv = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  const int kv = xb * 128 + wave * 32 + (lane & 31);
   Frag<T> kf[DH / 16], vf[VLDS ? 1 : DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
@@ -843,7 +865,7 @@ attn_bwd_dkdv_tr(BwdArgs a) {
   if (VLDS && grp == 0) {
     RowTile<128, DH> tvb;
     tvb.init(V, a.ldv, L, tid);
-    tvb.load(blockIdx.x * 128);
+    tvb.load(xb * 128);
     tvb.store(vsh);
   }
   const T* vrow = vsh + (wave * 32 + (lane & 31)) * RP + g * 8;
@@ -1039,7 +1061,8 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
   const int tid = threadIdx.x & 255, wave = tid >> 6;
   auto& ks = ks_all[grp];
   auto& vs = vs_all[grp];
-  const int h = blockIdx.y, b = blockIdx.z;
+  int xb, h, b;
+  attn_block_coords(xb, h, b);
   const int L = a.L;
   const int64_t row0 = (int64_t)b * L;
   if (grp == 0 && tid < DH) kbar[tid] = a.ksum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
@@ -1048,7 +1071,7 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
   const T* V = static_cast<const T*>(a.v) + row0 * a.ldv + h * DH;
   const T* dO = static_cast<const T*>(a.dO) + row0 * a.lddo + h * DH;
 
-  const int qi = blockIdx.x * 128 + wave * 32 + (lane & 31);
+  const int qi = xb * 128 + wave * 32 + (lane & 31);
   Frag<T> qf[DH / 16], of[DH / 16];
 #pragma unroll
   for (int kk = 0; kk < DH / 16; ++kk) {
