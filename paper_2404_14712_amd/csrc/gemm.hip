@@ -395,16 +395,25 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WM, wn = wave / WM;
-  const int z = blockIdx.z;
-  const int split = z % g.splits;
-  const int64_t bz = z / g.splits;
+  int split = blockIdx.z % g.splits;
+  const int64_t bz = blockIdx.z / g.splits;
 
   // tile order: XCD-contiguous ranges of tile ids, walked in groups of 8 tile rows
   const int tiles_n = (g.N + BN - 1) / BN, tiles_m = (g.M + BM - 1) / BM;
   const int nt = tiles_m * tiles_n;
   int id = blockIdx.x;
   const int full = nt - nt % 8;
-  if (id < full) id = (id % 8) * (full / 8) + id / 8;
+  if (g.splits > 1 && g.batch == 1 && 8 % g.splits == 0 && (nt * g.splits) % 8 == 0) {
+    // split K: each XCD takes one K range over a contiguous 8 / splits share of
+    // the tiles, so its L2 holds one K range of the A and B panels its tiles
+    // share (every XCD running every range fetched each panel slice from HBM
+    // once per XCD)
+    const int lin = blockIdx.x + nt * (int)blockIdx.z, xcd = lin % 8;
+    split = xcd % g.splits;
+    id = (xcd / g.splits) * (nt * g.splits / 8) + lin / 8;
+  } else if (id < full) {
+    id = (id % 8) * (full / 8) + id / 8;
+  }
   const int per_group = 8 * tiles_n;
   const int first_m = (id / per_group) * 8;
   const int gsize = min(tiles_m - first_m, 8);
