@@ -414,9 +414,12 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
   } else if (id < full) {
     id = (id % 8) * (full / 8) + id / 8;
   }
-  const int per_group = 8 * tiles_n;
-  const int first_m = (id / per_group) * 8;
-  const int gsize = min(tiles_m - first_m, 8);
+  // groups of tile rows sized so that an XCD's share of C is about as tall
+  // as wide in elements (A and B panel bytes per tile in proportion)
+  constexpr int GR = BN == 128 ? 4 : 8;
+  const int per_group = GR * tiles_n;
+  const int first_m = (id / per_group) * GR;
+  const int gsize = min(tiles_m - first_m, GR);
   const int tile_m = first_m + (id % per_group) % gsize;
   const int tile_n = (id % per_group) / gsize;
   const int m0 = tile_m * BM, n0 = tile_n * BN;
