@@ -120,9 +120,32 @@ ORBIT_DEV void frag_from(Frag<float>& f, const float* x) {
   for (int j = 0; j < 4; ++j) { f.lo[j] = x[j]; f.hi[j] = x[4 + j]; }
 }
 
-ORBIT_DEV float gelu_f(float u) { return 0.5f * u * (1.0f + erff(u * 0.70710678118654752f)); }
+// erf(x) for x >= 0 from Abramowitz & Stegun, Handbook of Mathematical
+// Functions, formula 7.1.26 (absolute error below 1.5e-7), given e = exp(-x^2):
+// erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e,  t = 1 / (1 + p x).
+// The GELU epilogues run with the matrix cores idle, so one reciprocal and
+// one exponential (shared with the derivative's normal density) matter.
+ORBIT_DEV float erf_pos_as(float x, float e) {
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  float y = fmaf(1.061405429f, t, -1.453152027f);
+  y = fmaf(y, t, 1.421413741f);
+  y = fmaf(y, t, -0.284496736f);
+  y = fmaf(y, t, 0.254829592f);
+  return 1.0f - y * t * e;
+}
+// GELU(u) = u Phi(u), Phi(u) = (1 + erf(u / sqrt 2)) / 2
+ORBIT_DEV float gelu_f(float u) {
+  const float x = fabsf(u) * 0.70710678118654752f;
+  const float e = __expf(-x * x);
+  const float er = copysignf(erf_pos_as(x, e), u);
+  return 0.5f * u * (1.0f + er);
+}
+// GELU'(u) = Phi(u) + u phi(u), phi(u) = exp(-u^2 / 2) / sqrt(2 pi)
 ORBIT_DEV float gelu_grad_f(float u) {
-  return 0.5f * (1.0f + erff(u * 0.70710678118654752f)) + u * 0.39894228040143268f * __expf(-0.5f * u * u);
+  const float x = fabsf(u) * 0.70710678118654752f;
+  const float e = __expf(-x * x);
+  const float er = copysignf(erf_pos_as(x, e), u);
+  return 0.5f * (1.0f + er) + u * 0.39894228040143268f * e;
 }
 
 ORBIT_DEV float wave_sum(float v) {
