@@ -79,8 +79,10 @@ template <typename T> ORBIT_DEV void st8(T* p, const float* f) {
   if constexpr (sizeof(T) == 4) st128(p + 4, pack(f + 4, (T*)nullptr));
 }
 
+// b8: the bias of columns c0..c0+7 when the caller loaded it ahead (else NULL)
 template <typename T, typename OutT>
-ORBIT_DEV void epi_apply8(const Epi& e, int64_t bz, int r, int c0, float* v, OutT* C, int64_t ldc) {
+ORBIT_DEV void epi_apply8(const Epi& e, int64_t bz, int r, int c0, float* v, OutT* C, int64_t ldc,
+                          const float* b8 = nullptr) {
   const int64_t off = (int64_t)r * ldc + c0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) v[i] *= e.alpha;
@@ -91,7 +93,12 @@ ORBIT_DEV void epi_apply8(const Epi& e, int64_t bz, int r, int c0, float* v, Out
     for (int i = 0; i < 8; ++i) v[i] += t[i];
   }
   if (e.bias) {
-    ld8(static_cast<const T*>(e.bias) + bz * e.sBias + c0, t);
+    if (b8) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) t[i] = b8[i];
+    } else {
+      ld8(static_cast<const T*>(e.bias) + bz * e.sBias + c0, t);
+    }
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += t[i];
   }
@@ -592,6 +599,16 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
   float* ew = reinterpret_cast<float*>(smem) + wave * 32 * EP;
   OutT* C = static_cast<OutT*>(g.C) + bz * g.sC;
   const bool raw = g.splits > 1;
+  // a lane's 8 output columns are the same for all its rows: its bias is
+  // loaded once, not once per row pass
+  float b8[8];
+  {
+    const int pcol = n0 + wn * WTN + (lane % LPR) * 8;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) b8[q] = 0.f;
+    if (!raw && g.vec_ok && g.epi.bias && pcol < g.N)
+      ld8(static_cast<const bf16*>(g.epi.bias) + bz * g.epi.sBias + pcol, b8);
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -620,7 +637,7 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_dma_kernel(GemmKArgs g) 
             for (int q = 0; q < 8 && c0 + q < g.N; ++q) P[c0 + q] = v8[q];
           }
         } else if (g.vec_ok) {
-          epi_apply8<bf16, OutT>(g.epi, bz, r, c0, v8, C, g.ldc);
+          epi_apply8<bf16, OutT>(g.epi, bz, r, c0, v8, C, g.ldc, b8);
         } else {
           for (int q = 0; q < 8 && c0 + q < g.N; ++q) epi_apply<bf16, OutT>(g.epi, bz, r, c0 + q, v8[q], C, g.ldc);
         }
