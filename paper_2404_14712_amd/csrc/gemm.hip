@@ -2,7 +2,8 @@
 // store, GELU derivative, residual, accumulate). Three operand layouts cover
 // all linear layers: forward (A K-major, B N-major), input gradient (both
 // K-major) and weight gradient (both M/N-major: the reduction runs over
-// tokens).
+// tokens; the DMA kernel also forms the column sums of B there, the layer's
+// bias gradient).
 //
 // Large bf16 products run on gemm_dma_kernel: 256x256 tiles, 8 waves (two per
 // SIMD, each owning a 128x64 block of C), operands copied HBM -> LDS by the
