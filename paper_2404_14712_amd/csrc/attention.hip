@@ -1114,6 +1114,22 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
     const T* Ks = ks[cur];
     const T* Vs = vs[cur];
     f32x16 s[2], dp[2];
+    // the softmax of a 32-key half; at head_dim 64 both halves' products are
+    // issued before either half's softmax (the register budget allows it)
+    auto soft = [&](int mt) {
+      if constexpr (decltype(mask)::value) {
+        const int jbase = jt * KT;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3) >= L) s[mt][v] = -INFINITY;
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -lse2));
+        dp[mt][v] = p * (dp[mt][v] - Dq);
+      }
+    };
+    constexpr bool kBoth = DH == 64;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -1126,17 +1142,11 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
         ld_frag(af, Vs + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
         mma16(dp[mt], af, of[kk]);
       }
-      if constexpr (decltype(mask)::value) {
-        const int jbase = jt * KT;
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (jbase + mt * 32 + (v >> 2) * 8 + g * 4 + (v & 3) >= L) s[mt][v] = -INFINITY;
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][v], a.sl2, -lse2));
-        dp[mt][v] = p * (dp[mt][v] - Dq);
-      }
+      if constexpr (!kBoth) soft(mt);
+    }
+    if constexpr (kBoth) {
+      soft(0);
+      soft(1);
     }
     // dQ^T[c][q] += K^T[c][kv] dS^T[kv][q]
 #pragma unroll
