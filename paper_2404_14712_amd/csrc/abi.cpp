@@ -362,6 +362,15 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
   ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, sv.x1, z.d, sv.mu2, sv.r2, p->ln2_g, dy, w.dx1, z.d, T, z.d, s));
+  {
+    // LN2 parameter gradients right after the LN backward, which has just
+    // streamed the same dh and x1 through the caches
+    ColJob j[1];
+    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = sv.x1; j[0].ldx = z.d; j[0].mean = sv.mu2;
+    j[0].rstd = sv.r2; j[0].part = w.p_ln2; j[0].out_sum = gr->ln2_b; j[0].out_xsum = gr->ln2_g;
+    ORBIT_TRY(colsum_partials(dt, j, 1, T, s));
+    fin.add_job(j[0], T);
+  }
   bool fused_proj;
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dw";
@@ -371,14 +380,11 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     fused_proj = dw_bias(g, w.p_proj, gr->b_proj);
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  {
-    ColJob j[2];
-    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = sv.x1; j[0].ldx = z.d; j[0].mean = sv.mu2;
-    j[0].rstd = sv.r2; j[0].part = w.p_ln2; j[0].out_sum = gr->ln2_b; j[0].out_xsum = gr->ln2_g;
-    int nj = 1;
-    if (!fused_proj) bias_job(j[nj++], w.dx1, z.d, w.p_proj, gr->b_proj);
-    ORBIT_TRY(colsum_partials(dt, j, nj, T, s));
-    for (int i = 0; i < nj; ++i) fin.add_job(j[i], T);
+  if (!fused_proj) {
+    ColJob j[1];
+    bias_job(j[0], w.dx1, z.d, w.p_proj, gr->b_proj);
+    ORBIT_TRY(colsum_partials(dt, j, 1, T, s));
+    fin.add_job(j[0], T);
   }
   // attention sub-layer
   {
