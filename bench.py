@@ -209,6 +209,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (reference for HBM byte counters) and exit")
+    ap.add_argument("--kernel-table", action="store_true",
+                    help="print, instead of the JSON line, a markdown table of every kernel of one "
+                         "instrumented step: time, algorithmic flops and bytes, achieved rate against peak")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the model; runs on more than one GPU are not part "
@@ -264,6 +267,23 @@ def main():
     step_kernel_ms = sum(v["ms"] for v in tot.values())
     dominant = max(tot, key=lambda n: tot[n]["ms"])
     breakdown = sorted(((n, v["ms"]) for n, v in tot.items()), key=lambda t: -t[1])[:8]
+
+    if a.kernel_table:
+        peak_f = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_F32_TFLOPS
+        print(f"| kernel | launches | ms/step | % step | algorithmic TFLOP/s (% of {peak_f:.0f}) | "
+              f"algorithmic GB/s (% of {PEAK_HBM_GBS:.0f}) |")
+        print("|---|---|---|---|---|---|")
+        for n, v in sorted(tot.items(), key=lambda kv: -kv[1]["ms"]):
+            if v["ms"] <= 0:
+                continue
+            sec = v["ms"] * 1e-3
+            tf = v["flops"] / sec / 1e12 if v["flops"] > 0 else None
+            gb = v["bytes"] / sec / 1e9 if v["bytes"] > 0 else None
+            tfs = f"{tf:.0f} ({100 * tf / peak_f:.1f}%)" if tf is not None else "-"
+            gbs = f"{gb:.0f} ({100 * gb / PEAK_HBM_GBS:.1f}%)" if gb is not None else "-"
+            print(f"| `{n}` | {int(v['launches'])} | {v['ms']:.3f} | {100 * v['ms'] / step_kernel_ms:.1f} | "
+                  f"{tfs} | {gbs} |")
+        return
 
     # timed region: HIP events around every launch of the dominant kernel
     lib.orbit_timing_enable(1)
