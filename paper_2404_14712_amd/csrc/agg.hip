@@ -531,15 +531,27 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
   // output projection: dpos, db_o, dW_o, dzh
   if (gr.pos) ORBIT_TRY(colsum(dt, dz, (int64_t)z.L * z.d, z.B, z.L * z.d, nullptr, 0, nullptr, nullptr, gr.pos,
                                nullptr, accumulate, cws, s));
-  ORBIT_TRY(colsum(dt, dz, z.d, (int)z.T, z.d, nullptr, 0, nullptr, nullptr, gr.b_o, nullptr, accumulate, cws, s));
   {
+    // db_o is the column sum of dz, the weight-gradient product's B operand:
+    // taken from that product where its kernel forms it
     Gemm g = base_gemm(dt);
     g.tag = "agg_out_dw";
     g.A = sv.zh; g.lda = z.A; g.a_kmajor = false;
     g.B = dz; g.ldb = z.d; g.b_kmajor = false;
     g.C = gr.w_o; g.ldc = z.d; g.out_f32 = true; g.accumulate = accumulate != 0;
     g.M = z.A; g.N = z.d; g.K = (int)z.T;
+    g.bsum_max_parts = colsum_chunks((int)z.T);
+    const int parts = gr.b_o ? gemm_bsum_parts(g) : 0;
+    const bool fused = parts > 0 && parts <= colsum_chunks((int)z.T);
+    if (fused) g.bsum = static_cast<float*>(cws);
+    else
+      ORBIT_TRY(colsum(dt, dz, z.d, (int)z.T, z.d, nullptr, 0, nullptr, nullptr, gr.b_o, nullptr, accumulate, cws, s));
     ORBIT_TRY(gemm(g, gws, gws_bytes, s));
+    if (fused) {
+      ColFinal f;
+      f.add(static_cast<const float*>(cws), z.d, parts, z.d, gr.b_o);
+      ORBIT_TRY(f.run(accumulate, s));
+    }
   }
   {
     Gemm g = base_gemm(dt);

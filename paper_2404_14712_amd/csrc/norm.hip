@@ -245,6 +245,7 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, i
 constexpr int kCsCols = 512;      // columns per block (64 lanes x 8)
 constexpr int kCsRowLanes = 16;   // row lanes per block
 constexpr int kCsMaxChunks = 32;
+constexpr int kCsThinRows = 8;     // at most this many rows: colsum_thin_kernel
 
 int cs_rows_per_chunk(int rows) {
   return (int)std::max<int64_t>(64, cdiv(cdiv(rows, kCsMaxChunks), 16) * 16);
@@ -322,6 +323,33 @@ __global__ void __launch_bounds__(1024) colsum_partials_kernel(CsArgs a) {
     for (int q = 0; q < kCsRowLanes; ++q) t += red[which][q][cc];
     J.part[bz * J.spart + ((int64_t)which * a.chunks + chunk) * J.n + c] = t;
   }
+}
+
+// Column sums of a few rows (the batch sum of a per-position gradient): one
+// thread per 8 consecutive columns adds the rows in order and writes (or adds
+// to) the output directly, with no partials.
+template <typename T>
+__global__ void __launch_bounds__(256) colsum_thin_kernel(const T* src, int64_t ld, int rows, int64_t n,
+                                                          float* out, int accumulate) {
+  const int64_t c = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (c >= n) return;
+  float s[8], d[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s[i] = 0.f;
+  for (int r = 0; r < rows; ++r) {
+    load8(src + (int64_t)r * ld + c, d);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s[i] += d[i];
+  }
+  float4* o = reinterpret_cast<float4*>(out + c);
+  float4 lo = make_float4(s[0], s[1], s[2], s[3]), hi = make_float4(s[4], s[5], s[6], s[7]);
+  if (accumulate) {
+    const float4 a0 = o[0], a1 = o[1];
+    lo = make_float4(a0.x + lo.x, a0.y + lo.y, a0.z + lo.z, a0.w + lo.w);
+    hi = make_float4(a1.x + hi.x, a1.y + hi.y, a1.z + hi.z, a1.w + hi.w);
+  }
+  o[0] = lo;
+  o[1] = hi;
 }
 
 struct CsFinalK {
@@ -734,6 +762,18 @@ orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int 
                     const float* mean, const float* rstd, float* out_sum, float* out_xsum, int accumulate,
                     void* ws, hipStream_t s) {
   if (rows <= 0 || n <= 0) return ORBIT_OK;
+  if (rows <= kCsThinRows && !x && n % 8 == 0 && lddy % 8 == 0 && (reinterpret_cast<uintptr_t>(out_sum) & 15) == 0 &&
+      (reinterpret_cast<uintptr_t>(dy) & 15) == 0) {
+    if (!out_sum) return ORBIT_OK;
+    const dim3 grid((unsigned)cdiv((int64_t)n, 8 * 256));
+    KernelInfo ki{dt == ORBIT_BF16 ? "colsum_thin<bf16>" : "colsum_thin<f32>", 0.0,
+                  (double)rows * n * (dt == ORBIT_BF16 ? 2 : 4) + (accumulate ? 8.0 : 4.0) * n};
+    if (dt == ORBIT_BF16)
+      return launch(ki, colsum_thin_kernel<bf16>, grid, dim3(256), 0, s, static_cast<const bf16*>(dy), lddy, rows,
+                    (int64_t)n, out_sum, accumulate);
+    return launch(ki, colsum_thin_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(dy), lddy, rows,
+                  (int64_t)n, out_sum, accumulate);
+  }
   ColJob J{};
   J.src = dy; J.ld = lddy; J.n = n;
   J.x = x; J.ldx = ldx; J.mean = mean; J.rstd = rstd;
