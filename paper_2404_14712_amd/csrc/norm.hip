@@ -729,27 +729,32 @@ void ColFinal::add_job(const ColJob& J, int rows) {
 }
 
 orbit_status ColFinal::run(int accumulate, hipStream_t s) {
-  size_t i = 0;
-  while (i < items.size()) {
-    // a launch takes consecutive items of the same kind (many or few chunks)
-    const bool many = items[i].chunks > 8;
+  // items are independent (each writes its own output), so a launch takes up
+  // to kColMaxFinal items of one kind (many or few chunks) in any order
+  for (int pass = 0; pass < 2; ++pass) {
+    const bool many = pass == 0;
     const int el = many ? 16 : 256;
-    CsFinalArgs a{};
-    a.accumulate = accumulate;
-    int64_t cb = 0;
-    double bytes = 0;
-    for (; i < items.size() && a.nitems < kColMaxFinal && (items[i].chunks > 8) == many; ++i) {
-      const Item& it = items[i];
-      CsFinalK& K = a.item[a.nitems++];
-      K.part = it.part; K.ldp = it.ldp; K.out = it.out; K.chunks = it.chunks; K.n = it.n; K.cb0 = (int)cb;
-      cb += cdiv(it.n, el);
-      bytes += 4.0 * it.chunks * it.n;
-    }
-    KernelInfo kf{"colsum_final", 0.0, bytes};
-    if (many) {
-      ORBIT_TRY(launch(kf, colsum_final_kernel<16>, dim3((unsigned)cb), dim3(256), 0, s, a));
-    } else {
-      ORBIT_TRY(launch(kf, colsum_final_kernel<1>, dim3((unsigned)cb), dim3(256), 0, s, a));
+    size_t i = 0;
+    for (;;) {
+      CsFinalArgs a{};
+      a.accumulate = accumulate;
+      int64_t cb = 0;
+      double bytes = 0;
+      for (; i < items.size() && a.nitems < kColMaxFinal; ++i) {
+        if ((items[i].chunks > 8) != many) continue;
+        const Item& it = items[i];
+        CsFinalK& K = a.item[a.nitems++];
+        K.part = it.part; K.ldp = it.ldp; K.out = it.out; K.chunks = it.chunks; K.n = it.n; K.cb0 = (int)cb;
+        cb += cdiv(it.n, el);
+        bytes += 4.0 * it.chunks * it.n;
+      }
+      if (a.nitems == 0) break;
+      KernelInfo kf{"colsum_final", 0.0, bytes};
+      if (many) {
+        ORBIT_TRY(launch(kf, colsum_final_kernel<16>, dim3((unsigned)cb), dim3(256), 0, s, a));
+      } else {
+        ORBIT_TRY(launch(kf, colsum_final_kernel<1>, dim3((unsigned)cb), dim3(256), 0, s, a));
+      }
     }
   }
   items.clear();
