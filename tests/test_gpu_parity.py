@@ -102,6 +102,41 @@ def test_var_aggregate(lib, case):
         compare(f"d{k}", host(g[k]), rg[k], rg2[k], tol, floor_ref=rg["b_q"])
 
 
+@pytest.mark.parametrize("case", [AGG_CASES[0], AGG_CASES[3], AGG_CASES[6]])
+def test_var_aggregate_accumulate(lib, case):
+    """Two backward calls, the second with accumulate = 1: every parameter
+    gradient (the batch-summed position gradient and the bias gradients taken
+    from the weight-gradient products included) is twice one call's."""
+    import torch
+    from paper_2404_14712_amd._lib import AggDesc
+    dtype, B, L, V, d, H, dh = case
+    c = synth.small_config(2, dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
+    A = H * dh
+    tok = synth.normal(c.cfg, "tok", (B, L, V, d), dtype=dtype)
+    prm = synth.make_params(c.cfg, "agg", synth.agg_param_shapes(d, A, L), 0.2, dtype)
+    desc = AggDesc(B, L, V, d, H, dh, 1 if dtype == "bf16" else 0)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    z = torch.zeros(B, L, d, dtype=tdt, device="cuda")
+    saved = torch.empty(lib.orbit_var_aggregate_saved_bytes(desc), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(lib.orbit_var_aggregate_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    pd = _dev_params(prm, dtype)
+    tokd = dev(tok, dtype)
+    lib.orbit_var_aggregate(desc, tokd, pd, z, saved, ws)
+    dz = synth.normal(c.cfg, "dz", (B, L, d), dtype=dtype)
+    dzd = dev(dz, dtype)
+    dtok = torch.zeros(B, L, V, d, dtype=tdt, device="cuda")
+    g = {k: torch.full(v.shape, 7.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
+    lib.orbit_var_aggregate_bwd(desc, tokd, pd, saved, dzd, dtok, g, 0, ws)
+    lib.orbit_var_aggregate_bwd(desc, tokd, pd, saved, dzd, dtok, g, 1, ws)
+    torch.cuda.synchronize()
+    _, cache = O.agg_fwd(tok, prm, H)
+    _, rg = O.agg_bwd(dz, cache, prm)
+    _, cache2 = O.agg_fwd(tok, prm, H, store=rounder(dtype))
+    _, rg2 = O.agg_bwd(dz, cache2, prm)
+    for k in rg:
+        compare(f"2 d{k}", host(g[k]), 2 * rg[k], 2 * rg2[k], TOL[dtype], floor_ref=2 * rg["b_q"])
+
+
 # ---------------------------------------------------------------------------
 # block
 # ---------------------------------------------------------------------------
