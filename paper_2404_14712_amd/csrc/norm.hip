@@ -241,7 +241,8 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, i
 // lanes x 8 consecutive columns, 16 row lanes striding over the chunk with 4
 // rows in flight; the 16 row lanes are combined in LDS in a fixed order and
 // the chunk's partial row is stored. Phase 2 sums the chunk partials of any
-// number of outputs in a fixed order (one launch for a whole backward call).
+// number of outputs in a fixed order (per backward call, one launch for the
+// outputs with many partials and one for those with few).
 constexpr int kCsCols = 512;      // columns per block (64 lanes x 8)
 constexpr int kCsRowLanes = 16;   // row lanes per block
 constexpr int kCsMaxChunks = 32;
