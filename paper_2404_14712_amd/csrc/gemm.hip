@@ -765,7 +765,9 @@ Choice pick_bf16(const Gemm& g) {
 }
 
 TileCfg pick_tile(const Gemm& g) {
-  if (g.N <= 32) return kNarrowN;
+  // a long reduction against a few columns (the aggregation's score product,
+  // K = d = 16384 on the 113B shard): 64x64 tiles stream A ~4% faster
+  if (g.N <= 32) return g.dtype == ORBIT_BF16 && g.a_kmajor && g.b_kmajor && g.K >= 8192 ? kSmall : kNarrowN;
   if (g.M <= 32) return kNarrowM;
   if (g.M <= 64 || g.N <= 64) return kSmall;
   if (g.dtype == ORBIT_BF16 && g.K >= 256 && g.M >= 128 && g.N >= 128) return pick_bf16(g).t;

@@ -25,7 +25,9 @@ GEMM_SHAPES = [(37, 40, 24), (200, 136, 72), (130, 264, 520), (1, 48, 64), (300,
                (300, 520, 256), (520, 1032, 1024), (1000, 264, 4096), (264, 2048, 544),
                (1024, 512, 2048), (2048, 1024, 1024), (776, 392, 1056),
                # short reductions on the two-blocks-per-CU DMA tile
-               (300, 200, 64), (520, 264, 32)]
+               (300, 200, 64), (520, 264, 32),
+               # few columns, long reduction (64x64 tiles)
+               (300, 16, 8192)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
