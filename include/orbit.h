@@ -109,7 +109,13 @@ orbit_status orbit_vit_block_fwd(const orbit_block_desc* desc, const orbit_block
                                  void* ws, size_t ws_bytes, void* stream);
 
 /* Backward of orbit_vit_block_fwd given the same x and params and the `saved`
- * tensors of that call. dy, dx: [B, L, d] (dtype); dx may alias dy. */
+ * tensors of that call. dy, dx: [B, L, d] (dtype); dx may alias dy, not x.
+ * saved == NULL selects activation checkpointing (Sec. III-B; Table I): the
+ * call first recomputes the tensors the backward reads from x (the forward
+ * without its last product, whose output the backward does not need) into
+ * the workspace, then runs the backward; results are bitwise identical to
+ * those from a stored `saved`. The caller then keeps only each block's input
+ * between the passes (the forward can run with saved == NULL too). */
 orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block_params* p,
                                  const void* x, const void* saved, const void* dy, void* dx,
                                  const orbit_block_grads* g, int accumulate,

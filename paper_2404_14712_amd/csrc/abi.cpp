@@ -191,6 +191,56 @@ size_t block_ws_bytes(const BlockDims& z) {
   return block_ws_layout(z, nullptr, 0, nullptr, true);
 }
 
+// The forward's kernel sequence, writing the tensors the backward reads into
+// `sv`. With y == NULL the last product (fc2, whose output the backward does
+// not read) is skipped: the recompute of the activation-checkpoint backward.
+orbit_status block_forward_steps(const BlockDims& z, const orbit_block_params* p, const void* x, void* y,
+                                 const BlockSaved& sv, const BlockWs& w, hipStream_t s) {
+  const int T = (int)z.T;
+  const orbit_dtype dt = z.dt;
+  ORBIT_TRY(layernorm_fwd(dt, x, z.d, p->ln1_g, p->ln1_b, sv.h1, z.d, sv.mu1, sv.r1, T, z.d, z.eps, s));
+  {
+    Gemm g; g.dtype = dt; g.tag = "qkv";
+    g.A = sv.h1; g.lda = z.d; g.B = p->w_qkv; g.ldb = 3 * z.A; g.C = sv.qkv; g.ldc = 3 * z.A;
+    g.M = T; g.N = 3 * z.A; g.K = z.d; g.bias = p->b_qkv;
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+  }
+  const size_t e = esz(dt);
+  AttnIO io{};
+  io.B = z.B; io.H = z.H; io.L = z.L; io.dh = z.dh;
+  io.v = static_cast<char*>(sv.qkv) + 2 * z.A * e; io.ldv = 3 * z.A;
+  if (z.qk) {
+    ORBIT_TRY(qk_norm_fwd(dt, sv.qkv, 3 * z.A, sv.qkn, 2 * z.A, p->qn_g, p->qn_b, p->kn_g, p->kn_b, sv.qmu, sv.qr,
+                          T, z.H, z.dh, z.eps, s));
+    io.q = sv.qkn; io.ldq = 2 * z.A;
+    io.k = static_cast<char*>(sv.qkn) + z.A * e; io.ldk = 2 * z.A;
+  } else {
+    io.q = sv.qkv; io.ldq = 3 * z.A;
+    io.k = static_cast<char*>(sv.qkv) + z.A * e; io.ldk = 3 * z.A;
+  }
+  ORBIT_TRY(attn_fwd(dt, io, sv.o, z.A, sv.lse, sv.o32, z.A, s));
+  {
+    Gemm g; g.dtype = dt; g.tag = "proj";
+    g.A = sv.o; g.lda = z.A; g.B = p->w_proj; g.ldb = z.d; g.C = sv.x1; g.ldc = z.d;
+    g.M = T; g.N = z.d; g.K = z.A; g.bias = p->b_proj; g.res = x; g.ldr = z.d;
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+  }
+  ORBIT_TRY(layernorm_fwd(dt, sv.x1, z.d, p->ln2_g, p->ln2_b, sv.h2, z.d, sv.mu2, sv.r2, T, z.d, z.eps, s));
+  {
+    Gemm g; g.dtype = dt; g.tag = "fc1";
+    g.A = sv.h2; g.lda = z.d; g.B = p->w_fc1; g.ldb = z.F; g.C = sv.g; g.ldc = z.F;
+    g.M = T; g.N = z.F; g.K = z.d; g.bias = p->b_fc1; g.gelu_out = sv.u; g.ldgo = z.F;
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+  }
+  if (y) {
+    Gemm g; g.dtype = dt; g.tag = "fc2";
+    g.A = sv.g; g.lda = z.F; g.B = p->w_fc2; g.ldb = z.d; g.C = y; g.ldc = z.d;
+    g.M = T; g.N = z.d; g.K = z.F; g.bias = p->b_fc2; g.res = sv.x1; g.ldr = z.d;
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+  }
+  return ORBIT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -231,50 +281,7 @@ orbit_status orbit_vit_block_fwd(const orbit_block_desc* desc, const orbit_block
   BlockWs w;
   block_ws_layout(z, ws, ws_bytes, &w, true);
   const BlockSaved sv = carve_block_saved(z, inference ? ws : saved, nullptr);
-  const int T = (int)z.T;
-  const orbit_dtype dt = z.dt;
-
-  ORBIT_TRY(layernorm_fwd(dt, x, z.d, p->ln1_g, p->ln1_b, sv.h1, z.d, sv.mu1, sv.r1, T, z.d, z.eps, s));
-  {
-    Gemm g; g.dtype = dt; g.tag = "qkv";
-    g.A = sv.h1; g.lda = z.d; g.B = p->w_qkv; g.ldb = 3 * z.A; g.C = sv.qkv; g.ldc = 3 * z.A;
-    g.M = T; g.N = 3 * z.A; g.K = z.d; g.bias = p->b_qkv;
-    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
-  }
-  const size_t e = esz(dt);
-  AttnIO io{};
-  io.B = z.B; io.H = z.H; io.L = z.L; io.dh = z.dh;
-  io.v = static_cast<char*>(sv.qkv) + 2 * z.A * e; io.ldv = 3 * z.A;
-  if (z.qk) {
-    ORBIT_TRY(qk_norm_fwd(dt, sv.qkv, 3 * z.A, sv.qkn, 2 * z.A, p->qn_g, p->qn_b, p->kn_g, p->kn_b, sv.qmu, sv.qr,
-                          T, z.H, z.dh, z.eps, s));
-    io.q = sv.qkn; io.ldq = 2 * z.A;
-    io.k = static_cast<char*>(sv.qkn) + z.A * e; io.ldk = 2 * z.A;
-  } else {
-    io.q = sv.qkv; io.ldq = 3 * z.A;
-    io.k = static_cast<char*>(sv.qkv) + z.A * e; io.ldk = 3 * z.A;
-  }
-  ORBIT_TRY(attn_fwd(dt, io, sv.o, z.A, sv.lse, sv.o32, z.A, s));
-  {
-    Gemm g; g.dtype = dt; g.tag = "proj";
-    g.A = sv.o; g.lda = z.A; g.B = p->w_proj; g.ldb = z.d; g.C = sv.x1; g.ldc = z.d;
-    g.M = T; g.N = z.d; g.K = z.A; g.bias = p->b_proj; g.res = x; g.ldr = z.d;
-    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
-  }
-  ORBIT_TRY(layernorm_fwd(dt, sv.x1, z.d, p->ln2_g, p->ln2_b, sv.h2, z.d, sv.mu2, sv.r2, T, z.d, z.eps, s));
-  {
-    Gemm g; g.dtype = dt; g.tag = "fc1";
-    g.A = sv.h2; g.lda = z.d; g.B = p->w_fc1; g.ldb = z.F; g.C = sv.g; g.ldc = z.F;
-    g.M = T; g.N = z.F; g.K = z.d; g.bias = p->b_fc1; g.gelu_out = sv.u; g.ldgo = z.F;
-    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
-  }
-  {
-    Gemm g; g.dtype = dt; g.tag = "fc2";
-    g.A = sv.g; g.lda = z.F; g.B = p->w_fc2; g.ldb = z.d; g.C = y; g.ldc = z.d;
-    g.M = T; g.N = z.d; g.K = z.F; g.bias = p->b_fc2; g.res = sv.x1; g.ldr = z.d;
-    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
-  }
-  return ORBIT_OK;
+  return block_forward_steps(z, p, x, y, sv, w, s);
 }
 
 orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block_params* p, const void* x,
@@ -285,10 +292,18 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
   BlockDims z;
   ORBIT_TRY(block_dims(fn, desc, &z));
   REQ(p != nullptr && gr != nullptr, ORBIT_E_ARG, "%s: params or grads is NULL", fn);
-  PTR(x, "x"); PTR(saved, "saved"); PTR(dy, "dy"); PTR(dx, "dx"); PTR(ws, "ws");
+  PTR(x, "x"); OPT_PTR(saved, "saved"); PTR(dy, "dy"); PTR(dx, "dx"); PTR(ws, "ws");
   PTR(p->ln1_g, "ln1_g"); PTR(p->w_qkv, "w_qkv"); PTR(p->w_proj, "w_proj"); PTR(p->ln2_g, "ln2_g");
   PTR(p->w_fc1, "w_fc1"); PTR(p->w_fc2, "w_fc2");
   if (z.qk) { PTR(p->qn_g, "qn_g"); PTR(p->kn_g, "kn_g"); }
+  REQ(dx != x, ORBIT_E_ARG, "%s: dx must not alias x", fn);
+  const bool recompute = saved == nullptr;
+  if (recompute) {
+    // the forward's other parameters are read again by the recompute
+    PTR(p->ln1_b, "ln1_b"); PTR(p->b_qkv, "b_qkv"); PTR(p->b_proj, "b_proj"); PTR(p->ln2_b, "ln2_b");
+    PTR(p->b_fc1, "b_fc1");
+    if (z.qk) { PTR(p->qn_b, "qn_b"); PTR(p->kn_b, "kn_b"); }
+  }
   PTR(gr->ln1_g, "grads.ln1_g"); PTR(gr->ln1_b, "grads.ln1_b"); PTR(gr->w_qkv, "grads.w_qkv");
   PTR(gr->b_qkv, "grads.b_qkv"); PTR(gr->qn_g, "grads.qn_g"); PTR(gr->qn_b, "grads.qn_b");
   PTR(gr->kn_g, "grads.kn_g"); PTR(gr->kn_b, "grads.kn_b"); PTR(gr->w_proj, "grads.w_proj");
@@ -302,7 +317,10 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
   hipStream_t s = S(stream);
   BlockWs w;
   block_ws_layout(z, ws, ws_bytes, &w, true);
-  const BlockSaved sv = carve_block_saved(z, const_cast<void*>(saved), nullptr);
+  // activation checkpointing: the saved tensors are recomputed from x into the
+  // workspace's saved-tensor region (the region the inference forward uses)
+  const BlockSaved sv = carve_block_saved(z, recompute ? ws : const_cast<void*>(saved), nullptr);
+  if (recompute) ORBIT_TRY(block_forward_steps(z, p, x, nullptr, sv, w, s));
   const int T = (int)z.T;
   const orbit_dtype dt = z.dt;
   const size_t e = esz(dt);

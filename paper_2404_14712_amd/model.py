@@ -62,8 +62,13 @@ def _code(dt: str) -> int:
 class ViTPass:
     """Device state of one forward+backward pass (see module docstring)."""
 
-    def __init__(self, lib: OrbitLib, dims: PassDims, params: Dict[str, object], device="cuda"):
+    def __init__(self, lib: OrbitLib, dims: PassDims, params: Dict[str, object], device="cuda",
+                 checkpoint: bool = False):
+        """checkpoint: activation checkpointing of the blocks (Sec. III-B): the
+        forward keeps only each block's input and the backward recomputes the
+        rest (orbit_vit_block_bwd with saved = NULL)."""
         self.lib, self.z, self.dev = lib, dims, torch.device(device)
+        self.checkpoint = checkpoint
         z = dims
         tdt = torch_dtype(z.dtype)
         self.tdt = tdt
@@ -77,7 +82,8 @@ class ViTPass:
         E = lambda *shape, dt=tdt: torch.empty(*shape, dtype=dt, device=self.dev)
         F32 = lambda *shape: torch.zeros(*shape, dtype=torch.float32, device=self.dev)
         self.xs = [E(z.B, z.L, z.d) for _ in range(z.blocks + 1)]
-        self.saved = [torch.empty(sb, dtype=torch.uint8, device=self.dev) for _ in range(z.blocks)]
+        self.saved = [None if checkpoint else torch.empty(sb, dtype=torch.uint8, device=self.dev)
+                      for _ in range(z.blocks)]
         self.dxa = E(z.B, z.L, z.d)
         self.dxb = E(z.B, z.L, z.d)
         self.grads: Dict[str, object] = {"blocks": [
@@ -112,7 +118,8 @@ class ViTPass:
         Returns the loss tensor (full) or the input gradient. With a list for
         `marks`, appends (phase boundary, recorded timing event) pairs on the
         current stream: blocks_fwd / blocks_fwd_end around the block forwards,
-        blocks_bwd / blocks_bwd_end around the block backwards."""
+        blocks_bwd / blocks_bwd_end around the block backwards, and agg_fwd /
+        agg_fwd_end, agg_bwd / agg_bwd_end around the aggregation calls."""
         z, lib, P, G = self.z, self.lib, self.params, self.grads
 
         def mark(name):
@@ -124,9 +131,13 @@ class ViTPass:
         if z.mode == "full":
             e = P["embed"]
             lib.orbit_patch_embed(self.edesc, inputs["img"], e["w_pe"], e["b_pe"], e.get("ve"), self.tok)
+            mark("agg_fwd")
             lib.orbit_var_aggregate(self.adesc, self.tok, P["agg"], self.xs[0], self.asaved, self.ws)
+            mark("agg_fwd_end")
         elif z.mode == "agg_blocks":
+            mark("agg_fwd")
             lib.orbit_var_aggregate(self.adesc, inputs["tok"], P["agg"], self.xs[0], self.asaved, self.ws)
+            mark("agg_fwd_end")
         else:
             self.xs[0] = inputs["x"]
         mark("blocks_fwd")
@@ -152,8 +163,10 @@ class ViTPass:
         self.dx = dy
         if z.mode in ("full", "agg_blocks"):
             tok = self.tok if z.mode == "full" else inputs["tok"]
+            mark("agg_bwd")
             lib.orbit_var_aggregate_bwd(self.adesc, tok, P["agg"], self.asaved, dy, self.dtok, G["agg"], accumulate,
                                         self.ws)
+            mark("agg_bwd_end")
         if z.mode == "full":
             lib.orbit_patch_embed_bwd(self.edesc, inputs["img"], self.dtok, G["embed"]["w_pe"], G["embed"]["b_pe"],
                                       G["embed"].get("ve"), accumulate, self.ws)
@@ -167,6 +180,12 @@ def block_flops(z: PassDims) -> float:
     T = z.T
     return 2.0 * T * z.d * 3 * A + 4.0 * z.B * z.heads * z.L * z.L * z.head_dim + 2.0 * T * A * z.d \
         + 4.0 * T * z.d * z.mlp
+
+
+def recompute_flops(z: PassDims) -> float:
+    """Extra algorithmic flops of activation checkpointing per pass: each
+    block's forward products again, except the last (fc2)."""
+    return (block_flops(z) - 2.0 * z.T * z.mlp * z.d) * z.blocks
 
 
 def pass_flops(z: PassDims) -> Dict[str, float]:

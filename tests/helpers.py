@@ -36,37 +36,15 @@ def rel_err(got, ref) -> float:
     return float(num / den)
 
 
-def rounder(dtype: str):
-    """Storage rounding of the GPU path's intermediates: bf16 (RNE) or float32."""
-    if dtype == "bf16":
-        return lambda a: synth.bf16_round(np.asarray(a, np.float32)).astype(np.float64)
-    return lambda a: np.asarray(a, np.float32).astype(np.float64)
+# Per-tensor errors of the current test, reported at the end of the session
+# (tests/conftest.py prints the worst tensor of every test, so the errors are
+# visible in a quiet run's tail).
+RESULTS: list = []
 
 
-# The bound of a tensor is max(TOL, FLOOR_FACTOR * floor), where floor is how far
-# the same oracle moves when its stored intermediates are rounded to the GPU's
-# storage precision (the unavoidable error of any implementation that stores
-# them so). Where the synthetic model makes a result ill-conditioned (tokens
-# that differ by a few percent amplify every rounding of the shared part),
-# floor exceeds TOL; elsewhere the bound is TOL itself.
-FLOOR_FACTOR = 3.0
-
-
-def _err(got, ref, floor_ref):
-    ref = np.asarray(ref, np.float64)
-    if floor_ref is not None and np.abs(ref).max() <= 1e-9 * np.abs(floor_ref).max():
-        return float(np.abs(np.asarray(got, np.float64)).max() / max(np.abs(floor_ref).max(), 1e-30))
-    return rel_err(got, ref)
-
-
-def compare(name, got, ref, ref_stored, tol, floor_ref=None):
-    """check() with the bound raised to FLOOR_FACTOR x the storage-precision floor."""
-    floor = _err(ref_stored, ref, floor_ref)
-    e = _err(got, ref, floor_ref)
-    bound = max(tol, FLOOR_FACTOR * floor)
-    assert np.all(np.isfinite(np.asarray(got, np.float64))), f"{name}: non-finite values"
-    assert e <= bound, f"{name}: max relative error {e:.3e} > bound {bound:.1e} (tol {tol:.0e}, floor {floor:.2e})"
-    return e, floor
+def record(name: str, err: float, tol: float) -> None:
+    import os
+    RESULTS.append((os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0], name, float(err), float(tol)))
 
 
 def check(name, got, ref, tol, floor_ref=None):
@@ -80,6 +58,7 @@ def check(name, got, ref, tol, floor_ref=None):
     else:
         e = rel_err(got, ref)
     assert np.all(np.isfinite(np.asarray(got, np.float64))), f"{name}: non-finite values"
+    record(name, e, tol)
     assert e <= tol, f"{name}: max relative error {e:.3e} > {tol:.1e}"
     return e
 

@@ -97,6 +97,9 @@ def test_other_entry_validation(lib):
     assert lib.lib.orbit_mse_loss(0x100, 0x200, 0, 1.0, 0x300, None, 0x400, 1024, None) == L.ORBIT_E_ARG
     assert lib.lib.orbit_gemm(1, 16, 16, 16, 0x100, 16, 0, 0x200, 16, 1, 0x300, 16, 1, 1.0, None, 0, None, 0,
                               None) == L.ORBIT_E_UNSUPPORTED
+    # B stored N-major with N = 12: its contiguous dimension is not a multiple of 8
+    assert lib.lib.orbit_gemm(1, 16, 12, 16, 0x100, 16, 1, 0x200, 16, 0, 0x300, 16, 1, 1.0, None, 0, None, 0,
+                              None) == L.ORBIT_E_ARG and "multiple of 8" in lib.last_error()
     assert lib.lib.orbit_attention_fwd(1, 1, 1, 8, 96, 0x100, 96, 0x200, 96, 0x300, 96, 0x400, 96, 0x500,
                                        None, 0, None) == L.ORBIT_E_UNSUPPORTED
 

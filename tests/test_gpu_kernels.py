@@ -30,15 +30,26 @@ GEMM_SHAPES = [(37, 40, 24), (200, 136, 72), (130, 264, 520), (1, 48, 64), (300,
                (300, 16, 8192)]
 
 
+LAYOUTS = {"KN": (1, 0), "KK": (1, 1), "MM": (0, 0)}
+
+
+def _gemm_cases():
+    # the ABI requires the contiguous dimension of each operand to be a
+    # multiple of 8; other layout/shape pairs are rejected (tests/test_abi.py)
+    for shape in GEMM_SHAPES:
+        M, N, K = shape
+        for layout, (a_k, b_k) in LAYOUTS.items():
+            if (not a_k and M % 8) or (b_k and K % 8) or (not b_k and N % 8) or (a_k and K % 8):
+                continue
+            yield pytest.param(layout, shape, id=f"{layout}-{M}x{N}x{K}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("layout", ["KN", "KK", "MM"])
-@pytest.mark.parametrize("shape", GEMM_SHAPES)
+@pytest.mark.parametrize("layout,shape", list(_gemm_cases()))
 def test_gemm(lib, dtype, layout, shape):
     import torch
     M, N, K = shape
-    a_k, b_k = {"KN": (1, 0), "KK": (1, 1), "MM": (0, 0)}[layout]
-    if (not a_k and M % 8) or (b_k and K % 8) or (not b_k and N % 8) or (a_k and K % 8):
-        pytest.skip("contiguous dimension not a multiple of 8")
+    a_k, b_k = LAYOUTS[layout]
     A = _mat((M, K), dtype)
     B = _mat((K, N), dtype)
     bias = _mat((N,), dtype)
@@ -68,11 +79,27 @@ def test_gemm(lib, dtype, layout, shape):
 @pytest.mark.parametrize("dh", [32, 64, 128])
 @pytest.mark.parametrize("L", [1, 37, 130])
 def test_attention(lib, dtype, dh, L):
+    _attention_case(lib, dtype, dh, L, 1.0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dh", [64, 128])
+def test_attention_wide_logits(lib, dtype, dh):
+    """Queries and keys scaled by 2: the logits of every row spread over more
+    than 16 log2 units, twice the margin past which the online softmax raises
+    its running maximum and rescales the output, so that path runs on later
+    key tiles too, not only on the first."""
+    _attention_case(lib, dtype, dh, 300, 2.0)
+
+
+def _attention_case(lib, dtype, dh, L, qk_scale):
     import torch
     B, H = 2, 3
     A = H * dh
     # q, k, v live in one [T, 3A] buffer (as in the block), scaled like QK-normalised rows
     qkv = _mat((B * L, 3 * A), dtype, 1.0)
+    if qk_scale != 1.0:
+        qkv[:, :2 * A] *= np.float32(qk_scale)   # a power of two: bf16 values stay exact
     dO = _mat((B * L, A), dtype, 1.0)
     t = dev(qkv, dtype)
     e = t.element_size()
@@ -96,7 +123,11 @@ def test_attention(lib, dtype, dh, L):
     tol = TOL[dtype]
     check("o", host(o), un(ref_o), tol)
     check("o32", host(o32), un(ref_o), tol)
-    lse_ref = np.log(np.exp((Q @ np.swapaxes(K_, -1, -2)) / np.sqrt(dh)).sum(-1))
+    S_ = (Q @ np.swapaxes(K_, -1, -2)) / np.sqrt(dh)
+    if qk_scale != 1.0:
+        assert (S_.max(-1) - S_.min(-1)).min() * np.log2(np.e) > 16, "logits not spread widely enough"
+    mx = S_.max(-1, keepdims=True)
+    lse_ref = (mx + np.log(np.exp(S_ - mx).sum(-1, keepdims=True)))[..., 0]
     check("lse", host(lse), lse_ref, tol)
     gh = host(g)
     check("dq", gh[:, :A], un(dq), tol)
