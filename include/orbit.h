@@ -268,6 +268,24 @@ orbit_status orbit_attention_bwd(int32_t dtype, int32_t B, int32_t H, int32_t L,
                                  void* dq, void* dk, void* dv, int64_t ldg, void* ws, size_t ws_bytes,
                                  void* stream);
 
+/* orbit_attention_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). The same kernels and results (bitwise)
+ * as orbit_attention_bwd; their scratch lives in a device array the library
+ * holds per GPU (ORBIT_ATTN_BWD_NOALLOC_MAX_SCRATCH bytes on each GPU the
+ * library runs on, until the process ends). The call allocates nothing.
+ * Sizes whose orbit_attention_bwd_workspace_bytes exceeds that maximum return
+ * ORBIT_E_UNSUPPORTED. Every call on one GPU shares that GPU's array, so calls
+ * that overlap on one GPU (concurrent streams or host threads) race: order
+ * them on one stream. The array needs no clearing: every call writes the
+ * scratch it reads. */
+#define ORBIT_ATTN_BWD_NOALLOC_MAX_SCRATCH ((size_t)16 << 20)
+orbit_status orbit_attention_bwd_noalloc(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
+                                         const void* q, int64_t ldq, const void* k, int64_t ldk,
+                                         const void* v, int64_t ldv, const void* o, int64_t ldo,
+                                         int32_t o_f32, const float* lse, const void* dO, int64_t lddo,
+                                         void* dq, void* dk, void* dv, int64_t ldg, void* stream);
+
 /* LayerNorm over rows of length n (biased variance): y = g (x - mean) rstd + b;
  * mean, rstd [rows] float32 (may be NULL). n <= 16384, multiple of 8. */
 orbit_status orbit_layernorm_fwd(int32_t dtype, int32_t rows, int32_t n, const void* x, const void* g,

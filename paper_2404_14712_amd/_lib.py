@@ -107,6 +107,8 @@ _PROTOS = {
     "orbit_attention_bwd_workspace_bytes": (c_size_t, [c_int32] * 4),
     "orbit_attention_bwd": (c_int, [c_int32] * 5 + [P, c_int64, P, c_int64, P, c_int64, P, c_int64, c_int32, P, P,
                                                     c_int64, P, P, P, c_int64, P, c_size_t, P]),
+    "orbit_attention_bwd_noalloc": (c_int, [c_int32] * 5 + [P, c_int64, P, c_int64, P, c_int64, P, c_int64, c_int32,
+                                                            P, P, c_int64, P, P, P, c_int64, P]),
     "orbit_layernorm_fwd": (c_int, [c_int32, c_int32, c_int32, P, P, P, c_float, P, P, P, P]),
     "orbit_status_string": (c_char_p, [c_int]),
     "orbit_last_error": (c_char_p, []),
@@ -278,6 +280,12 @@ class OrbitLib:
             dtype, B, H, L, dh, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, int(o_f32), _ptr(lse),
             _ptr(dO), lddo, _ptr(dq), _ptr(dk), _ptr(dv), ldg, _ptr(ws), ws.numel() * ws.element_size(),
             _stream(stream)))
+
+    def orbit_attention_bwd_noalloc(self, dtype, B, H, L, dh, q, ldq, k, ldk, v, ldv, o, ldo, o_f32, lse, dO, lddo,
+                                    dq, dk, dv, ldg, stream=None):
+        self._check("orbit_attention_bwd_noalloc", self.lib.orbit_attention_bwd_noalloc(
+            dtype, B, H, L, dh, _ptr(q), ldq, _ptr(k), ldk, _ptr(v), ldv, _ptr(o), ldo, int(o_f32), _ptr(lse),
+            _ptr(dO), lddo, _ptr(dq), _ptr(dk), _ptr(dv), ldg, _stream(stream)))
 
     def orbit_layernorm_fwd(self, dtype, rows, n, x, g, b, eps, y, mean, rstd, stream=None):
         self._check("orbit_layernorm_fwd", self.lib.orbit_layernorm_fwd(

@@ -781,6 +781,28 @@ static orbit_status attn_check(const char* fn, int32_t dtype, int32_t B, int32_t
   return ORBIT_OK;
 }
 
+}  // extern "C"
+
+namespace orbit {
+// arguments of the attention backward other than its workspace
+orbit_status attention_bwd_check(const char* fn, int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
+                                 const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv,
+                                 const void* o, int64_t ldo, const float* lse, const void* dO, int64_t lddo,
+                                 const void* dq, const void* dk, const void* dv, int64_t ldg) {
+  ORBIT_TRY(attn_check(fn, dtype, B, H, L, head_dim));
+  PTR(q, "q"); PTR(k, "k"); PTR(v, "v"); PTR(o, "o"); PTR(lse, "lse"); PTR(dO, "dO");
+  PTR(dq, "dq"); PTR(dk, "dk"); PTR(dv, "dv");
+  const int64_t A = (int64_t)H * head_dim;
+  REQ(ldq >= A && ldk >= A && ldv >= A && ldo >= A && lddo >= A && ldg >= A, ORBIT_E_ARG,
+      "%s: leading dimensions must be >= heads*head_dim", fn);
+  REQ(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0 && ldo % 8 == 0 && lddo % 8 == 0 && ldg % 8 == 0, ORBIT_E_ARG,
+      "%s: leading dimensions must be multiples of 8", fn);
+  return ORBIT_OK;
+}
+}  // namespace orbit
+
+extern "C" {
+
 orbit_status orbit_attention_fwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim, const void* q,
                                  int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv, void* o,
                                  int64_t ldo, float* lse, float* o32, int64_t ldo32, void* stream) {
@@ -802,15 +824,10 @@ orbit_status orbit_attention_bwd(int32_t dtype, int32_t B, int32_t H, int32_t L,
                                  void* dk, void* dv, int64_t ldg, void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "orbit_attention_bwd";
   clear_error();
-  ORBIT_TRY(attn_check(fn, dtype, B, H, L, head_dim));
-  PTR(q, "q"); PTR(k, "k"); PTR(v, "v"); PTR(o, "o"); PTR(lse, "lse"); PTR(dO, "dO");
-  PTR(dq, "dq"); PTR(dk, "dk"); PTR(dv, "dv"); PTR(ws, "ws");
+  ORBIT_TRY(attention_bwd_check(fn, dtype, B, H, L, head_dim, q, ldq, k, ldk, v, ldv, o, ldo, lse, dO, lddo, dq, dk,
+                                dv, ldg));
+  PTR(ws, "ws");
   REQ(ws_bytes >= attn_bwd_workspace_bytes(B, H, L, head_dim), ORBIT_E_ARG, "%s: workspace too small", fn);
-  const int64_t A = (int64_t)H * head_dim;
-  REQ(ldq >= A && ldk >= A && ldv >= A && ldo >= A && lddo >= A && ldg >= A, ORBIT_E_ARG,
-      "%s: leading dimensions must be >= heads*head_dim", fn);
-  REQ(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0 && ldo % 8 == 0 && lddo % 8 == 0 && ldg % 8 == 0, ORBIT_E_ARG,
-      "%s: leading dimensions must be multiples of 8", fn);
   AttnIO io{q, k, v, ldq, ldk, ldv, B, H, L, head_dim};
   return attn_bwd((orbit_dtype)dtype, io, o, ldo, o_f32 ? 1 : 0, lse, dO, lddo, dq, dk, dv, ldg,
                   static_cast<float*>(ws), S(stream));

@@ -82,6 +82,12 @@ orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, fl
 // workspace of attn_bwd: D[b,h,l] = rowsum(dO * O), sums of q and k over the
 // sequence, and the column-reduction scratch
 size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh);
+// validation of the attention backward's arguments other than its workspace
+// (shared by the entry points that take a workspace and the one that does not)
+orbit_status attention_bwd_check(const char* fn, int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
+                                 const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv,
+                                 const void* o, int64_t ldo, const float* lse, const void* dO, int64_t lddo,
+                                 const void* dq, const void* dk, const void* dv, int64_t ldg);
 // O is float32 when o_f32, else dtype
 orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t ldo, int o_f32, const float* lse,
                       const void* dO, int64_t lddo, void* dq, void* dk, void* dv, int64_t ldg,
