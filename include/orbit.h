@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define ORBIT_ABI_VERSION 1
+#define ORBIT_ABI_VERSION 2
 
 typedef enum {
   ORBIT_OK = 0,
@@ -192,17 +192,22 @@ orbit_status orbit_var_aggregate_bwd(const orbit_agg_desc* desc, const void* tok
 /* Prediction head (Sec. II: projection from feature space to image space)   */
 /* ------------------------------------------------------------------------ */
 
-/* x[B, L, d] -> pred[B, L, out] float32:  pred = LN_f(x) W_h + b_h
- * (LN_f skipped when final_ln == 0). W_h [d, out], b_h [out]; a token's
- * output row holds its V patches, pixel index v*patch^2 + i*patch + j. */
+/* x[B, L, d] -> pred[B, L, out] float32: h = LN_f(x) (skipped when
+ * final_ln == 0); then `hidden` layers h <- GELU(h W_hid[k] + b_hid[k]) of
+ * width d (the multi-layer decoder of the ClimaX architecture the paper
+ * builds on; 0 = none); then pred = h W_h + b_h.
+ * W_hid [hidden, d, d], b_hid [hidden, d] (NULL when hidden == 0), W_h
+ * [d, out], b_h [out]; a token's output row holds its V patches, pixel index
+ * v*patch^2 + i*patch + j. hidden is at most 8. */
 typedef struct {
   int32_t B, L, d, out, final_ln;
   float eps;
   int32_t dtype;
+  int32_t hidden;
 } orbit_head_desc;
 
-typedef struct { const void *lnf_g, *lnf_b, *w_h, *b_h; } orbit_head_params;
-typedef struct { float *lnf_g, *lnf_b, *w_h, *b_h; } orbit_head_grads;
+typedef struct { const void *lnf_g, *lnf_b, *w_h, *b_h, *w_hid, *b_hid; } orbit_head_params;
+typedef struct { float *lnf_g, *lnf_b, *w_h, *b_h, *w_hid, *b_hid; } orbit_head_grads;
 
 size_t orbit_head_saved_bytes(const orbit_head_desc* desc);
 size_t orbit_head_workspace_bytes(const orbit_head_desc* desc);
@@ -227,6 +232,21 @@ orbit_status orbit_head_bwd(const orbit_head_desc* desc, const void* x,
 size_t orbit_mse_workspace_bytes(int64_t n);
 orbit_status orbit_mse_loss(const float* pred, const float* tgt, int64_t n, float scale,
                             float* loss, float* dpred, void* ws, size_t ws_bytes, void* stream);
+
+/* Latitude-weighted mean squared error (Sec. IV: the training loss) of
+ * predictions and targets in token layout pred, tgt [B, L, V*patch^2] float32
+ * on an H x W grid (L = (H/patch)(W/patch), patch 4):
+ *   loss[0] = mean over (b, v, y, x) of w_y (pred - tgt)^2,
+ *   dpred = 2 w_y (pred - tgt) / n * scale   (n = B*L*V*patch^2),
+ * w_y = cos(lat_y) / mean_y cos(lat_y) with rows at equally spaced latitudes,
+ * cell centres lat_y = -90 + (y + 1/2) 180 / H degrees. dpred may be NULL.
+ * Reduced in a fixed order (bitwise reproducible). */
+typedef struct {
+  int32_t B, H, W, V, patch;
+} orbit_wmse_desc;
+size_t orbit_wmse_workspace_bytes(const orbit_wmse_desc* desc);
+orbit_status orbit_wmse_loss(const orbit_wmse_desc* desc, const float* pred, const float* tgt, float scale,
+                             float* loss, float* dpred, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Building blocks of the calls above, exposed for kernel-level testing      */

@@ -360,35 +360,61 @@ def agg_bwd(dz, cache, prm: Dict[str, np.ndarray]):
 # ---------------------------------------------------------------------------
 
 def head_fwd(x, prm: Dict[str, np.ndarray], final_ln: int = 1, eps: float = 1e-5, store=None):
-    """pred[B, L, V*p*p] = LN_f(x) W_h + b_h (LN_f skipped when final_ln == 0).
-    The output row of a token holds its V patches, pixel index v*p*p + i*p + j."""
+    """pred[B, L, V*p*p] = LN_f(x) followed by the prediction head (Sec. II:
+    projection from feature space back to image space).
+
+    Reading: the head of the ClimaX architecture the paper builds on, i.e.
+    `hidden` layers h <- GELU(h W_k + b_k) of width d (weights w_hid[k] [d, d],
+    b_hid[k] [d]; none when prm has no w_hid or it has zero layers), then one
+    linear map d -> V*p*p (w_h, b_h). LN_f is skipped when final_ln == 0. The
+    output row of a token holds its V patches, pixel index v*p*p + i*p + j.
+    """
     x = _f(x)
-    p = {k_: _f(v_) for k_, v_ in prm.items()}
+    p = {k_: (None if v_ is None else _f(v_)) for k_, v_ in prm.items()}
     S = _keep(store)
     if final_ln:
         hf, c_ln = layer_norm_fwd(x, p["lnf_g"], p["lnf_b"], eps)
         hf = S(hf)
     else:
         hf, c_ln = x, None
-    return hf @ p["w_h"] + p["b_h"], dict(hf=hf, c_ln=c_ln, final_ln=final_ln, store=store)
+    W, bias = p.get("w_hid"), p.get("b_hid")
+    nh = 0 if W is None else W.shape[0]
+    acts, pres = [hf], []
+    h = hf
+    for k in range(nh):
+        u = h @ W[k] + bias[k]
+        pres.append(S(u))
+        h = S(gelu(u))
+        acts.append(h)
+    return h @ p["w_h"] + p["b_h"], dict(hf=hf, c_ln=c_ln, final_ln=final_ln, store=store, acts=acts, pres=pres)
 
 
 def head_bwd(dpred, cache, prm: Dict[str, np.ndarray]):
-    p = {k_: _f(v_) for k_, v_ in prm.items()}
+    p = {k_: (None if v_ is None else _f(v_)) for k_, v_ in prm.items()}
     dpred = _f(dpred)
     B, L, n = dpred.shape
-    hf = cache["hf"]
-    d = hf.shape[-1]
+    acts, pres = cache["acts"], cache["pres"]
+    d = cache["hf"].shape[-1]
+    T = B * L
     S = _keep(cache.get("store"))
-    gr = {"b_h": dpred.reshape(B * L, n).sum(0)}
+    gr = {"b_h": dpred.reshape(T, n).sum(0)}
     dpred = S(dpred)
-    gr["w_h"] = hf.reshape(B * L, d).T @ dpred.reshape(B * L, n)
-    dhf = S(dpred @ p["w_h"].T)
+    gr["w_h"] = acts[-1].reshape(T, -1).T @ dpred.reshape(T, n)
+    dh = S(dpred @ p["w_h"].T)
+    nh = len(pres)
+    if nh:
+        gr["w_hid"] = np.empty_like(p["w_hid"])
+        gr["b_hid"] = np.empty_like(p["b_hid"])
+    for k in range(nh - 1, -1, -1):
+        du = S(dh * gelu_grad(pres[k]))
+        gr["w_hid"][k] = acts[k].reshape(T, d).T @ du.reshape(T, d)
+        gr["b_hid"][k] = du.reshape(T, d).sum(0)
+        dh = S(du @ p["w_hid"][k].T)
     if cache["final_ln"]:
-        dx, gr["lnf_g"], gr["lnf_b"] = layer_norm_bwd(dhf, cache["c_ln"], p["lnf_g"])
+        dx, gr["lnf_g"], gr["lnf_b"] = layer_norm_bwd(dh, cache["c_ln"], p["lnf_g"])
         dx = S(dx)
     else:
-        dx = dhf
+        dx = dh
         gr["lnf_g"] = np.zeros(d)
         gr["lnf_b"] = np.zeros(d)
     return dx, gr
@@ -402,16 +428,55 @@ def mse(pred, tgt, scale: float = 1.0):
     return float((r * r).sum() / n), 2.0 * r / n * scale
 
 
+def lat_weights(H: int) -> np.ndarray:
+    """Latitude weights of the rows of an H-row equiangular grid (Sec. IV: the
+    training loss is the latitude-weighted MSE; grid cells shrink towards the
+    poles, so a row is weighted by its cell area, proportional to cos(latitude)).
+
+    Reading: rows are equally spaced in latitude with cell centres at
+    -90 + (y + 1/2) * 180 / H degrees, and the weights are normalised to mean 1.
+    """
+    lat = np.deg2rad(-90.0 + (np.arange(H, dtype=F64) + 0.5) * 180.0 / H)
+    c = np.cos(lat)
+    return c / c.mean()
+
+
+def unpatchify(t, Wp: int, p: int) -> np.ndarray:
+    """Token layout [B, L, V*p*p] (patch l = ph*Wp + pw, pixel v*p*p + i*p + j)
+    -> image layout [B, V, (L/Wp)*p, Wp*p]; the inverse of patchify."""
+    t = _f(t)
+    B, L, n = t.shape
+    V = n // (p * p)
+    Hp = L // Wp
+    x = t.reshape(B, Hp, Wp, V, p, p)                # [B,ph,pw,v,i,j]
+    x = x.transpose(0, 3, 1, 4, 2, 5)                # [B,v,ph,i,pw,j]
+    return x.reshape(B, V, Hp * p, Wp * p)
+
+
+def wmse(pred, tgt, Wp: int, p: int, scale: float = 1.0):
+    """Latitude-weighted mean squared error (Sec. IV) of predictions and targets
+    in token layout [B, L, V*p*p], and its gradient (times scale) in that layout:
+    loss = mean over (b, v, y, x) of w[y] (pred - tgt)^2, w = lat_weights(H)."""
+    r = unpatchify(pred, Wp, p) - unpatchify(tgt, Wp, p)     # [B,V,H,W]
+    w = lat_weights(r.shape[2])[None, None, :, None]
+    n = r.size
+    g = 2.0 * w * r / n * scale                               # [B,V,H,W]
+    B, V = g.shape[:2]
+    g_tok = patchify(g, p).transpose(0, 2, 1, 3)              # [B,L,V,p*p]
+    return float((w * r * r).sum() / n), g_tok.reshape(B, -1, V * p * p)
+
+
 # ---------------------------------------------------------------------------
 # Whole model (Sec. II, Fig. 1): embed -> aggregate -> blocks -> head -> loss
 # ---------------------------------------------------------------------------
 
 def model_fwd_bwd(img, tgt, emb, agg, blocks, head, *, p: int, agg_heads: int, heads: int,
-                  qk_norm: int = 1, eps: float = 1e-5, final_ln: int = 1, store=None):
+                  qk_norm: int = 1, eps: float = 1e-5, final_ln: int = 1, store=None, loss: str = "mse"):
     """Forward and backward of the full ClimaX-style model for one batch.
 
     Returns (loss, pred, grads) with grads = {"embed": .., "agg": ..,
     "blocks": [..], "head": ..}. `store` as in block_fwd (None: exact).
+    loss: "mse" (plain mean) or "wmse" (latitude-weighted, Sec. IV).
     """
     tok = patch_embed_fwd(img, emb["w_pe"], emb["b_pe"], emb.get("ve"), p, store)
     x, c_agg = agg_fwd(tok, agg, agg_heads, store)
@@ -420,7 +485,10 @@ def model_fwd_bwd(img, tgt, emb, agg, blocks, head, *, p: int, agg_heads: int, h
         x, c = block_fwd(x, prm, heads, qk_norm, eps, store)
         caches.append(c)
     pred, c_head = head_fwd(x, head, final_ln, eps, store)
-    loss, dpred = mse(pred, tgt)
+    if loss == "wmse":
+        loss, dpred = wmse(pred, tgt, _f(img).shape[3] // p, p)
+    else:
+        loss, dpred = mse(pred, tgt)
     dx, g_head = head_bwd(dpred, c_head, head)
     g_blocks = [None] * len(blocks)
     for i in range(len(blocks) - 1, -1, -1):

@@ -17,11 +17,12 @@ LIB_PATH = os.path.join(HERE, "liborbit.so")
 
 ORBIT_OK, ORBIT_E_ARG, ORBIT_E_UNSUPPORTED, ORBIT_E_DEVICE = 0, 1, 2, 3
 ORBIT_F32, ORBIT_BF16 = 0, 1
+ABI_VERSION = 2
 
 BLOCK_PARAMS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "qn_g", "qn_b", "kn_g", "kn_b",
                 "w_proj", "b_proj", "ln2_g", "ln2_b", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
 AGG_PARAMS = ("q0", "w_q", "b_q", "w_k", "b_k", "w_v", "b_v", "w_o", "b_o", "pos")
-HEAD_PARAMS = ("lnf_g", "lnf_b", "w_h", "b_h")
+HEAD_PARAMS = ("lnf_g", "lnf_b", "w_h", "b_h", "w_hid", "b_hid")
 
 
 class BlockDesc(ctypes.Structure):
@@ -58,7 +59,11 @@ class AggGrads(ctypes.Structure):
 
 class HeadDesc(ctypes.Structure):
     _fields_ = [("B", c_int32), ("L", c_int32), ("d", c_int32), ("out", c_int32), ("final_ln", c_int32),
-                ("eps", c_float), ("dtype", c_int32)]
+                ("eps", c_float), ("dtype", c_int32), ("hidden", c_int32)]
+
+
+class WmseDesc(ctypes.Structure):
+    _fields_ = [("B", c_int32), ("H", c_int32), ("W", c_int32), ("V", c_int32), ("patch", c_int32)]
 
 
 class HeadParams(ctypes.Structure):
@@ -99,6 +104,8 @@ _PROTOS = {
                                c_size_t, P]),
     "orbit_mse_workspace_bytes": (c_size_t, [c_int64]),
     "orbit_mse_loss": (c_int, [P, P, c_int64, c_float, P, P, P, c_size_t, P]),
+    "orbit_wmse_workspace_bytes": (c_size_t, [POINTER(WmseDesc)]),
+    "orbit_wmse_loss": (c_int, [POINTER(WmseDesc), P, P, c_float, P, P, P, c_size_t, P]),
     "orbit_gemm_workspace_bytes": (c_size_t, [c_int32] * 6),
     "orbit_gemm": (c_int, [c_int32, c_int32, c_int32, c_int32, P, c_int64, c_int32, P, c_int64, c_int32, P,
                            c_int64, c_int32, c_float, P, c_int32, P, c_size_t, P]),
@@ -154,8 +161,8 @@ class OrbitLib:
             f.restype = res
             f.argtypes = args
         v = self.lib.orbit_abi_version()
-        if v != 1:
-            raise RuntimeError(f"{path}: ABI version {v}, expected 1")
+        if v != ABI_VERSION:
+            raise RuntimeError(f"{path}: ABI version {v}, expected {ABI_VERSION}")
 
     # -- helpers --------------------------------------------------------
     def _check(self, fn: str, st: int):
@@ -252,6 +259,14 @@ class OrbitLib:
     def orbit_mse_loss(self, pred, tgt, n, scale, loss, dpred, ws, stream=None):
         self._check("orbit_mse_loss", self.lib.orbit_mse_loss(
             _ptr(pred), _ptr(tgt), int(n), float(scale), _ptr(loss), _ptr(dpred), _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(stream)))
+
+    def orbit_wmse_workspace_bytes(self, desc) -> int:
+        return self.lib.orbit_wmse_workspace_bytes(ctypes.byref(desc))
+
+    def orbit_wmse_loss(self, desc, pred, tgt, scale, loss, dpred, ws, stream=None):
+        self._check("orbit_wmse_loss", self.lib.orbit_wmse_loss(
+            ctypes.byref(desc), _ptr(pred), _ptr(tgt), float(scale), _ptr(loss), _ptr(dpred), _ptr(ws),
             ws.numel() * ws.element_size(), _stream(stream)))
 
     # -- building blocks -------------------------------------------------------

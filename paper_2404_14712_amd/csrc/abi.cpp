@@ -579,17 +579,26 @@ static orbit_status head_check(const char* fn, const orbit_head_desc* d) {
   REQ(d->d <= 16384, ORBIT_E_UNSUPPORTED, "%s: d=%d exceeds 16384", fn, d->d);
   REQ(d->final_ln == 0 || d->final_ln == 1, ORBIT_E_ARG, "%s: final_ln must be 0 or 1", fn);
   REQ(d->eps > 0.f, ORBIT_E_ARG, "%s: eps must be positive", fn);
+  REQ(d->hidden >= 0 && d->hidden <= 8, ORBIT_E_ARG, "%s: hidden=%d must be 0..8", fn, d->hidden);
+  REQ((int64_t)d->B * d->L < (1ll << 31), ORBIT_E_UNSUPPORTED, "%s: too many tokens", fn);
   return ORBIT_OK;
 }
 
-struct HeadSaved { float *mu, *r; void* hf; };
+// saved: LN_f statistics and output, then per hidden layer its
+// pre-activation u_k and output g_k = GELU(u_k) ([T, d] each)
+struct HeadSaved { float *mu, *r; void* hf; void* u[8]; void* g[8]; };
 static HeadSaved carve_head_saved(const orbit_head_desc& d, void* base, size_t* used) {
   Carver c(base);
   const int64_t T = (int64_t)d.B * d.L;
+  const size_t e = esz(d.dtype);
   HeadSaved s{};
   s.mu = c.take<float>(T);
   s.r = c.take<float>(T);
-  s.hf = c.take<char>(T * d.d * esz(d.dtype));
+  s.hf = c.take<char>(T * d.d * e);
+  for (int k = 0; k < d.hidden; ++k) {
+    s.u[k] = c.take<char>(T * d.d * e);
+    s.g[k] = c.take<char>(T * d.d * e);
+  }
   if (used) *used = c.used();
   return s;
 }
@@ -599,19 +608,27 @@ static size_t head_gemm_ws(const orbit_head_desc& d) {
   g.dtype = (orbit_dtype)d.dtype;
   const int T = d.B * d.L;
   size_t m = 0;
-  g.M = T; g.N = d.out; g.K = d.d; m = std::max(m, gemm_workspace_bytes(g));
-  g.M = d.d; g.N = d.out; g.K = T; g.a_kmajor = false; m = std::max(m, gemm_workspace_bytes(g));
-  g.M = T; g.N = d.d; g.K = d.out; g.a_kmajor = true; g.b_kmajor = true; m = std::max(m, gemm_workspace_bytes(g));
+  for (int n : {d.out, d.d}) {
+    if (n == d.d && d.hidden == 0) continue;
+    g.a_kmajor = true; g.b_kmajor = false;
+    g.M = T; g.N = n; g.K = d.d; m = std::max(m, gemm_workspace_bytes(g));
+    g.M = d.d; g.N = n; g.K = T; g.a_kmajor = false; m = std::max(m, gemm_workspace_bytes(g));
+    g.M = T; g.N = d.d; g.K = n; g.a_kmajor = true; g.b_kmajor = true; m = std::max(m, gemm_workspace_bytes(g));
+  }
   return m;
 }
 
-struct HeadWs { void* dpb; void* dhf; void* cws; void* gws; size_t gws_bytes; };
+// workspace: dpred in the compute dtype, the gradient of the current
+// activation and of the next (ping-pong over the hidden layers), column-sum
+// scratch and the GEMM split-K partials
+struct HeadWs { void* dpb; void* dh[2]; void* cws; void* gws; size_t gws_bytes; };
 static size_t head_ws_layout(const orbit_head_desc& d, void* base, size_t bytes, HeadWs* w) {
   Carver c(base);
   const int64_t T = (int64_t)d.B * d.L;
   HeadWs t{};
   t.dpb = c.take<char>(T * d.out * esz(d.dtype));
-  t.dhf = c.take<char>(T * d.d * esz(d.dtype));
+  t.dh[0] = c.take<char>(T * d.d * esz(d.dtype));
+  t.dh[1] = d.hidden > 0 ? c.take<char>(T * d.d * esz(d.dtype)) : nullptr;
   t.cws = c.take<char>(std::max(colsum_workspace_bytes((int)T, d.out), colsum_workspace_bytes((int)T, d.d)));
   const size_t g = head_gemm_ws(d);
   t.gws = c.take<char>(g);
@@ -643,10 +660,13 @@ orbit_status orbit_head_fwd(const orbit_head_desc* desc, const void* x, const or
   REQ(p != nullptr, ORBIT_E_ARG, "%s: params is NULL", fn);
   PTR(x, "x"); PTR(pred, "pred"); PTR(p->w_h, "w_h"); PTR(p->b_h, "b_h"); OPT_PTR(saved, "saved"); PTR(ws, "ws");
   if (desc->final_ln) { PTR(p->lnf_g, "lnf_g"); PTR(p->lnf_b, "lnf_b"); }
+  if (desc->hidden) { PTR(p->w_hid, "w_hid"); PTR(p->b_hid, "b_hid"); }
   const size_t need = orbit_head_workspace_bytes(desc);
   REQ(ws_bytes >= need, ORBIT_E_ARG, "%s: workspace of %zu bytes is smaller than the %zu required", fn, ws_bytes,
       need);
   const orbit_head_desc& d = *desc;
+  const orbit_dtype dt = (orbit_dtype)d.dtype;
+  const size_t e = esz(dt);
   hipStream_t s = S(stream);
   size_t sv_bytes = 0;
   carve_head_saved(d, nullptr, &sv_bytes);
@@ -656,11 +676,20 @@ orbit_status orbit_head_fwd(const orbit_head_desc* desc, const void* x, const or
   const int T = d.B * d.L;
   const void* hin = x;
   if (d.final_ln) {
-    ORBIT_TRY(layernorm_fwd((orbit_dtype)d.dtype, x, d.d, p->lnf_g, p->lnf_b, sv.hf, d.d, sv.mu, sv.r, T, d.d, d.eps,
-                            s));
+    ORBIT_TRY(layernorm_fwd(dt, x, d.d, p->lnf_g, p->lnf_b, sv.hf, d.d, sv.mu, sv.r, T, d.d, d.eps, s));
     hin = sv.hf;
   }
-  Gemm g; g.dtype = (orbit_dtype)d.dtype; g.tag = "head";
+  for (int k = 0; k < d.hidden; ++k) {
+    // g_k = GELU(h W_k + b_k), pre-activation u_k stored by the epilogue
+    Gemm g; g.dtype = dt; g.tag = "head_hidden";
+    g.A = hin; g.lda = d.d; g.B = static_cast<const char*>(p->w_hid) + (size_t)k * d.d * d.d * e; g.ldb = d.d;
+    g.C = sv.g[k]; g.ldc = d.d; g.M = T; g.N = d.d; g.K = d.d;
+    g.bias = static_cast<const char*>(p->b_hid) + (size_t)k * d.d * e;
+    g.gelu_out = sv.u[k]; g.ldgo = d.d;
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+    hin = sv.g[k];
+  }
+  Gemm g; g.dtype = dt; g.tag = "head";
   g.A = hin; g.lda = d.d; g.B = p->w_h; g.ldb = d.out; g.C = pred; g.ldc = d.out; g.out_f32 = true;
   g.M = T; g.N = d.out; g.K = d.d; g.bias = p->b_h;
   return gemm(g, w.gws, w.gws_bytes, s);
@@ -678,12 +707,16 @@ orbit_status orbit_head_bwd(const orbit_head_desc* desc, const void* x, const or
   if (desc->final_ln) {
     PTR(p->lnf_g, "lnf_g"); PTR(gr->lnf_g, "grads.lnf_g"); PTR(gr->lnf_b, "grads.lnf_b");
   }
+  if (desc->hidden) {
+    PTR(p->w_hid, "w_hid"); PTR(gr->w_hid, "grads.w_hid"); PTR(gr->b_hid, "grads.b_hid");
+  }
   REQ(accumulate == 0 || accumulate == 1, ORBIT_E_ARG, "%s: accumulate must be 0 or 1", fn);
   const size_t need = orbit_head_workspace_bytes(desc);
   REQ(ws_bytes >= need, ORBIT_E_ARG, "%s: workspace of %zu bytes is smaller than the %zu required", fn, ws_bytes,
       need);
   const orbit_head_desc& d = *desc;
   const orbit_dtype dt = (orbit_dtype)d.dtype;
+  const size_t e = esz(dt);
   hipStream_t s = S(stream);
   size_t sv_bytes = 0;
   carve_head_saved(d, nullptr, &sv_bytes);
@@ -691,7 +724,8 @@ orbit_status orbit_head_bwd(const orbit_head_desc* desc, const void* x, const or
   HeadWs w;
   head_ws_layout(d, static_cast<char*>(ws) + sv_bytes, ws_bytes - sv_bytes, &w);
   const int T = d.B * d.L;
-  const void* hin = d.final_ln ? sv.hf : x;
+  const void* hf = d.final_ln ? sv.hf : x;
+  const int nh = d.hidden;
   ORBIT_TRY(colsum_f32(dpred, d.out, T, d.out, gr->b_h, accumulate, w.cws, s));
   const void* dpb = dpred;
   if (dt == ORBIT_BF16) {
@@ -700,20 +734,44 @@ orbit_status orbit_head_bwd(const orbit_head_desc* desc, const void* x, const or
   }
   {
     Gemm g; g.dtype = dt; g.tag = "head_dw";
-    g.A = hin; g.lda = d.d; g.a_kmajor = false; g.B = dpb; g.ldb = d.out; g.b_kmajor = false;
+    g.A = nh ? sv.g[nh - 1] : hf; g.lda = d.d; g.a_kmajor = false; g.B = dpb; g.ldb = d.out; g.b_kmajor = false;
     g.C = gr->w_h; g.ldc = d.out; g.out_f32 = true; g.accumulate = accumulate != 0;
     g.M = d.d; g.N = d.out; g.K = T;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
+  // gradient entering the last activation; with hidden layers the GELU
+  // derivative of its pre-activation is fused into the product
+  void* dcur = (nh == 0 && !d.final_ln) ? dx : w.dh[0];
   {
     Gemm g; g.dtype = dt; g.tag = "head_dx";
     g.A = dpb; g.lda = d.out; g.B = p->w_h; g.ldb = d.out; g.b_kmajor = true;
-    g.C = d.final_ln ? w.dhf : dx; g.ldc = d.d; g.M = T; g.N = d.d; g.K = d.out;
+    g.C = dcur; g.ldc = d.d; g.M = T; g.N = d.d; g.K = d.out;
+    if (nh) { g.gelu_in = sv.u[nh - 1]; g.ldgi = d.d; }
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
+  for (int k = nh - 1; k >= 0; --k) {
+    // dcur holds du_k, the gradient of the k-th pre-activation
+    const void* hk = k ? sv.g[k - 1] : hf;
+    {
+      Gemm g; g.dtype = dt; g.tag = "head_hidden_dw";
+      g.A = hk; g.lda = d.d; g.a_kmajor = false; g.B = dcur; g.ldb = d.d; g.b_kmajor = false;
+      g.C = gr->w_hid + (size_t)k * d.d * d.d; g.ldc = d.d; g.out_f32 = true; g.accumulate = accumulate != 0;
+      g.M = d.d; g.N = d.d; g.K = T;
+      ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+    }
+    ORBIT_TRY(colsum(dt, dcur, d.d, T, d.d, nullptr, 0, nullptr, nullptr, gr->b_hid + (size_t)k * d.d, nullptr,
+                     accumulate, w.cws, s));
+    void* dnext = (k == 0 && !d.final_ln) ? dx : (dcur == w.dh[0] ? w.dh[1] : w.dh[0]);
+    Gemm g; g.dtype = dt; g.tag = "head_hidden_dx";
+    g.A = dcur; g.lda = d.d; g.B = static_cast<const char*>(p->w_hid) + (size_t)k * d.d * d.d * e; g.ldb = d.d;
+    g.b_kmajor = true; g.C = dnext; g.ldc = d.d; g.M = T; g.N = d.d; g.K = d.d;
+    if (k) { g.gelu_in = sv.u[k - 1]; g.ldgi = d.d; }
+    ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
+    dcur = dnext;
+  }
   if (d.final_ln) {
-    ORBIT_TRY(layernorm_bwd(dt, w.dhf, d.d, x, d.d, sv.mu, sv.r, p->lnf_g, nullptr, dx, d.d, T, d.d, s));
-    ORBIT_TRY(colsum(dt, w.dhf, d.d, T, d.d, x, d.d, sv.mu, sv.r, gr->lnf_b, gr->lnf_g, accumulate, w.cws, s));
+    ORBIT_TRY(layernorm_bwd(dt, dcur, d.d, x, d.d, sv.mu, sv.r, p->lnf_g, nullptr, dx, d.d, T, d.d, s));
+    ORBIT_TRY(colsum(dt, dcur, d.d, T, d.d, x, d.d, sv.mu, sv.r, gr->lnf_b, gr->lnf_g, accumulate, w.cws, s));
   } else if (!accumulate) {
     if (gr->lnf_g) ORBIT_TRY(fill_f32(gr->lnf_g, d.d, 0.f, s));
     if (gr->lnf_b) ORBIT_TRY(fill_f32(gr->lnf_b, d.d, 0.f, s));
@@ -734,6 +792,34 @@ orbit_status orbit_mse_loss(const float* pred, const float* tgt, int64_t n, floa
   PTR(pred, "pred"); PTR(tgt, "tgt"); PTR(loss, "loss"); OPT_PTR(dpred, "dpred"); PTR(ws, "ws");
   REQ(ws_bytes >= mse_workspace_bytes(n), ORBIT_E_ARG, "%s: workspace too small", fn);
   return mse(pred, tgt, n, scale, loss, dpred, ws, S(stream));
+}
+
+static orbit_status wmse_check(const char* fn, const orbit_wmse_desc* d) {
+  REQ(d != nullptr, ORBIT_E_ARG, "%s: desc is NULL", fn);
+  REQ(d->B > 0 && d->H > 0 && d->W > 0 && d->V > 0, ORBIT_E_ARG, "%s: sizes must be positive", fn);
+  REQ(d->patch == 4, ORBIT_E_UNSUPPORTED, "%s: patch size %d unsupported (4)", fn, d->patch);
+  REQ(d->H % 4 == 0 && d->W % 4 == 0, ORBIT_E_ARG, "%s: H=%d and W=%d must be multiples of the patch", fn, d->H,
+      d->W);
+  REQ((int64_t)d->B * (d->H / 4) * (d->W / 4) < (1ll << 31) && (int64_t)d->V * 16 < (1ll << 31),
+      ORBIT_E_UNSUPPORTED, "%s: too many tokens", fn);
+  return ORBIT_OK;
+}
+
+size_t orbit_wmse_workspace_bytes(const orbit_wmse_desc* desc) {
+  if (wmse_check("orbit_wmse_workspace_bytes", desc) != ORBIT_OK) return 0;
+  return wmse_workspace_bytes((int64_t)desc->B * (desc->H / 4) * (desc->W / 4));
+}
+
+orbit_status orbit_wmse_loss(const orbit_wmse_desc* desc, const float* pred, const float* tgt, float scale,
+                             float* loss, float* dpred, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "orbit_wmse_loss";
+  clear_error();
+  ORBIT_TRY(wmse_check(fn, desc));
+  PTR(pred, "pred"); PTR(tgt, "tgt"); PTR(loss, "loss"); OPT_PTR(dpred, "dpred"); PTR(ws, "ws");
+  const orbit_wmse_desc& d = *desc;
+  const int L = (d.H / 4) * (d.W / 4);
+  REQ(ws_bytes >= wmse_workspace_bytes((int64_t)d.B * L), ORBIT_E_ARG, "%s: workspace too small", fn);
+  return wmse(pred, tgt, d.B, L, d.W / 4, d.H, d.V * 16, scale, loss, dpred, ws, S(stream));
 }
 
 // ---------------------------------------------------------------------------

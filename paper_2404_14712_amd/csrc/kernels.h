@@ -106,6 +106,11 @@ orbit_status patch_embed_bwd(orbit_dtype dt, const float* img, const void* dtok,
 size_t mse_workspace_bytes(int64_t n);
 orbit_status mse(const float* pred, const float* tgt, int64_t n, float scale, float* loss,
                  float* dpred, void* ws, hipStream_t s);
+// latitude-weighted MSE of token-layout predictions [B*L, out] on an H-row
+// grid of 4x4 patches, Wp patches per row; workspace: one float per token
+size_t wmse_workspace_bytes(int64_t tokens);
+orbit_status wmse(const float* pred, const float* tgt, int B, int L, int Wp, int H, int out, float scale,
+                  float* loss, float* dpred, void* ws, hipStream_t s);
 
 // ---- small helpers ------------------------------------------------------------
 // dst[i] = (dtype) src[i] (float32 -> dtype); used for dpred before the head GEMMs

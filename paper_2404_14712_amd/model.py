@@ -19,7 +19,7 @@ from typing import Dict, List, Optional
 
 import torch
 
-from ._lib import (AggDesc, BlockDesc, EmbedDesc, HeadDesc, ORBIT_BF16, ORBIT_F32, OrbitLib)
+from ._lib import (AggDesc, BlockDesc, EmbedDesc, HeadDesc, ORBIT_BF16, ORBIT_F32, OrbitLib, WmseDesc)
 
 
 @dataclasses.dataclass
@@ -41,6 +41,8 @@ class PassDims:
     agg_head_dim: int = 0
     final_ln: int = 1
     patch: int = 4
+    head_hidden: int = 0  # GELU layers of width d in the prediction head before its last linear map
+    loss: str = "mse"     # "mse" or "wmse" (latitude-weighted, Sec. IV)
 
     @property
     def T(self):
@@ -100,7 +102,7 @@ class ViTPass:
             self.edesc = EmbedDesc(z.B, z.V, Hg, Wg, z.patch, z.d, code)
             ws = max(ws, lib.orbit_patch_embed_workspace_bytes(self.edesc))
             self.tok = E(z.B, z.L, z.V, z.d)
-            self.hdesc = HeadDesc(z.B, z.L, z.d, z.out, z.final_ln, z.eps, code)
+            self.hdesc = HeadDesc(z.B, z.L, z.d, z.out, z.final_ln, z.eps, code, z.head_hidden)
             ws = max(ws, lib.orbit_head_workspace_bytes(self.hdesc))
             self.hsaved = torch.empty(lib.orbit_head_saved_bytes(self.hdesc), dtype=torch.uint8, device=self.dev)
             self.pred = F32(z.B, z.L, z.out)
@@ -108,8 +110,11 @@ class ViTPass:
             self.loss = F32(1)
             n = z.T * z.out
             ws = max(ws, lib.orbit_mse_workspace_bytes(n))
+            if z.loss == "wmse":
+                self.wdesc = WmseDesc(z.B, z.grid[0], z.grid[1], z.V, z.patch)
+                ws = max(ws, lib.orbit_wmse_workspace_bytes(self.wdesc))
             self.grads["embed"] = {k: F32(*v.shape) for k, v in params["embed"].items() if v is not None}
-            self.grads["head"] = {k: F32(*v.shape) for k, v in params["head"].items()}
+            self.grads["head"] = {k: F32(*v.shape) for k, v in params["head"].items() if v is not None}
         self.ws = torch.empty(ws, dtype=torch.uint8, device=self.dev)
 
     # ------------------------------------------------------------------------
@@ -146,7 +151,10 @@ class ViTPass:
         mark("blocks_fwd_end")
         if z.mode == "full":
             lib.orbit_head_fwd(self.hdesc, self.xs[-1], P["head"], self.pred, self.hsaved, self.ws)
-            lib.orbit_mse_loss(self.pred, inputs["tgt"], self.pred.numel(), 1.0, self.loss, self.dpred, self.ws)
+            if z.loss == "wmse":
+                lib.orbit_wmse_loss(self.wdesc, self.pred, inputs["tgt"], 1.0, self.loss, self.dpred, self.ws)
+            else:
+                lib.orbit_mse_loss(self.pred, inputs["tgt"], self.pred.numel(), 1.0, self.loss, self.dpred, self.ws)
             lib.orbit_head_bwd(self.hdesc, self.xs[-1], P["head"], self.hsaved, self.dpred, self.dxa, G["head"],
                                accumulate, self.ws)
             dy = self.dxa
@@ -202,6 +210,6 @@ def pass_flops(z: PassDims) -> Dict[str, float]:
         out["aggregation"] = 3.0 * fwd
     if z.mode == "full":
         out["patch_embed"] = 3.0 * 2.0 * T * z.V * 16 * z.d
-        out["head"] = 3.0 * 2.0 * T * z.d * z.out
+        out["head"] = 3.0 * 2.0 * T * z.d * (z.out + z.head_hidden * z.d)
     out["total"] = sum(out.values())
     return out

@@ -153,8 +153,11 @@ def embed_param_shapes(V: int, d: int, p: int = PATCH) -> Dict[str, tuple]:
     return {"w_pe": (V, p * p, d), "b_pe": (V, d), "ve": (V, d)}
 
 
-def head_param_shapes(d: int, out: int) -> Dict[str, tuple]:
-    return {"lnf_g": (d,), "lnf_b": (d,), "w_h": (d, out), "b_h": (out,)}
+def head_param_shapes(d: int, out: int, hidden: int = 0) -> Dict[str, tuple]:
+    s = {"lnf_g": (d,), "lnf_b": (d,), "w_h": (d, out), "b_h": (out,)}
+    if hidden:
+        s.update({"w_hid": (hidden, d, d), "b_hid": (hidden, d)})
+    return s
 
 
 def _is_ln_gain(name: str) -> bool:
@@ -191,8 +194,8 @@ def embed_params(c: Config) -> Dict[str, np.ndarray]:
     return make_params(c.cfg, "embed", embed_param_shapes(c.V, c.d), c.sigma, c.dtype)
 
 
-def head_params(c: Config) -> Dict[str, np.ndarray]:
-    return make_params(c.cfg, "head", head_param_shapes(c.d, c.out_dim), c.sigma, c.dtype)
+def head_params(c: Config, hidden: int = 0) -> Dict[str, np.ndarray]:
+    return make_params(c.cfg, "head", head_param_shapes(c.d, c.out_dim, hidden), c.sigma, c.dtype)
 
 
 def image(c: Config) -> np.ndarray:

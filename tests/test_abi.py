@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_strings(lib):
-    assert lib.lib.orbit_abi_version() == 1
+    assert lib.lib.orbit_abi_version() == L.ABI_VERSION == 2
     assert lib.lib.orbit_status_string(0) == b"ok"
     assert lib.lib.orbit_status_string(1) == b"invalid argument"
 
@@ -92,8 +92,19 @@ def test_other_entry_validation(lib):
     assert lib.orbit_var_aggregate_saved_bytes(a) == 0
     a = L.AggDesc(1, 4, 5, 256, 32, 8, 1)
     assert lib.orbit_var_aggregate_saved_bytes(a) > 0
-    h = L.HeadDesc(1, 4, 64, 60, 1, 1e-5, 0)  # out not a multiple of 8
+    h = L.HeadDesc(1, 4, 64, 60, 1, 1e-5, 0, 0)  # out not a multiple of 8
     assert lib.orbit_head_saved_bytes(h) == 0
+    h = L.HeadDesc(1, 4, 64, 64, 1, 1e-5, 0, 9)  # more than 8 hidden layers
+    assert lib.orbit_head_saved_bytes(h) == 0 and "hidden" in lib.last_error()
+    # two hidden layers keep their pre-activations and outputs: 4 more [T, d] tensors
+    h0 = L.HeadDesc(1, 4, 64, 64, 1, 1e-5, 0, 0)
+    h2 = L.HeadDesc(1, 4, 64, 64, 1, 1e-5, 0, 2)
+    assert lib.orbit_head_saved_bytes(h2) >= lib.orbit_head_saved_bytes(h0) + 4 * 4 * 64 * 4
+    w = L.WmseDesc(2, 128, 256, 48, 4)
+    assert lib.orbit_wmse_workspace_bytes(w) >= 2 * 2048 * 4
+    assert lib.orbit_wmse_workspace_bytes(L.WmseDesc(2, 130, 256, 48, 4)) == 0 and "multiples" in lib.last_error()
+    assert lib.lib.orbit_wmse_loss(ctypes.byref(L.WmseDesc(2, 128, 256, 48, 3)), 0x100, 0x200, 1.0, 0x300, None,
+                                   0x400, 1 << 20, None) == L.ORBIT_E_UNSUPPORTED
     assert lib.lib.orbit_mse_loss(0x100, 0x200, 0, 1.0, 0x300, None, 0x400, 1024, None) == L.ORBIT_E_ARG
     assert lib.lib.orbit_gemm(1, 16, 16, 16, 0x100, 16, 0, 0x200, 16, 1, 0x300, 16, 1, 1.0, None, 0, None, 0,
                               None) == L.ORBIT_E_UNSUPPORTED

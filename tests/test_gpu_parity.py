@@ -14,11 +14,11 @@ from helpers import TOL, check, dev, host
 pytestmark = pytest.mark.gpu
 
 
-def _dims(c: synth.Config, mode: str):
+def _dims(c: synth.Config, mode: str, head_hidden: int = 0, loss: str = "mse"):
     from paper_2404_14712_amd.model import PassDims
     return PassDims(mode=mode, dtype=c.dtype, B=c.B, L=c.L, d=c.d, blocks=c.blocks, heads=c.heads,
                     head_dim=c.head_dim, mlp=c.mlp, qk_norm=c.qk_norm, eps=c.eps, V=c.V, grid=c.grid,
-                    agg_heads=c.agg_heads, agg_head_dim=c.agg_head_dim)
+                    agg_heads=c.agg_heads, agg_head_dim=c.agg_head_dim, head_hidden=head_hidden, loss=loss)
 
 
 def _dev_params(p: dict, dtype: str):
@@ -291,15 +291,20 @@ def test_vit_block_inference_and_determinism(lib):
 # ---------------------------------------------------------------------------
 # head and loss
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("dtype,B,L,d,out,final_ln", [("f32", 2, 37, 128, 64, 1), ("bf16", 2, 100, 512, 768, 1),
-                                                      ("bf16", 1, 33, 256, 1456, 0)])
-def test_head(lib, dtype, B, L, d, out, final_ln):
+@pytest.mark.parametrize("dtype,B,L,d,out,final_ln,hidden", [
+    ("f32", 2, 37, 128, 64, 1, 0), ("bf16", 2, 100, 512, 768, 1, 0), ("bf16", 1, 33, 256, 1456, 0, 0),
+    # the multi-layer decoder (GELU layers of width d before the last linear map)
+    ("f32", 2, 37, 128, 64, 1, 2), ("bf16", 2, 100, 512, 768, 1, 2), ("bf16", 1, 290, 256, 1456, 0, 1)])
+def test_head(lib, dtype, B, L, d, out, final_ln, hidden):
     import torch
     from paper_2404_14712_amd._lib import HeadDesc
     c = synth.small_config(1, dtype=dtype, B=B, L=L, d=d, V=out // 16, sigma=0.05)
     x = synth.activations(c, "x")
-    prm = synth.head_params(c)
-    desc = HeadDesc(B, L, d, out, final_ln, 1e-5, 1 if dtype == "bf16" else 0)
+    prm = synth.head_params(c, hidden)
+    if hidden:  # hidden-layer weights of the scale that keeps the activations O(1)
+        prm["w_hid"] = synth.normal(c.cfg, "head.w_hid.unit", prm["w_hid"].shape, std=1.0 / np.sqrt(d),
+                                    dtype=dtype)
+    desc = HeadDesc(B, L, d, out, final_ln, 1e-5, 1 if dtype == "bf16" else 0, hidden)
     saved = torch.empty(lib.orbit_head_saved_bytes(desc), dtype=torch.uint8, device="cuda")
     ws = torch.empty(lib.orbit_head_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
     pred = torch.zeros(B, L, out, dtype=torch.float32, device="cuda")
@@ -323,6 +328,29 @@ def test_head(lib, dtype, B, L, d, out, final_ln):
         check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["b_h"])
 
 
+@pytest.mark.parametrize("B,H,W,V", [(2, 32, 64, 4), (4, 128, 256, 48), (1, 8, 4, 1)])
+def test_wmse(lib, B, H, W, V):
+    """Latitude-weighted MSE (Sec. IV) against the oracle's image-layout definition."""
+    import torch
+    from paper_2404_14712_amd._lib import WmseDesc
+    L, n = (H // 4) * (W // 4), V * 16
+    r = np.random.default_rng(H + V)
+    pred = r.standard_normal((B, L, n)).astype(np.float32)
+    tgt = r.standard_normal((B, L, n)).astype(np.float32)
+    desc = WmseDesc(B, H, W, V, 4)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    dpred = torch.zeros(B, L, n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(lib.orbit_wmse_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    lib.orbit_wmse_loss(desc, dev(pred, "f32"), dev(tgt, "f32"), 0.5, loss, dpred, ws)
+    torch.cuda.synchronize()
+    rl, rd = O.wmse(pred, tgt, W // 4, 4, 0.5)
+    from helpers import record
+    le = abs(host(loss)[0] - rl) / rl
+    record("wmse loss", le, 1e-5)
+    assert le <= 1e-5, (host(loss)[0], rl)
+    check("wmse dpred", host(dpred), rd, 1e-5)
+
+
 @pytest.mark.parametrize("n", [1, 1000, 6291456])
 def test_mse(lib, n):
     import torch
@@ -342,23 +370,23 @@ def test_mse(lib, n):
 # ---------------------------------------------------------------------------
 # whole model: the tiny fp32 configuration exactly, and a reduced bf16 one
 # ---------------------------------------------------------------------------
-def _model_inputs(c):
+def _model_inputs(c, head_hidden=0):
     img = synth.image(c)
     tgt = synth.target(c)
     emb = synth.embed_params(c)
     agg = synth.agg_params(c)
     blocks = [synth.block_params(c, i) for i in range(c.blocks)]
-    head = synth.head_params(c)
+    head = synth.head_params(c, head_hidden)
     return img, tgt, emb, agg, blocks, head
 
 
-def _run_model(lib, c, checkpoint=False):
+def _run_model(lib, c, checkpoint=False, head_hidden=0, loss="mse"):
     import torch
     from paper_2404_14712_amd.model import ViTPass
-    img, tgt, emb, agg, blocks, head = _model_inputs(c)
+    img, tgt, emb, agg, blocks, head = _model_inputs(c, head_hidden)
     params = {"embed": _dev_params(emb, c.dtype), "agg": _dev_params(agg, c.dtype),
               "blocks": [_dev_params(b, c.dtype) for b in blocks], "head": _dev_params(head, c.dtype)}
-    vp = ViTPass(lib, _dims(c, "full"), params, checkpoint=checkpoint)
+    vp = ViTPass(lib, _dims(c, "full", head_hidden, loss), params, checkpoint=checkpoint)
     loss = vp.forward_backward({"img": dev(img, "f32"), "tgt": dev(tgt, "f32")})
     torch.cuda.synchronize()
     return vp, loss, (img, tgt, emb, agg, blocks, head)
@@ -369,7 +397,7 @@ def _check_model(vp, loss, inputs, c, tol):
     `tol`. Returns the QK-LayerNorm parameter gradients of blocks after the
     first as (name, gpu, oracle) for check_qkln_depth: see there."""
     img, tgt, emb, agg, blocks, head = inputs
-    kw = dict(p=4, agg_heads=c.agg_heads, heads=c.heads, qk_norm=c.qk_norm, eps=c.eps)
+    kw = dict(p=4, agg_heads=c.agg_heads, heads=c.heads, qk_norm=c.qk_norm, eps=c.eps, loss=vp.z.loss)
     rl, pred, rg = O.model_fwd_bwd(img, tgt, emb, agg, blocks, head, **kw)
     return check_pass(vp, loss, rl, pred, rg, c, tol)
 
@@ -476,6 +504,22 @@ def test_full_model_checkpoint_bitwise(lib):
     for i, gb in enumerate(vp.grads["blocks"]):
         for k in gb:
             assert torch.equal(gb[k], vc.grads["blocks"][i][k]), (i, k)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_full_model_decoder_head_wmse(lib, dtype):
+    """The whole pass with the paper's training loss (latitude-weighted MSE)
+    and a two-layer decoder head: the tiny configuration in fp32, a reduced
+    115M-structure model in bf16 (one block, so no block past the first)."""
+    if dtype == "f32":
+        c = synth.CONFIGS[1]
+    else:
+        c = synth.small_config(2, B=2, L=128, grid=(32, 64), V=12, d=256, blocks=1, heads=4, head_dim=64,
+                               mlp=1024, agg_heads=8, agg_head_dim=32, sigma=0.05)
+    vp, loss, inputs = _run_model(lib, c, head_hidden=2, loss="wmse")
+    assert vp.z.loss == "wmse" and "w_hid" in vp.grads["head"]
+    deferred = _check_model(vp, loss, inputs, c, TOL[dtype])
+    assert not deferred
 
 
 def test_full_model_tiny_fp32(lib):

@@ -542,3 +542,115 @@ def test_store_hook_is_identity_when_exact():
     y2, _ = O.block_fwd(x, prm, 2, store=r)
     e = np.abs(y2 - y0).max() / np.abs(y0).max()
     assert 0 < e < 2e-2
+
+
+# ---------------------------------------------------------------------------
+# latitude-weighted MSE (Sec. IV) and the multi-layer prediction head (Sec. II)
+# ---------------------------------------------------------------------------
+def test_lat_weights_closed_forms():
+    # 2 rows at +-45 degrees: equal weights; 4 rows at +-22.5 / +-67.5 degrees:
+    # cos(67.5) / cos(22.5) = tan(22.5) = sqrt(2) - 1 and a mean of 1 give
+    # weights 2 - sqrt(2) and sqrt(2)
+    assert np.allclose(O.lat_weights(2), [1.0, 1.0], atol=1e-15)
+    r2 = np.sqrt(2.0)
+    assert np.allclose(O.lat_weights(4), [2 - r2, r2, r2, 2 - r2], atol=1e-14)
+    w = O.lat_weights(128)
+    assert abs(w.mean() - 1.0) < 1e-14 and np.allclose(w, w[::-1], atol=1e-14)
+    # sum of cos over equiangular cell centres = 1 / sin(pi / (2H)), so w[y] = cos(lat_y) H sin(pi / (2H))
+    H = 128
+    lat = np.deg2rad(-90 + (np.arange(H) + 0.5) * 180 / H)
+    assert np.allclose(w, np.cos(lat) * H * np.sin(np.pi / (2 * H)), atol=1e-13)
+
+
+def _tok_layout(img, p):
+    B, V = img.shape[:2]
+    return O.patchify(img, p).transpose(0, 2, 1, 3).reshape(B, -1, V * p * p)
+
+
+def test_wmse_layout_roundtrip_and_special_cases():
+    r = np.random.default_rng(7)
+    img = r.standard_normal((2, 3, 8, 12))
+    tok = _tok_layout(img, 4)
+    assert np.array_equal(O.unpatchify(tok, 3, 4), img)
+    tgt = _tok_layout(r.standard_normal((2, 3, 8, 12)), 4)
+    # pred = tgt: zero loss and gradient
+    l0, g0 = O.wmse(tgt, tgt, 3, 4)
+    assert l0 == 0.0 and not g0.any()
+    # a residual constant over the grid: the weights average to 1, so the loss
+    # is the plain MSE (the square of the constant)
+    l1, _ = O.wmse(tgt + 0.5, tgt, 3, 4)
+    assert abs(l1 - 0.25) < 1e-14
+    # a residual on the two equatorial rows only weighs more than one on the
+    # two polar rows (cells shrink towards the poles)
+    eq, po = np.zeros((2, 3, 8, 12)), np.zeros((2, 3, 8, 12))
+    eq[:, :, 3:5] = 1.0
+    po[:, :, [0, 7]] = 1.0
+    le = O.wmse(_tok_layout(eq, 4), 0 * tgt, 3, 4)[0]
+    lp = O.wmse(_tok_layout(po, 4), 0 * tgt, 3, 4)[0]
+    assert le > 4.5 * lp
+
+
+def test_wmse_brute_force():
+    """Scalar loop over the token layout: the row of element (b, l, v*16 + i*4 + j)
+    is (l // Wp) * 4 + i; its weight is cos(latitude) over the mean of cos."""
+    r = np.random.default_rng(8)
+    B, L, V, Wp, p = 1, 6, 2, 3, 4
+    pred = r.standard_normal((B, L, V * p * p))
+    tgt = r.standard_normal((B, L, V * p * p))
+    H = (L // Wp) * p
+    lat = [math.radians(-90 + (y + 0.5) * 180 / H) for y in range(H)]
+    cm = sum(math.cos(a) for a in lat) / H
+    tot, n, g = 0.0, pred.size, np.zeros_like(pred)
+    for l in range(L):
+        for c in range(V * p * p):
+            y = (l // Wp) * p + (c % (p * p)) // p
+            w = math.cos(lat[y]) / cm
+            e = pred[0, l, c] - tgt[0, l, c]
+            tot += w * e * e
+            g[0, l, c] = 2 * w * e / n * 1.5
+    loss, dpred = O.wmse(pred, tgt, Wp, p, scale=1.5)
+    assert abs(loss - tot / n) < 1e-12 and np.allclose(dpred, g, atol=1e-15)
+
+
+def test_fd_wmse():
+    r = np.random.default_rng(9)
+    pred = r.standard_normal((2, 6, 32))
+    tgt = r.standard_normal((2, 6, 32))
+    loss, dpred = O.wmse(pred, tgt, 3, 4)
+    _fd_check(lambda: O.wmse(pred, tgt, 3, 4)[0], {"pred": pred}, {"pred": dpred}, full_max=400)
+
+
+@pytest.mark.parametrize("final_ln", [0, 1])
+def test_fd_decoder_head(final_ln):
+    """The head with two hidden GELU layers (the ClimaX decoder) against finite differences."""
+    r = np.random.default_rng(10)
+    d, n, nh = 8, 12, 2
+    x = r.standard_normal((2, 3, d))
+    prm = _head_prm(d, n)
+    prm["w_hid"] = r.standard_normal((nh, d, d)) * 0.5
+    prm["b_hid"] = r.standard_normal((nh, d)) * 0.3
+    Rw = r.standard_normal((2, 3, n))
+
+    def f():
+        return float((O.head_fwd(x, prm, final_ln)[0] * Rw).sum())
+
+    pred, cache = O.head_fwd(x, prm, final_ln)
+    dx, gr = O.head_bwd(Rw, cache, prm)
+    tensors = {"x": x, **{k: v for k, v in prm.items() if final_ln or not k.startswith("lnf")}}
+    grads = {"x": dx, **{k: gr[k] for k in tensors if k != "x"}}
+    _fd_check(f, tensors, grads, full_max=400)
+
+
+def test_decoder_head_without_hidden_layers_is_the_linear_head():
+    r = np.random.default_rng(11)
+    d, n = 8, 12
+    x = r.standard_normal((2, 3, d))
+    prm = _head_prm(d, n)
+    p0 = dict(prm, w_hid=np.zeros((0, d, d)), b_hid=np.zeros((0, d)))
+    a, ca = O.head_fwd(x, prm, 1)
+    b, cb = O.head_fwd(x, p0, 1)
+    assert np.array_equal(a, b)
+    Rw = r.standard_normal((2, 3, n))
+    ga, gb = O.head_bwd(Rw, ca, prm)[1], O.head_bwd(Rw, cb, p0)[1]
+    for k in ga:
+        assert np.array_equal(ga[k], gb[k]), k

@@ -189,3 +189,56 @@ def test_whole_model_vs_torch():
     assert np.allclose(g["agg"]["q0"], at["q0"].grad.numpy(), atol=1e-12)
     assert np.allclose(g["agg"]["pos"], at["pos"].grad.numpy(), atol=1e-12)
     assert np.allclose(g["agg"]["w_o"], mha.out_proj.weight.grad.numpy().T, atol=1e-12)
+
+
+def test_decoder_head_and_wmse_vs_torch():
+    """The multi-layer prediction head (LayerNorm, two Linear + exact GELU
+    layers, a final Linear; torch.nn modules) and the latitude-weighted MSE
+    (torch's own fold back to the image layout and its cos), with autograd."""
+    B, V, Hg, Wg, p, d, nh = 2, 3, 8, 12, 4, 16, 2
+    Wp = Wg // p
+    L = (Hg // p) * Wp
+    n = V * p * p
+    x = _rand(B, L, d)
+    tgt = _rand(B, L, n)
+    head = {"lnf_g": 1 + _rand(d, s=.3), "lnf_b": _rand(d, s=.3), "w_hid": _rand(nh, d, d, s=.4),
+            "b_hid": _rand(nh, d, s=.3), "w_h": _rand(d, n, s=.3), "b_h": _rand(n, s=.3)}
+    pred, cache = O.head_fwd(x, head, 1)
+    loss, dpred = O.wmse(pred, tgt, Wp, p)
+    dx, g = O.head_bwd(dpred, cache, head)
+
+    xt = _t(x)
+    ln = torch.nn.LayerNorm(d, eps=1e-5, dtype=T64)
+    lins = [torch.nn.Linear(d, d, dtype=T64) for _ in range(nh)]
+    out = torch.nn.Linear(d, n, dtype=T64)
+    with torch.no_grad():
+        ln.weight.copy_(torch.tensor(head["lnf_g"]))
+        ln.bias.copy_(torch.tensor(head["lnf_b"]))
+        for k, lin in enumerate(lins):
+            lin.weight.copy_(torch.tensor(head["w_hid"][k].T))
+            lin.bias.copy_(torch.tensor(head["b_hid"][k]))
+        out.weight.copy_(torch.tensor(head["w_h"].T))
+        out.bias.copy_(torch.tensor(head["b_h"]))
+    h = ln(xt)
+    for lin in lins:
+        h = Fn.gelu(lin(h), approximate="none")
+    pr = out(h)
+    # token layout [B, L, V*p*p] -> image [B, V, H, W] with torch's fold
+    cols = pr.reshape(B, L, V, p * p).permute(0, 2, 3, 1).reshape(B, V * p * p, L)
+    img = Fn.fold(cols, (Hg, Wg), kernel_size=p, stride=p).reshape(B, V, Hg, Wg)
+    tcols = torch.tensor(tgt).reshape(B, L, V, p * p).permute(0, 2, 3, 1).reshape(B, V * p * p, L)
+    timg = Fn.fold(tcols, (Hg, Wg), kernel_size=p, stride=p).reshape(B, V, Hg, Wg)
+    lat = torch.deg2rad(torch.linspace(-90 + 90 / Hg, 90 - 90 / Hg, Hg, dtype=T64))
+    w = torch.cos(lat) / torch.cos(lat).mean()
+    lt = (w[None, None, :, None] * (img - timg) ** 2).mean()
+    lt.backward()
+    assert abs(loss - lt.item()) < 1e-12
+    assert np.allclose(pred, pr.detach().numpy(), atol=1e-12)
+    assert np.allclose(dx, xt.grad.numpy(), atol=1e-12)
+    assert np.allclose(g["lnf_g"], ln.weight.grad.numpy(), atol=1e-12)
+    assert np.allclose(g["lnf_b"], ln.bias.grad.numpy(), atol=1e-12)
+    for k, lin in enumerate(lins):
+        assert np.allclose(g["w_hid"][k], lin.weight.grad.numpy().T, atol=1e-12), k
+        assert np.allclose(g["b_hid"][k], lin.bias.grad.numpy(), atol=1e-12), k
+    assert np.allclose(g["w_h"], out.weight.grad.numpy().T, atol=1e-12)
+    assert np.allclose(g["b_h"], out.bias.grad.numpy(), atol=1e-12)
