@@ -1,7 +1,8 @@
 #!/usr/bin/env python
 """Throughput of the ViT forward+backward pass on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 113b-shard|10b-shard|1b|115m|tiny]
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+                    [--workload 113b-shard|10b-shard|1b|115m|tiny|10b-paper-tp8|113b-paper-tp8]
 
 One step is one pass of the whole path over one batch of synthetic input,
 resident in HBM before the timed region starts:
@@ -9,7 +10,9 @@ resident in HBM before the timed region starts:
   full model (115m, 1b, tiny): patch embedding -> variable aggregation ->
       pre-LN blocks -> head -> MSE loss -> the whole backward;
   10b-shard : 4 blocks of one GPU's tensor-parallel shard, forward + backward;
-  113b-shard: variable aggregation + 2 shard blocks, forward + backward.
+  113b-shard: variable aggregation + 2 shard blocks, forward + backward;
+  10b-paper-tp8, 113b-paper-tp8: shard blocks at the paper's own widths
+      (head_dim 256 and 192), forward + backward.
 
 The default workload is the 113B-scale shard (the largest configuration).
 The same run also times the 10B-scale shard's 4-block stack, and reports
@@ -36,7 +39,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-WORKLOADS = {"115m": 2, "1b": 3, "10b-shard": 4, "113b-shard": 5, "tiny": 1}
+WORKLOADS = {"115m": 2, "1b": 3, "10b-shard": 4, "113b-shard": 5, "tiny": 1, "10b-paper-tp8": 6,
+             "113b-paper-tp8": 7}
 GATE_PCT = 50.0
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3      # MI355X fp32

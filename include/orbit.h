@@ -21,7 +21,8 @@
  *             gradient is float32. In bf16 mode all products accumulate in
  *             float32; LayerNorm statistics, softmax and GELU run in float32.
  * Sizes.      Feature sizes (d, heads*head_dim, mlp, V*patch^2) must be
- *             multiples of 8; head_dim must be 32, 64 or 128; token counts
+ *             multiples of 8; head_dim must be 32, 64 or 128, or in bf16 mode
+ *             also 192 or 256 (the paper's 1B/113B and 10B widths); token counts
  *             (B, L, V) are arbitrary positive integers.
  * Streams.    `stream` is a hipStream_t passed as void* (NULL = the null
  *             stream). Every call only enqueues work on it and returns; results

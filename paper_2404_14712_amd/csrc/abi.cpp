@@ -41,6 +41,14 @@ orbit_status check_dtype(const char* fn, int dt) {
   return ORBIT_OK;
 }
 
+// attention head widths with kernels: 32, 64 and 128 in both dtypes; 192 and
+// 256 (the paper's 1B/113B and 10B head widths) in bf16
+orbit_status head_dim_check(const char* fn, int dt, int dh) {
+  REQ(dh == 32 || dh == 64 || dh == 128 || (dt == ORBIT_BF16 && (dh == 192 || dh == 256)), ORBIT_E_UNSUPPORTED,
+      "%s: head_dim %d unsupported (32, 64, 128; 192 and 256 in bf16)", fn, dh);
+  return ORBIT_OK;
+}
+
 // ---------------------------------------------------------------------------
 // block
 // ---------------------------------------------------------------------------
@@ -59,8 +67,7 @@ orbit_status block_dims(const char* fn, const orbit_block_desc* desc, BlockDims*
   REQ(d.B > 0 && d.L > 0 && d.d > 0 && d.heads > 0 && d.head_dim > 0 && d.mlp > 0, ORBIT_E_ARG,
       "%s: sizes must be positive (B=%d L=%d d=%d heads=%d head_dim=%d mlp=%d)", fn, d.B, d.L, d.d, d.heads,
       d.head_dim, d.mlp);
-  REQ(d.head_dim == 32 || d.head_dim == 64 || d.head_dim == 128, ORBIT_E_UNSUPPORTED,
-      "%s: head_dim %d unsupported (32, 64 or 128)", fn, d.head_dim);
+  ORBIT_TRY(head_dim_check(fn, d.dtype, d.head_dim));
   REQ(d.d % 8 == 0 && d.mlp % 8 == 0, ORBIT_E_ARG, "%s: d=%d and mlp=%d must be multiples of 8", fn, d.d, d.mlp);
   REQ(d.d <= 16384, ORBIT_E_UNSUPPORTED, "%s: d=%d exceeds 16384", fn, d.d);
   REQ(d.qk_norm == 0 || d.qk_norm == 1, ORBIT_E_ARG, "%s: qk_norm must be 0 or 1", fn);
@@ -863,7 +870,7 @@ orbit_status orbit_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const vo
 static orbit_status attn_check(const char* fn, int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t dh) {
   ORBIT_TRY(check_dtype(fn, dtype));
   REQ(B > 0 && H > 0 && L > 0, ORBIT_E_ARG, "%s: sizes must be positive", fn);
-  REQ(dh == 32 || dh == 64 || dh == 128, ORBIT_E_UNSUPPORTED, "%s: head_dim %d unsupported", fn, dh);
+  ORBIT_TRY(head_dim_check(fn, dtype, dh));
   return ORBIT_OK;
 }
 

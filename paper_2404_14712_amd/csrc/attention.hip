@@ -221,7 +221,8 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(FwdArgs a) {
 template <typename T, typename OT, int DH>
 __global__ void __launch_bounds__(256) attn_bwd_pre(const OT* __restrict__ o, int64_t ldo, const T* __restrict__ dO,
                                                     int64_t lddo, float* __restrict__ D, int B, int H, int L) {
-  constexpr int G = DH / 8;
+  // a row's DH / 8 chunks on the next power of two lanes (head_dim 192: 24 of 32)
+  constexpr int CH = DH / 8, G = pow2_ceil(CH);
   const int li = threadIdx.x % G;
   // row (t, h), 32-bit (the host keeps B * L * H below 2^31)
   const unsigned row = blockIdx.x * (256u / G) + threadIdx.x / G;
@@ -229,7 +230,7 @@ __global__ void __launch_bounds__(256) attn_bwd_pre(const OT* __restrict__ o, in
   const unsigned t = valid ? row / (unsigned)H : 0u;
   const int h = (int)(row - t * (unsigned)H);
   float s = 0.f;
-  if (valid) {
+  if (valid && li < CH) {
     float a8[8], b8[8];
     const OT* op = o + (int64_t)t * ldo + h * DH + li * 8;
     const T* dp = dO + (int64_t)t * lddo + h * DH + li * 8;
@@ -1254,7 +1255,7 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
   const int64_t rows = (int64_t)io.B * io.L * io.H;
   KernelInfo kp{sizeof(T) == 2 ? "attn_bwd_pre<bf16>" : "attn_bwd_pre<f32>", 2.0 * rows * DH,
                 rows * DH * (sizeof(T) + (o_f32 ? 4.0 : sizeof(T)))};
-  const dim3 gp((unsigned)cdiv(rows, 256 / (DH / 8)));
+  const dim3 gp((unsigned)cdiv(rows, 256 / pow2_ceil(DH / 8)));
   if (o_f32)
     ORBIT_TRY(launch(kp, attn_bwd_pre<T, float, DH>, gp, dim3(256), 0, s, (const float*)o, ldo, (const T*)dO, lddo,
                      D, io.B, io.H, io.L));
@@ -1321,6 +1322,8 @@ orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, fl
     if (io.dh == 32) AF(bf16, 32);
     if (io.dh == 64) AF(bf16, 64);
     if (io.dh == 128) AF(bf16, 128);
+    if (io.dh == 192) AF(bf16, 192);
+    if (io.dh == 256) AF(bf16, 256);
   } else {
     if (io.dh == 32) AF(float, 32);
     if (io.dh == 64) AF(float, 64);
@@ -1339,6 +1342,8 @@ orbit_status attn_bwd(orbit_dtype dt, const AttnIO& io, const void* o, int64_t l
     if (io.dh == 32) AB(bf16, 32);
     if (io.dh == 64) AB(bf16, 64);
     if (io.dh == 128) AB(bf16, 128);
+    if (io.dh == 192) AB(bf16, 192);
+    if (io.dh == 256) AB(bf16, 256);
   } else {
     if (io.dh == 32) AB(float, 32);
     if (io.dh == 64) AB(float, 64);

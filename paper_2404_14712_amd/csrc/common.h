@@ -174,6 +174,9 @@ bool timing_on();
 void timing_begin(hipStream_t s, const KernelInfo& k);
 void timing_end(hipStream_t s);
 
+// smallest power of two >= n (n >= 1)
+constexpr int pow2_ceil(int n) { return n <= 1 ? 1 : 2 * pow2_ceil((n + 1) / 2); }
+
 #define ORBIT_TRY(expr)                                   \
   do {                                                    \
     orbit_status st__ = (expr);                           \

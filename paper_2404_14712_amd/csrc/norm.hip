@@ -402,8 +402,11 @@ __global__ void __launch_bounds__(256) qkln_fwd_kernel(const T* __restrict__ src
                                                        const T* __restrict__ kg, const T* __restrict__ kb,
                                                        float* mean, float* rstd, int T_, int H, int A,
                                                        float eps) {
-  constexpr int G = DH / 8;
+  // a row's DH / 8 chunks of 8 values on G = the next power of two lanes
+  // (lanes past the last chunk hold zeros; head_dim 192 runs 24 of 32)
+  constexpr int CH = DH / 8, G = pow2_ceil(CH);
   const int li = threadIdx.x % G;
+  const bool lv = li < CH;
   // row (t, j): head slot j < 2H of token t (q heads, then k heads), at
   // column j * DH of the token's [q | k] columns; rows < 2^31 (host check)
   const unsigned row = blockIdx.x * (256u / G) + threadIdx.x / G;
@@ -413,7 +416,7 @@ __global__ void __launch_bounds__(256) qkln_fwd_kernel(const T* __restrict__ src
   const unsigned j = valid ? row - t * nr : 0u;
   const int sidx = (int)j >= H;
   float v[8];
-  if (valid) load8(src + (int64_t)t * lds + j * DH + li * 8, v);
+  if (valid && lv) load8(src + (int64_t)t * lds + j * DH + li * 8, v);
   else
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = 0.f;
@@ -425,11 +428,11 @@ __global__ void __launch_bounds__(256) qkln_fwd_kernel(const T* __restrict__ src
   const float mu = s / (float)DH;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) q += (v[i] - mu) * (v[i] - mu);
+  for (int i = 0; i < 8; ++i) q += lv ? (v[i] - mu) * (v[i] - mu) : 0.f;
 #pragma unroll
   for (int o = G / 2; o >= 1; o >>= 1) q += __shfl_xor(q, o, 64);
   const float r = rsqrtf(q / (float)DH + eps);
-  if (!valid) return;
+  if (!valid || !lv) return;
   float gg[8], bb[8], y[8];
   load8((sidx ? kg : qg) + li * 8, gg);
   load8((sidx ? kb : qb) + li * 8, bb);
@@ -450,18 +453,24 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
                                                        const float* __restrict__ rstd,
                                                        const T* __restrict__ qg, const T* __restrict__ kg,
                                                        int T_, int H, int A, float* __restrict__ part) {
-  constexpr int G = DH / 8;
+  constexpr int CH = DH / 8, G = pow2_ceil(CH);  // as in the forward
   constexpr int NG = 256 / G;  // row groups per block
   __shared__ float sm[NG][4][DH];
   const int li = threadIdx.x % G, grp = threadIdx.x / G;
+  const bool lv = li < CH;
   float ag[2][8], ab[2][8];
 #pragma unroll
   for (int s = 0; s < 2; ++s)
 #pragma unroll
     for (int i = 0; i < 8; ++i) ag[s][i] = ab[s][i] = 0.f;
   float gq[8], gk[8];
-  load8(qg + li * 8, gq);
-  load8(kg + li * 8, gk);
+  if (lv) {
+    load8(qg + li * 8, gq);
+    load8(kg + li * 8, gk);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) gq[i] = gk[i] = 0.f;
+  }
   // rows (t, j) as in the forward; a row group walks rows base, base +
   // stride, ... keeping (t, j) by carries (one division at the start)
   const unsigned nr = 2u * H;
@@ -491,7 +500,7 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
       jc += sj;
       tc += st;
       if (jc >= nr) { jc -= nr; ++tc; }
-      if (valid[u]) {
+      if (valid[u] && lv) {
         load8(d + off_d[u], dy[u]);
         load8(src + off_s, xv[u]);
       } else {
@@ -517,7 +526,7 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
         s1 += __shfl_xor(s1, o, 64);
         s2 += __shfl_xor(s2, o, 64);
       }
-      if (valid[u]) {
+      if (valid[u] && lv) {
         const float m1 = s1 / (float)DH, m2 = s2 / (float)DH;
         float o8[8];
 #pragma unroll
@@ -531,12 +540,14 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
       }
     }
   }
+  if (lv) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    sm[grp][0][li * 8 + i] = ag[0][i];
-    sm[grp][1][li * 8 + i] = ab[0][i];
-    sm[grp][2][li * 8 + i] = ag[1][i];
-    sm[grp][3][li * 8 + i] = ab[1][i];
+    for (int i = 0; i < 8; ++i) {
+      sm[grp][0][li * 8 + i] = ag[0][i];
+      sm[grp][1][li * 8 + i] = ab[0][i];
+      sm[grp][2][li * 8 + i] = ag[1][i];
+      sm[grp][3][li * 8 + i] = ab[1][i];
+    }
   }
   __syncthreads();
   for (int e = threadIdx.x; e < 4 * DH; e += 256) {
@@ -633,7 +644,7 @@ template <typename T, int DH>
 orbit_status qk_fwd_t(const void* src, int64_t lds, void* dst, int64_t ldd, const void* qg, const void* qb,
                       const void* kg, const void* kb, float* mean, float* rstd, int T_, int H, float eps,
                       hipStream_t s) {
-  constexpr int G = DH / 8;
+  constexpr int G = pow2_ceil(DH / 8);
   const int64_t rows = (int64_t)T_ * 2 * H;
   KernelInfo ki{sizeof(T) == 2 ? "qkln_fwd_kernel<bf16>" : "qkln_fwd_kernel<f32>", 8.0 * rows * DH,
                 2.0 * rows * DH * sizeof(T)};
@@ -647,7 +658,7 @@ orbit_status qk_bwd_t(void* d, int64_t ldd, const void* src, int64_t lds, const 
                       const void* qg, const void* kg, float* dqg, float* dqb, float* dkg, float* dkb,
                       int accumulate, int T_, int H, void* ws, ColFinal* fin, hipStream_t s) {
   const int64_t rows = (int64_t)T_ * 2 * H;
-  const int blocks = (int)std::min<int64_t>(kQkBwdBlocks, cdiv(rows, 256 / (DH / 8)));
+  const int blocks = (int)std::min<int64_t>(kQkBwdBlocks, cdiv(rows, 256 / pow2_ceil(DH / 8)));
   float* part = static_cast<float*>(ws);
   KernelInfo ki{sizeof(T) == 2 ? "qkln_bwd_kernel<bf16>" : "qkln_bwd_kernel<f32>", 12.0 * rows * DH,
                 3.0 * rows * DH * sizeof(T)};
@@ -808,6 +819,8 @@ orbit_status qk_norm_fwd(orbit_dtype dt, const void* src, int64_t lds, void* dst
     if (dh == 32) QKF(bf16, 32);
     if (dh == 64) QKF(bf16, 64);
     if (dh == 128) QKF(bf16, 128);
+    if (dh == 192) QKF(bf16, 192);
+    if (dh == 256) QKF(bf16, 256);
   } else {
     if (dh == 32) QKF(float, 32);
     if (dh == 64) QKF(float, 64);
@@ -834,6 +847,8 @@ orbit_status qk_norm_bwd(orbit_dtype dt, void* d, int64_t ldd, const void* src, 
     if (dh == 32) QKB(bf16, 32);
     if (dh == 64) QKB(bf16, 64);
     if (dh == 128) QKB(bf16, 128);
+    if (dh == 192) QKB(bf16, 192);
+    if (dh == 256) QKB(bf16, 256);
   } else {
     if (dh == 32) QKB(float, 32);
     if (dh == 64) QKB(float, 64);

@@ -83,6 +83,13 @@ CONFIGS: Dict[int, Config] = {
     5: Config(5, "113B-scale tensor-parallel shard (d=16384, TP 16), aggregation + 2 blocks",
               "bf16", B=1, L=2048, d=16384, blocks=2, heads=8, head_dim=128, mlp=4096,
               sigma=0.005, V=91, agg_heads=8, agg_head_dim=128, agg_only_prefix=True),
+    # the paper's own widths (Sec. IV) under tensor parallelism over the 8 GPUs
+    # of a node (the paper's best 113B layout, Sec. V-C, is FSDP x TP 8)
+    6: Config(6, "10B model's tensor-parallel shard at the paper's widths (d=8192, 4 of 32 heads of 256, TP 8), "
+                 "4 blocks", "bf16", B=2, L=2048, d=8192, blocks=4, heads=4, head_dim=256, mlp=4096, sigma=0.01),
+    7: Config(7, "113B model's tensor-parallel shard at the paper's widths (d=12288, 8 of 64 heads of 192, TP 8), "
+                 "2 blocks", "bf16", B=1, L=2048, d=12288, blocks=2, heads=8, head_dim=192, mlp=6144,
+              sigma=0.005),
 }
 
 

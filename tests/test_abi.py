@@ -51,6 +51,11 @@ def test_size_queries_are_deterministic_and_reject_bad_descs(lib):
     assert lib.orbit_vit_block_workspace_bytes(d) > 0
     assert lib.orbit_vit_block_saved_bytes(_bdesc(head_dim=48)) == 0
     assert "head_dim" in lib.last_error()
+    # the paper's head widths 192 and 256 run in bf16 only
+    assert lib.orbit_vit_block_saved_bytes(_bdesc(heads=2, head_dim=192, d=384, dtype=1)) > 0
+    assert lib.orbit_vit_block_saved_bytes(_bdesc(heads=2, head_dim=256, d=512, dtype=1)) > 0
+    assert lib.orbit_vit_block_saved_bytes(_bdesc(heads=2, head_dim=192, d=384, dtype=0)) == 0
+    assert "head_dim 192" in lib.last_error()
     assert lib.orbit_vit_block_saved_bytes(_bdesc(d=100)) == 0
     assert lib.orbit_vit_block_saved_bytes(_bdesc(dtype=7)) == 0
     assert lib.orbit_vit_block_saved_bytes(_bdesc(L=0)) == 0

@@ -78,6 +78,49 @@ def test_block_full_size(lib, cfg, keep):
 
 
 # ---------------------------------------------------------------------------
+# the paper's own model shapes (Sec. IV): the 1B model (3072 wide, 16 heads of
+# 192, unsharded), the 10B model's tensor-parallel shard over 8 GPUs (8192
+# wide, 4 of 32 heads of 256, MLP 4096 of 32768) and the 113B model's (12288
+# wide, 8 of 64 heads of 192, MLP 6144 of 49152): one block of 2048 tokens
+# ---------------------------------------------------------------------------
+PAPER_SHAPES = {
+    "1b-paper": dict(d=3072, heads=16, head_dim=192, mlp=12288, sigma=0.02),
+    "10b-paper-tp8": dict(d=8192, heads=4, head_dim=256, mlp=4096, sigma=0.01),
+    "113b-paper-tp8": dict(d=12288, heads=8, head_dim=192, mlp=6144, sigma=0.005),
+}
+
+
+@pytest.mark.parametrize("name", list(PAPER_SHAPES))
+def test_block_paper_shapes(lib, name):
+    import torch
+    from paper_2404_14712_amd._lib import BlockDesc
+    c = synth.small_config(4, B=1, L=2048, **PAPER_SHAPES[name])
+    x = synth.activations(c, "x")
+    dy = synth.normal(c.cfg, "dy", x.shape, dtype=c.dtype)
+    prm = synth.block_params(c, 0)
+    desc = BlockDesc(c.B, c.L, c.d, c.heads, c.head_dim, c.mlp, c.qk_norm, c.eps, 1)
+    saved = torch.empty(lib.orbit_vit_block_saved_bytes(desc), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(lib.orbit_vit_block_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    pd = _dev_params(prm, c.dtype)
+    xd = dev(x, c.dtype)
+    y = torch.empty_like(xd)
+    dx = torch.empty_like(xd)
+    g = {k: torch.full(v.shape, 5.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
+    print(f"{name}: block d={c.d} heads={c.heads}x{c.head_dim} mlp={c.mlp} L={c.L}", flush=True)
+    lib.orbit_vit_block_fwd(desc, pd, xd, y, saved, ws)
+    lib.orbit_vit_block_bwd(desc, pd, xd, saved, dev(dy, c.dtype), dx, g, 0, ws)
+    torch.cuda.synchronize()
+    ref, cache = O.block_fwd(x, prm, c.heads, c.qk_norm, c.eps)
+    rdx, rg = O.block_bwd(dy, cache, prm)
+    del cache
+    tol = TOL[c.dtype]
+    check("y", host(y), ref, tol)
+    check("dx", host(dx), rdx, tol)
+    for k in rg:
+        check(f"d{k}", host(g[k]), rg[k], tol, floor_ref=rg["ln1_b"])
+
+
+# ---------------------------------------------------------------------------
 # aggregation: 115M (V=48), 1B (V=91), 113B shard (V=91, d=16384, 8 of 128 heads)
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("cfg,per_batch", [(2, 8), (3, 8), (5, 12)], ids=["115m", "1b", "113b-shard"])

@@ -92,6 +92,14 @@ def test_attention_wide_logits(lib, dtype, dh):
     _attention_case(lib, dtype, dh, 300, 2.0)
 
 
+@pytest.mark.parametrize("dh", [192, 256])
+@pytest.mark.parametrize("L", [1, 37, 300])
+def test_attention_wide_heads(lib, dh, L):
+    """The paper's head widths: 192 (1B: 3072 / 16 heads; 113B: 12288 / 64)
+    and 256 (10B: 8192 / 32), bf16."""
+    _attention_case(lib, "bf16", dh, L, 1.0)
+
+
 def _attention_case(lib, dtype, dh, L, qk_scale):
     import torch
     B, H = 2, 3

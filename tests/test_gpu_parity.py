@@ -186,6 +186,10 @@ BLOCK_CASES = [
     ("bf16", 2, 256, 512, 4, 64, 1024, 1),
     ("bf16", 1, 2048, 256, 4, 64, 512, 0),
     ("bf16", 1, 1024, 264, 2, 64, 520, 1),    # ragged column tiles of the bias sums
+    # the paper's head widths (bf16): 192 and 256, ragged token counts
+    ("bf16", 1, 130, 512, 2, 192, 512, 1),
+    ("bf16", 2, 70, 512, 2, 256, 1032, 1),
+    ("bf16", 1, 300, 768, 4, 192, 512, 0),
 ]
 
 
