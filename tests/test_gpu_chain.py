@@ -5,15 +5,15 @@ oracle run the same way.
 * 115M-scale model: patch embedding, aggregation over 48 variables, 8 blocks,
   head and loss, on one sample of the full 128x256 grid (2048 patches).
 * 1B-scale model: 91 variables with per-variable scales, 16 blocks of width
-  2048, on one sample of a 64x128 grid (512 patches; the fp64 oracle of the
-  full 2048-patch grid takes minutes per pass).
+  2048, on one sample of the full 128x256 grid (2048 patches).
 * 10B-scale shard: 4 chained shard blocks on the full batch of 2 x 2048
   tokens, the upstream gradient nonzero on the first sample only (samples are
   independent, so the oracle runs that sample and the other's input gradient
   must be exactly zero).
 * 113B-scale shard: aggregation over 91 variables at width 16384 followed by 2
-  shard blocks, on 256 of the 2048 patches (the oracle's unfolded key/value
-  projections cost 2 x 256 x 91 x 16384 x 1024 flops each at this size).
+  shard blocks, on 512 of the 2048 patches (the oracle's unfolded key/value
+  projections cost 2 x 512 x 91 x 16384 x 1024 flops each at this size, and
+  its float64 copy of the token tensor takes 5.6 GB).
 
 Every tensor is held to the bf16 bound 2e-2, except the query/key LayerNorm
 parameter gradients of the blocks after the first, whose bf16 storage floor is
@@ -143,9 +143,9 @@ def _shard_chain(lib, key, c, keep=(0,)):
 
 CHAINS = {
     "115m": lambda lib: _full_model(lib, "115m", synth.small_config(2, B=1)),
-    "1b": lambda lib: _full_model(lib, "1b", synth.small_config(3, B=1, grid=(64, 128), L=512)),
+    "1b": lambda lib: _full_model(lib, "1b", synth.small_config(3, B=1)),
     "10b-shard": lambda lib: _shard_chain(lib, "10b-shard", synth.CONFIGS[4]),
-    "113b-shard": lambda lib: _shard_chain(lib, "113b-shard", synth.small_config(5, L=256)),
+    "113b-shard": lambda lib: _shard_chain(lib, "113b-shard", synth.small_config(5, L=512)),
 }
 
 
