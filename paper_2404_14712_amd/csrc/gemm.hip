@@ -695,8 +695,6 @@ struct TileCfg {
 constexpr TileCfg kDma{DmaBig::BM, DmaBig::BN, DmaBig::WM, DmaBig::WN, true};
 constexpr TileCfg kDmaHalf{DmaHalf::BM, DmaHalf::BN, DmaHalf::WM, DmaHalf::WN, true};
 constexpr TileCfg kT256{256, 256, 2, 4};
-constexpr TileCfg kT256x128{256, 128, 4, 2};
-constexpr TileCfg kT128x256{128, 256, 2, 4};
 constexpr TileCfg kBig{128, 128, 2, 2};
 constexpr TileCfg kNarrowN{128, 32, 4, 1};
 constexpr TileCfg kNarrowM{32, 128, 1, 4};
@@ -716,25 +714,28 @@ bool dma_ok(const Gemm& g) {
          al16(g.A) && al16(g.B);
 }
 
-// bf16 products: the (tile, split) pair with the least modelled time, from
-// throughputs measured on MI355X per operand layout (forward: A K-major, B
-// N-major; input gradient: both K-major; weight gradient: A M-major, B
-// N-major). A work item (tile x K-slice) costs its K-steps plus ~4 K-steps of
-// prologue/epilogue at the tile's per-CU rate; the busiest CU runs
-// ceil(items / 256) of them. Tiles that run two blocks per CU reach their rate
-// only with both resident (55-67% of it alone). A split adds its float32 partials,
-// written and read back mostly through the L2/MALL, and the reduction launch.
+// bf16 products: the (tile, split) pair with the least modelled time. The
+// model was fitted (least squares on log time) to every tile and split on the
+// block products of five model sizes, measured on MI355X. A launch runs in
+// rounds of `slots` concurrent work items (tile x K range; one 256x256 DMA
+// block per CU, two of the smaller tiles); a round of ks 64-deep K steps takes
+// c + r * ks microseconds with every CU busy, r depending on the operand
+// layout (forward: A K-major, B N-major; input gradient: both K-major; weight
+// gradient: A M-major, B N-major). The last round, with a fraction f of the
+// slots filled, runs faster by 1 + beta (1 - f), up to `cap`: the chip is
+// power-limited, and with fewer CUs busy they clock higher and share the
+// memory system among fewer (a 144-tile launch on 256 CUs reaches 85% of the
+// full-chip rate). A split adds its float32 partials, written and read back,
+// at 0.29 us per MB.
 struct Choice { TileCfg t; int splits; };
 
 Choice pick_bf16(const Gemm& g) {
-  // TFLOP/s per layout; blocks per CU; fraction of the rate with one block per CU
-  struct Cand { TileCfg t; double fwd, dx, dw; int slots; double eff1; };
-  const Cand cands[] = {{kDma, 1250.0, 1053.0, 1290.0, 1, 1.0},
-                        {kDmaHalf, 1070.0, 1030.0, 1197.0, 2, 0.87},
-                        {kT256, 1000.0, 1050.0, 960.0, 1, 1.0},
-                        {kT256x128, 820.0, 830.0, 790.0, 1, 1.0},
-                        {kT128x256, 800.0, 860.0, 755.0, 1, 1.0},
-                        {kBig, 790.0, 900.0, 785.0, 2, 0.55}};
+  struct Cand { TileCfg t; int slots; double c, fwd, dx, dw, beta, cap; };
+  const Cand cands[] = {{kDma, 256, 11.38, 1.540, 1.610, 1.683, 0.85, 1.562},
+                        {kDmaHalf, 512, 8.41, 1.951, 1.906, 1.995, 1.343, 2.093},
+                        {kT256, 256, 9.97, 2.083, 1.986, 2.166, 0.239, 1.114},
+                        {kBig, 512, 5.47, 1.367, 1.197, 1.394, 0.60, 1.425}};
+  constexpr double kSplitUsPerMB = 0.2922;
   const bool dma = dma_ok(g);
   Choice best{kBig, 1};
   double best_us = 1e300;
@@ -742,23 +743,18 @@ Choice pick_bf16(const Gemm& g) {
     if (g.M < c.t.BM || g.N < c.t.BN) continue;
     if (c.t.dma && !dma) continue;
     const double rate = g.a_kmajor ? (g.b_kmajor ? c.dx : c.fwd) : c.dw;
-    const double cu_flops_per_us = rate * 1e12 / 256.0 * 1e-6;
-    const double kstep_flops = 2.0 * c.t.BM * c.t.BN * 64.0;
     const int64_t tiles = tiles_of(g, c.t);
     const int64_t ksteps = cdiv(g.K, 64);
     for (int sp = 1; sp <= 16; sp *= 2) {
       if (sp > 1 && (ksteps / sp < 8 || tiles * sp > 2048)) break;
       const int64_t items = tiles * sp;
       const int64_t ks = cdiv(cdiv(g.K, sp), 64);
-      int64_t n = cdiv(items, 256);
-      double eff = 1.0;
-      if (c.slots == 2) {
-        if (n == 1) eff = c.eff1;
-        else n = 2 * cdiv(items, 512);
-      }
-      double us = (double)n * (double)(ks + 4) * kstep_flops / (cu_flops_per_us * eff);
-      if (sp > 1) us += (double)sp * g.M * g.N * g.batch * 8.0 / 8.0e12 * 1e6 + 3.0;
-      if (us < best_us * 0.98) {
+      const int64_t n = cdiv(items, c.slots);
+      const double f = (double)(items - (n - 1) * c.slots) / c.slots;
+      const double boost = std::min(c.cap, 1.0 + c.beta * (1.0 - f));
+      double us = ((double)(n - 1) + 1.0 / boost) * (c.c + rate * (double)ks);
+      if (sp > 1) us += kSplitUsPerMB * sp * (double)g.M * g.N * g.batch * 4.0 / 1e6;
+      if (us < best_us) {
         best_us = us;
         best = {c.t, sp};
       }
@@ -885,8 +881,6 @@ orbit_status run_layout(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream
     }
     if (t.BM == 256 && t.BN == 256 && t.WM == 2) return run_cfg<T, OutT, 256, 256, 2, 4, AK, BKM>(g, a, s);
     if (t.BM == 256 && t.BN == 256 && t.WM == 4) return run_cfg<T, OutT, 256, 256, 4, 2, AK, BKM>(g, a, s);
-    if (t.BM == 256 && t.BN == 128) return run_cfg<T, OutT, 256, 128, 4, 2, AK, BKM>(g, a, s);
-    if (t.BM == 128 && t.BN == 256) return run_cfg<T, OutT, 128, 256, 2, 4, AK, BKM>(g, a, s);
   }
   if (t.BM == 128 && t.BN == 128) return run_cfg<T, OutT, 128, 128, 2, 2, AK, BKM>(g, a, s);
   if (t.BM == 128 && t.BN == 32) return run_cfg<T, OutT, 128, 32, 4, 1, AK, BKM>(g, a, s);
