@@ -312,6 +312,34 @@ def _rate(flops, ms, peak):
     return {"ms": round(ms, 4), "tflops": round(tf, 2), "pct_peak": round(100 * tf / peak, 2)}
 
 
+def mfma_peak(lib, device, blocks: int = 2048, iters: int = 2048, reps: int = 7) -> dict:
+    """Sustained bf16 matrix-core rate of this GPU, from the library's probe
+    kernel (8 independent 32x32x16 products in flight per wave, 8 blocks of 4
+    waves per CU), and the clock that rate implies at full issue."""
+    import torch
+
+    out = torch.empty(blocks * 4, dtype=torch.float32, device=device)
+    for _ in range(2):
+        lib.orbit_mfma_probe(blocks, iters, 1.0, out)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for i in range(reps):
+        lib.orbit_mfma_probe(blocks, iters, 1.0, out)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(reps))[reps // 2]
+    # every accumulator element ends at 16 iters (operands 1.0); each wave sums 8
+    assert bool((out == 128.0 * iters).all()), "matrix-core probe returned wrong values"
+    flops = blocks * 4.0 * iters * 8 * 32 * 32 * 16 * 2
+    tf = flops / (ms * 1e-3) / 1e12
+    # 256 CUs x 4 SIMDs x 1024 bf16 flop per clock per SIMD
+    return {"tflops": round(tf, 1), "pct_of_spec": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+            "implied_clock_ghz": round(tf * 1e12 / (256 * 4 * 1024) / 1e9, 3), "launch_ms": round(ms, 4),
+            "flops_per_launch": flops,
+            "kernel": f"{blocks} blocks x 4 waves, 8 independent bf16 32x32x16 products per wave, {iters} rounds"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -398,6 +426,9 @@ def main():
                  "algorithmic_bytes_per_launch": k_bytes})
     breakdown = sorted(((n, v["ms"]) for n, v in tot.items()), key=lambda t: -t[1])[:8]
     blocks = _rate(flops["blocks"], r["blocks_ms"], peak)
+    probe = mfma_peak(lib, dev) if c.dtype == "bf16" else None
+    if probe:
+        blocks["pct_measured_peak"] = round(100 * blocks["tflops"] / probe["tflops"], 2)
     blocks["note"] = ("transformer blocks only (forward + backward), one untimed step with events at the "
                       "block-stack boundaries")
     out = {
@@ -415,6 +446,8 @@ def main():
         "data": "synthetic (seeded N(0,1) fields and N(0,sigma) weights)",
         "config": describe(c),
         "pct_peak": round(100 * tflops / peak, 2),
+        "pct_measured_peak": round(100 * tflops / probe["tflops"], 2) if probe else None,
+        "mfma_peak_measured": probe,
         "samples_per_s": round(c.B / (ms * 1e-3), 2),
         "tokens_per_s": round(c.B * c.L / (ms * 1e-3), 1),
         "flops_per_step": flops,
@@ -451,6 +484,10 @@ def main():
             base_ms = r4["ms_median"]
         else:
             base_ms = r["ms_median"]
+        if probe:
+            for k, v in gate.items():
+                if isinstance(v, dict):
+                    v["pct_measured_peak"] = round(100 * v["tflops"] / probe["tflops"], 2)
         out["gate"] = gate
         rc = measure(lib, c4, a.steps, a.warmup, dev, checkpoint=True, instrument=False)
         out["checkpoint"] = {"workload": "10b-shard (4 blocks)", "ms": round(rc["ms_median"], 4),

@@ -340,6 +340,18 @@ orbit_status orbit_timing_summary(const char* prefix, int64_t* launches, double*
 /* Name of the i-th distinct kernel recorded (NULL past the end). */
 const char* orbit_timing_kernel_name(int i);
 
+/* Matrix-core throughput probe, for measuring the sustained bf16 peak and
+ * clock of the GPU the library runs on (not a step of the model). Launches
+ * `blocks` blocks of 4 waves; each wave keeps 8 independent bf16 32x32x16
+ * matrix products in flight for `iters` rounds, which is
+ * blocks * 4 * iters * 8 * 32768 flops; the caller times the launch on
+ * `stream`. Every operand element is bf16(x), so each accumulator element
+ * ends at 16 x^2 iters; out (device, float32, blocks * 4 elements, caller
+ * owned) receives per wave the sum of one element of each of its 8
+ * accumulators, 128 x^2 iters. blocks in [1, 2^20], iters in [1, 2^20];
+ * otherwise ORBIT_E_ARG. */
+orbit_status orbit_mfma_probe(int32_t blocks, int32_t iters, float x, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -125,6 +125,7 @@ _PROTOS = {
     "orbit_timing_summary": (c_int, [c_char_p, POINTER(c_int64), POINTER(c_double), POINTER(c_double),
                                      POINTER(c_double)]),
     "orbit_timing_kernel_name": (c_char_p, [c_int]),
+    "orbit_mfma_probe": (c_int, [c_int32, c_int32, c_float, P, P]),
 }
 
 EXPORTS = tuple(_PROTOS)
@@ -306,6 +307,11 @@ class OrbitLib:
         self._check("orbit_layernorm_fwd", self.lib.orbit_layernorm_fwd(
             dtype, rows, n, _ptr(x), _ptr(g), _ptr(b), float(eps), _ptr(y), _ptr(mean), _ptr(rstd),
             _stream(stream)))
+
+    # -- measurement aid -------------------------------------------------------
+    def orbit_mfma_probe(self, blocks, iters, x, out, stream=None):
+        self._check("orbit_mfma_probe", self.lib.orbit_mfma_probe(int(blocks), int(iters), float(x), _ptr(out),
+                                                                  _stream(stream)))
 
     # -- timing ----------------------------------------------------------------
     def orbit_timing_enable(self, on: bool):

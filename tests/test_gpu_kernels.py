@@ -165,3 +165,15 @@ def test_layernorm(lib, dtype, rows, n):
     check("ln y", host(y), ref, TOL[dtype])
     check("ln rstd", host(rstd), r[:, 0], 1e-4)
     check("ln mean", host(mean), x.astype(np.float64).mean(-1), 1e-4)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("blocks,iters,x", [(1, 1, 1.0), (256, 64, 1.0), (37, 1000, 0.5), (1024, 3, -2.0)])
+def test_mfma_probe(lib, blocks, iters, x):
+    """The matrix-core probe computes what its contract states: each wave's
+    value is 8 accumulator elements of 16 x^2 per round, exact in float32."""
+    import torch
+    out = torch.full((blocks * 4,), float("nan"), dtype=torch.float32, device="cuda")
+    lib.orbit_mfma_probe(blocks, iters, x, out)
+    torch.cuda.synchronize()
+    assert bool((out == 128.0 * x * x * iters).all())
