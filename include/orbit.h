@@ -161,7 +161,8 @@ orbit_status orbit_patch_embed_bwd(const orbit_embed_desc* desc, const float* im
  * with the W_o row-shard output left unreduced). The library evaluates the
  * exact algebraic refolding (query through W_k, weights applied before W_v),
  * which has the same value. heads must divide 64 and be a multiple of 8
- * (bf16) or 4 (float32); otherwise ORBIT_E_UNSUPPORTED. */
+ * (bf16) or 4 (float32), and head_dim at most 8192; otherwise
+ * ORBIT_E_UNSUPPORTED. d and head_dim must be multiples of 8 (ORBIT_E_ARG). */
 typedef struct {
   int32_t B, L, V, d, heads, head_dim;
   int32_t dtype;

@@ -522,6 +522,7 @@ static orbit_status agg_check(const char* fn, const orbit_agg_desc* d) {
   REQ(d->B > 0 && d->L > 0 && d->V > 0 && d->d > 0 && d->heads > 0 && d->head_dim > 0, ORBIT_E_ARG,
       "%s: sizes must be positive", fn);
   REQ(d->d % 8 == 0 && d->head_dim % 8 == 0, ORBIT_E_ARG, "%s: d and head_dim must be multiples of 8", fn);
+  REQ(d->head_dim <= 8192, ORBIT_E_UNSUPPORTED, "%s: head_dim=%d above 8192", fn, d->head_dim);
   // per-token rows of `heads` values are read as 16-byte vectors
   REQ((d->heads * (int)esz(d->dtype)) % 16 == 0, ORBIT_E_UNSUPPORTED,
       "%s: heads=%d must be a multiple of %d for this dtype", fn, d->heads, 16 / (int)esz(d->dtype));

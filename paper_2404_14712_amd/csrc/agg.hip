@@ -20,68 +20,142 @@
 namespace orbit {
 namespace {
 
+// 8 consecutive elements (16-byte aligned) widened to float
+ORBIT_DEV void agg_ld8(const bf16* p, float* f) {
+  const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) f[u] = (float)v[u];
+}
+ORBIT_DEV void agg_ld8(const float* p, float* f) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) { f[u] = a[u]; f[4 + u] = b[u]; }
+}
+
 // Weighted column sums out[j] = sum_i c_ij W[i][j] over the d rows of a [d, A]
 // weight, with c_ij = x[i] (query projection) or dU[i][j / dh] (query
-// gradient). Phase 1: one block per slice of kGvRows rows, threads along the
-// columns (coalesced row reads), one float32 partial per (slice, column);
-// phase 2 sums the slices in order (deterministic).
+// gradient). Phase 1: one block per slice of kGvRows rows; a thread takes 8
+// consecutive columns (16-byte row reads). When a row has fewer than 2048
+// columns the block's threads form several row groups that take alternate
+// rows of the slice and add their sums through LDS in a fixed order; one
+// float32 partial per (slice, column). Phase 2 sums the slices in order
+// (deterministic).
 constexpr int kGvRows = 64;
 
 template <typename T, bool DQ>
 __global__ void __launch_bounds__(256) agg_gemv_part(const T* __restrict__ W, const T* __restrict__ x,
                                                      const float* __restrict__ dU, float* __restrict__ part, int d,
                                                      int A, int H, int dh) {
+  __shared__ float red[256 * 8];
+  const int cg = A / 8;                      // column groups of 8
+  const int rg = cg >= 256 ? 1 : 256 / cg;   // row groups
   const int i0 = blockIdx.x * kGvRows, i1 = min(d, i0 + kGvRows);
-  for (int j = threadIdx.x; j < A; j += 256) {
-    const int h = j / dh;
-    float s = 0.f;
-    int i = i0;
-    for (; i + 8 <= i1; i += 8) {
-      float w[8], c[8];
+  const int t = threadIdx.x;
+  const int r = rg == 1 ? 0 : t / cg;
+  for (int base = 0; base < cg; base += 256) {
+    const int g = rg == 1 ? base + t : t % cg;
+    const bool act = g < cg && r < rg;
+    float acc[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        w[u] = to_f(W[(int64_t)(i + u) * A + j]);
-        c[u] = DQ ? dU[(int64_t)(i + u) * H + h] : to_f(x[i + u]);
+    for (int u = 0; u < 8; ++u) acc[u] = 0.f;
+    if (act) {
+      const int j = g * 8, h = j / dh;
+      int i = i0 + r;
+      // 8 rows' loads in flight at a time
+      for (; i + 7 * rg < i1; i += 8 * rg) {
+        float w[8][8], c[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          agg_ld8(W + (int64_t)(i + k * rg) * A + j, w[k]);
+          c[k] = DQ ? dU[(int64_t)(i + k * rg) * H + h] : to_f(x[i + k * rg]);
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) acc[u] += c[k] * w[k][u];
       }
+      for (; i < i1; i += rg) {
+        float w[8];
+        agg_ld8(W + (int64_t)i * A + j, w);
+        const float c = DQ ? dU[(int64_t)i * H + h] : to_f(x[i]);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s += c[u] * w[u];
+        for (int u = 0; u < 8; ++u) acc[u] += c * w[u];
+      }
     }
-    for (; i < i1; ++i) s += (DQ ? dU[(int64_t)i * H + h] : to_f(x[i])) * to_f(W[(int64_t)i * A + j]);
-    part[(int64_t)blockIdx.x * A + j] = s;
+    if (rg > 1) {
+      // one pass only (cg < 256): row groups 1.. hand their sums to group 0
+      if (act && r > 0)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) red[(r * cg + g) * 8 + u] = acc[u];
+      __syncthreads();
+      if (act && r == 0)
+        for (int rr = 1; rr < rg; ++rr)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) acc[u] += red[(rr * cg + g) * 8 + u];
+    }
+    if (act && r == 0) {
+      float* o = part + (int64_t)blockIdx.x * A + g * 8;
+      *reinterpret_cast<f32x4*>(o) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+      *reinterpret_cast<f32x4*>(o + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+    }
   }
 }
 
-// out[j] = sum over slices of part[slice][j] (+ bias[j])
+// out[j] = sum over slices of part[slice][j] (+ bias[j]): a block takes 16
+// columns; its 16 thread groups sum every 16th slice, and the 16 group sums
+// are added in order (deterministic)
 template <typename T>
 __global__ void __launch_bounds__(256) agg_gemv_final(const float* __restrict__ part, int slices, int A,
                                                       const T* __restrict__ bias, float* __restrict__ out) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= A) return;
+  __shared__ float red[16][17];
+  const int c = threadIdx.x & 15, sg = threadIdx.x >> 4;
+  const int j = blockIdx.x * 16 + c;
   float s = 0.f;
-  int k = 0;
-  for (; k + 16 <= slices; k += 16) {
-    float v[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) v[u] = part[(int64_t)(k + u) * A + j];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) s += v[u];
+  if (j < A)
+    for (int k = sg; k < slices; k += 16) s += part[(int64_t)k * A + j];
+  red[sg][c] = s;
+  __syncthreads();
+  if (sg == 0 && j < A) {
+    float t = 0.f;
+    for (int g = 0; g < 16; ++g) t += red[g][c];
+    out[j] = bias ? t + to_f(bias[j]) : t;
   }
-  for (; k < slices; ++k) s += part[(int64_t)k * A + j];
-  out[j] = bias ? s + to_f(bias[j]) : s;
 }
 
-// Ut[h][i] = sum_c w_k[i][h*dh + c] q[h*dh + c]   (one wave per (i, 8 heads))
+// Ut[h][i] = sum_c w_k[i][h*dh + c] q[h*dh + c]. One wave per row i: each
+// lane forms the dot products of 8-column chunks (16-byte reads of the row),
+// and lane h adds the dh / 8 chunks of head h in order. A row is taken in
+// passes of whole heads, at most kFoldMaxChunks chunks each.
+constexpr int kFoldMaxChunks = 1024;
 template <typename T>
 __global__ void __launch_bounds__(256) agg_fold_key(const T* __restrict__ wk, const float* __restrict__ q,
                                                     T* __restrict__ Ut, int d, int H, int dh) {
-  const int A = H * dh;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over d * H
-  if (idx >= (int64_t)d * H) return;
-  const int i = (int)(idx / H), h = (int)(idx % H);
-  const T* row = wk + (int64_t)i * A + h * dh;
-  float s = 0.f;
-  for (int c = 0; c < dh; ++c) s += to_f(row[c]) * q[h * dh + c];
-  Ut[(int64_t)h * d + i] = from_f<T>(s);
+  __shared__ float part[4][kFoldMaxChunks];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + wave;
+  const int per = dh / 8, hp = kFoldMaxChunks / per;  // chunks per head, heads per pass
+  const T* row = wk + (int64_t)i * H * dh;
+  for (int h0 = 0; h0 < H; h0 += hp) {
+    const int nh = min(hp, H - h0), c0 = h0 * per;
+    if (i < d) {
+      for (int ch = lane; ch < nh * per; ch += 64) {
+        float w[8], qq[8];
+        agg_ld8(row + (c0 + ch) * 8, w);
+        agg_ld8(q + (c0 + ch) * 8, qq);
+        float s = 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += w[u] * qq[u];
+        part[wave][ch] = s;
+      }
+    }
+    __syncthreads();
+    if (i < d && lane < nh) {
+      float s = 0.f;
+      for (int k = 0; k < per; ++k) s += part[wave][lane * per + k];
+      Ut[(int64_t)(h0 + lane) * d + i] = from_f<T>(s);
+    }
+    __syncthreads();
+  }
 }
 
 // softmax over v of S[(t*V + v)*H + h]: a32[t][h][v] (float32) and
@@ -190,23 +264,41 @@ __global__ void __launch_bounds__(256) agg_softmax_bwd(const float* __restrict__
 }
 
 // dW_k[i][j] = dU[i][h(j)] q[j];  dW_q[i][j] = q0[i] dq[j]
+// (4 consecutive columns per thread, 16-byte accesses)
 template <typename T>
 __global__ void __launch_bounds__(256) agg_outer(const float* __restrict__ dU, const float* __restrict__ q,
                                                  const T* __restrict__ q0, const float* __restrict__ dq,
                                                  float* __restrict__ dwk, float* __restrict__ dwq, int d, int H,
                                                  int dh, int accumulate) {
-  const int A = H * dh;
-  const int64_t total = (int64_t)d * A;
+  const int A = H * dh, c4 = A / 4;
+  const int64_t total = (int64_t)d * c4;
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int i = (int)(e / A), j = (int)(e % A);
-    const float vk = dU[(int64_t)i * H + j / dh] * q[j];
-    const float vq = to_f(q0[i]) * dq[j];
-    dwk[e] = accumulate ? dwk[e] + vk : vk;
-    dwq[e] = accumulate ? dwq[e] + vq : vq;
+    const int i = (int)(e / c4), j = (int)(e % c4) * 4;
+    const float u = dU[(int64_t)i * H + j / dh], q0i = to_f(q0[i]);
+    const f32x4 qv = *reinterpret_cast<const f32x4*>(q + j), dqv = *reinterpret_cast<const f32x4*>(dq + j);
+    f32x4* pk = reinterpret_cast<f32x4*>(dwk + (int64_t)i * A + j);
+    f32x4* pq = reinterpret_cast<f32x4*>(dwq + (int64_t)i * A + j);
+    f32x4 vk, vq;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      vk[k] = u * qv[k];
+      vq[k] = q0i * dqv[k];
+    }
+    if (accumulate) {
+      const f32x4 ok = *pk, oq = *pq;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        vk[k] = ok[k] + vk[k];
+        vq[k] = oq[k] + vq[k];
+      }
+    }
+    *pk = vk;
+    *pq = vq;
   }
 }
 
-// dq0[i] = sum_j w_q[i][j] dq[j]; db_q = dq; db_k = 0 (one wave per row i)
+// dq0[i] = sum_j w_q[i][j] dq[j]; db_q = dq; db_k = 0 (one wave per row i,
+// 8 columns per lane at a time)
 template <typename T>
 __global__ void __launch_bounds__(256) agg_query_bwd(const T* __restrict__ wq, const float* __restrict__ dq,
                                                      float* dq0, float* dbq, float* dbk, int d, int A,
@@ -214,8 +306,15 @@ __global__ void __launch_bounds__(256) agg_query_bwd(const T* __restrict__ wq, c
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + wave;
   if (i < d) {
+    const T* row = wq + (int64_t)i * A;
     float s = 0.f;
-    for (int j = lane; j < A; j += 64) s += to_f(wq[(int64_t)i * A + j]) * dq[j];
+    for (int ch = lane; ch < A / 8; ch += 64) {
+      float w[8], g[8];
+      agg_ld8(row + ch * 8, w);
+      agg_ld8(dq + ch * 8, g);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += w[u] * g[u];
+    }
     s = wave_sum(s);
     if (lane == 0) dq0[i] = accumulate ? dq0[i] + s : s;
   }
@@ -327,7 +426,7 @@ orbit_status gemv_cols(const char* name, const void* W, const void* x, const flo
   ORBIT_TRY(launch(k1, agg_gemv_part<T, DQ>, dim3((unsigned)slices), dim3(256), 0, s, static_cast<const T*>(W),
                    static_cast<const T*>(x), dU, part, d, A, H, dh));
   KernelInfo k2{"agg_gemv_final", 0.0, (double)slices * A * 4};
-  return launch(k2, agg_gemv_final<T>, dim3((unsigned)cdiv(A, 256)), dim3(256), 0, s, (const float*)part, slices, A,
+  return launch(k2, agg_gemv_final<T>, dim3((unsigned)cdiv(A, 16)), dim3(256), 0, s, (const float*)part, slices, A,
                 static_cast<const T*>(bias), out);
 }
 size_t gemv_part_bytes(int d, int A) { return (size_t)cdiv(d, kGvRows) * A * sizeof(float); }
@@ -434,11 +533,11 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
   KernelInfo ku{"agg_fold_key", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   if (dt == ORBIT_BF16) {
     ORBIT_TRY((gemv_cols<bf16, false>("agg_query", p.w_q, p.q0, nullptr, p.b_q, sv.q, gvp, z.d, z.A, z.H, z.dh, s)));
-    ORBIT_TRY(launch(ku, agg_fold_key<bf16>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s, (const bf16*)p.w_k,
+    ORBIT_TRY(launch(ku, agg_fold_key<bf16>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s, (const bf16*)p.w_k,
                      (const float*)sv.q, (bf16*)sv.Ut, z.d, z.H, z.dh));
   } else {
     ORBIT_TRY((gemv_cols<float, false>("agg_query", p.w_q, p.q0, nullptr, p.b_q, sv.q, gvp, z.d, z.A, z.H, z.dh, s)));
-    ORBIT_TRY(launch(ku, agg_fold_key<float>, dim3(g1((int64_t)z.d * z.H)), dim3(256), 0, s,
+    ORBIT_TRY(launch(ku, agg_fold_key<float>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s,
                      (const float*)p.w_k, (const float*)sv.q, (float*)sv.Ut, z.d, z.H, z.dh));
   }
   // 2. scores S[t*V+v][h] = x_{t,v} . u_h / sqrt(dh)
@@ -615,14 +714,14 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
   KernelInfo kqb{"agg_query_bwd", 2.0 * z.d * z.A, (double)z.d * z.A * esz(dt)};
   if (dt == ORBIT_BF16) {
     ORBIT_TRY((gemv_cols<bf16, true>("agg_dq", p.w_k, nullptr, dU, nullptr, dq, gvp, z.d, z.A, z.H, z.dh, s)));
-    ORBIT_TRY(launch(kou, agg_outer<bf16>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
+    ORBIT_TRY(launch(kou, agg_outer<bf16>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A / 4), 8192)),
                      dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const bf16*)p.q0, (const float*)dq,
                      gr.w_k, gr.w_q, z.d, z.H, z.dh, accumulate));
     ORBIT_TRY(launch(kqb, agg_query_bwd<bf16>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s, (const bf16*)p.w_q,
                      (const float*)dq, gr.q0, gr.b_q, gr.b_k, z.d, z.A, accumulate));
   } else {
     ORBIT_TRY((gemv_cols<float, true>("agg_dq", p.w_k, nullptr, dU, nullptr, dq, gvp, z.d, z.A, z.H, z.dh, s)));
-    ORBIT_TRY(launch(kou, agg_outer<float>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A), 8192)),
+    ORBIT_TRY(launch(kou, agg_outer<float>, dim3((unsigned)std::min<int64_t>(g1((int64_t)z.d * z.A / 4), 8192)),
                      dim3(256), 0, s, (const float*)dU, (const float*)sv.q, (const float*)p.q0, (const float*)dq,
                      gr.w_k, gr.w_q, z.d, z.H, z.dh, accumulate));
     ORBIT_TRY(launch(kqb, agg_query_bwd<float>, dim3((unsigned)cdiv(z.d, 4)), dim3(256), 0, s,
