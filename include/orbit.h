@@ -301,7 +301,7 @@ orbit_status orbit_attention_bwd(int32_t dtype, int32_t B, int32_t H, int32_t L,
  * that overlap on one GPU (concurrent streams or host threads) race: order
  * them on one stream. The array needs no clearing: every call writes the
  * scratch it reads. */
-#define ORBIT_ATTN_BWD_NOALLOC_MAX_SCRATCH ((size_t)16 << 20)
+#define ORBIT_ATTN_BWD_NOALLOC_MAX_SCRATCH ((size_t)160 << 20)
 orbit_status orbit_attention_bwd_noalloc(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
                                          const void* q, int64_t ldq, const void* k, int64_t ldk,
                                          const void* v, int64_t ldv, const void* o, int64_t ldo,

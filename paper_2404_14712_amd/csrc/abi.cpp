@@ -225,7 +225,9 @@ orbit_status block_forward_steps(const BlockDims& z, const orbit_block_params* p
     io.q = sv.qkv; io.ldq = 3 * z.A;
     io.k = static_cast<char*>(sv.qkv) + z.A * e; io.ldk = 3 * z.A;
   }
-  ORBIT_TRY(attn_fwd(dt, io, sv.o, z.A, sv.lse, sv.o32, z.A, s));
+  // the attention backward's workspace is idle during the forward and holds
+  // the forward's split partials
+  ORBIT_TRY(attn_fwd(dt, io, sv.o, z.A, sv.lse, sv.o32, z.A, w.D, attn_bwd_workspace_bytes(z.B, z.H, z.L, z.dh), s));
   {
     Gemm g; g.dtype = dt; g.tag = "proj";
     g.A = sv.o; g.lda = z.A; g.B = p->w_proj; g.ldb = z.d; g.C = sv.x1; g.ldc = z.d;
@@ -918,7 +920,7 @@ orbit_status orbit_attention_fwd(int32_t dtype, int32_t B, int32_t H, int32_t L,
       ORBIT_E_ARG, "%s: leading dimensions must be >= heads*head_dim and multiples of 8", fn);
   REQ(!o32 || (ldo32 >= A && ldo32 % 8 == 0), ORBIT_E_ARG, "%s: bad ldo32", fn);
   AttnIO io{q, k, v, ldq, ldk, ldv, B, H, L, head_dim};
-  return attn_fwd((orbit_dtype)dtype, io, o, ldo, lse, o32, ldo32, S(stream));
+  return attn_fwd((orbit_dtype)dtype, io, o, ldo, lse, o32, ldo32, nullptr, 0, S(stream));
 }
 
 orbit_status orbit_attention_bwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim, const void* q,

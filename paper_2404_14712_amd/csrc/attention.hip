@@ -28,6 +28,12 @@ struct FwdArgs {
   int64_t ldq, ldk, ldv, ldo, ldo32;
   int H, L;
   float sl2;  // log2(e) / sqrt(dh)
+  // key split (ns > 1): block column = split * query tiles + query tile; the
+  // float32 partials go to `part` ([ns][rows][dh] outputs, then [ns][rows]
+  // reference maxima and [ns][rows] row sums; rows = B H L, (sample, head,
+  // query) order) and attn_fwd_merge finishes O, o32 and lse
+  int B = 0, ns = 1;
+  float* part = nullptr;
 };
 
 // lane l: fragment slot j (0..7) of lane group g = l/32 in a 16-deep K step of
@@ -257,6 +263,11 @@ struct BwdArgs {
   int64_t ldq, ldk, ldv, lddo, ldg;
   int H, L;
   float sl2, scale;  // log2(e)/sqrt(dh), 1/sqrt(dh)
+  // sweep split (ns > 1): block column = split * tiles + tile; each split
+  // writes float32 partial sums to `part` (rows = B H L) and a merge kernel
+  // finishes the gradients
+  int B = 0, ns = 1;
+  float* part = nullptr;
 };
 
 // Stage a 32-row x DH tile X[r][c] (rows r0.., valid < rlim) into LDS twice:
@@ -675,6 +686,8 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
   int xb, h, b;
   attn_block_coords(xb, h, b);
   const int L = a.L;
+  const int sp = xb / ((L + 127) / 128);  // key split of this block
+  xb -= sp * ((L + 127) / 128);
   const int64_t row0 = (int64_t)b * L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
   const T* K = static_cast<const T*>(a.k) + row0 * a.ldk + h * DH;
@@ -701,15 +714,18 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
   tk.init(K, a.ldk, L, tid);
   tv.init(V, a.ldv, L, tid);
   const int nt = (L + KT - 1) / KT;
-  tk.load(0);
-  tv.load(0);
+  // this split's key tiles [t0, t1)
+  const int per = (nt + a.ns - 1) / a.ns;
+  const int t0 = sp * per, t1 = min(nt, t0 + per);
+  tk.load(t0 * KT);
+  tv.load(t0 * KT);
   tk.store(ks[0]);
   tv.store(vs[0]);
   __syncthreads();
 
   auto tile = [&](int jt, auto mask) {
-    const int cur = jt & 1;
-    if (jt + 1 < nt) {
+    const int cur = (jt - t0) & 1;
+    if (jt + 1 < t1) {
       tk.load((jt + 1) * KT);
       tv.load((jt + 1) * KT);
     }
@@ -769,17 +785,36 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
         mma16(o[c], vf, pf);
       }
     }
-    if (jt + 1 < nt) {
+    if (jt + 1 < t1) {
       tk.store(ks[cur ^ 1]);
       tv.store(vs[cur ^ 1]);
     }
     __syncthreads();
   };
-  const int nfull = L / KT;
-  for (int jt = 0; jt < nfull; ++jt) tile(jt, std::false_type{});
-  if (nfull < nt) tile(nfull, std::true_type{});
+  // full tiles, then the partial last tile of the sequence if it is in range
+  const int tf = min(t1, L / KT);
+  for (int jt = t0; jt < tf; ++jt) tile(jt, std::false_type{});
+  if (tf < t1) tile(tf, std::true_type{});
 
   const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  if (a.ns > 1) {
+    // unnormalised outputs, their reference maximum and row sum
+    if (qi < L) {
+      const int64_t R = (int64_t)a.B * a.H * L, r = ((int64_t)b * a.H + h) * L + qi;
+      float* po = a.part + ((int64_t)sp * R + r) * DH;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          st4(po + c * 32 + r4 * 8 + g * 4, o[c][r4 * 4], o[c][r4 * 4 + 1], o[c][r4 * 4 + 2], o[c][r4 * 4 + 3]);
+      if (g == 0) {
+        float* pm = a.part + (int64_t)a.ns * R * DH;
+        pm[(int64_t)sp * R + r] = m;
+        pm[(int64_t)(a.ns + sp) * R + r] = ltot;
+      }
+    }
+    return;
+  }
   if (qi < L) {
     const float inv = 1.f / ltot;
     T* O = static_cast<T*>(a.o) + (row0 + qi) * a.ldo + h * DH;
@@ -841,6 +876,8 @@ attn_bwd_dkdv_tr(BwdArgs a) {
   int xb, h, b;
   attn_block_coords(xb, h, b);
   const int L = a.L;
+  const int sp = xb / ((L + 127) / 128);  // query split of this block
+  xb -= sp * ((L + 127) / 128);
   const int64_t row0 = (int64_t)b * L;
   if (grp == 0 && tid < DH) qbar[tid] = a.qsum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
@@ -880,12 +917,15 @@ attn_bwd_dkdv_tr(BwdArgs a) {
   TL tq, to;
   tq.init(Q, a.ldq, L, tid);
   to.init(dO, a.lddo, L, tid);
-  const int nq = (L + QT - 1) / QT;
-  // group grp takes query tiles grp, grp + QG, ...; every group runs the same
-  // number of iterations (shared barriers), past its last tile without work
+  // this split's query tiles qt0 .. qt0 + nq - 1
+  const int nqa = (L + QT - 1) / QT, qper = (nqa + a.ns - 1) / a.ns, qt0 = sp * qper;
+  const int nq = max(0, min(nqa, qt0 + qper) - qt0);
+  // group grp takes query tiles grp, grp + QG, ... of the range; every group
+  // runs the same number of iterations (shared barriers), past its last tile
+  // without work
   const int iters = (nq + QG - 1) / QG;
   {
-    const int q0 = grp * QT;
+    const int q0 = (qt0 + grp) * QT;
     tq.load(q0);
     to.load(q0);
     tq.store(qs[0]);
@@ -901,7 +941,7 @@ attn_bwd_dkdv_tr(BwdArgs a) {
     const int cur = i & 1;
     float lse_n = 0.f, d_n = 0.f;
     if (it + QG < nq) {
-      const int q1 = (it + QG) * QT;
+      const int q1 = (qt0 + it + QG) * QT;
       tq.load(q1);
       to.load(q1);
       if (tid < QT) {
@@ -1022,6 +1062,28 @@ attn_bwd_dkdv_tr(BwdArgs a) {
     cs += rs[0];
     csr += rs[64];
   }
+  if (a.ns > 1) {
+    // raw sums of this query range: dK^T, dV^T and the two remainder sums
+    if (kv < L) {
+      const int64_t R = (int64_t)a.B * a.H * L, r = ((int64_t)b * a.H + h) * L + kv;
+      float* pk = a.part + ((int64_t)sp * R + r) * DH;
+      float* pv = a.part + ((int64_t)(a.ns + sp) * R + r) * DH;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int col = c * 32 + r4 * 8 + g * 4;
+          st4(pk + col, dkt[c][r4 * 4], dkt[c][r4 * 4 + 1], dkt[c][r4 * 4 + 2], dkt[c][r4 * 4 + 3]);
+          st4(pv + col, dvt[c][r4 * 4], dvt[c][r4 * 4 + 1], dvt[c][r4 * 4 + 2], dvt[c][r4 * 4 + 3]);
+        }
+      if (g == 0) {
+        float* pc = a.part + (int64_t)2 * a.ns * R * DH;
+        pc[(int64_t)sp * R + r] = cs;
+        pc[(int64_t)(a.ns + sp) * R + r] = csr;
+      }
+    }
+    return;
+  }
   const float corr = cs - csr;
   if (kv < L) {
     T* dK = static_cast<T*>(a.dk) + (row0 + kv) * a.ldg + h * DH;
@@ -1065,6 +1127,8 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
   int xb, h, b;
   attn_block_coords(xb, h, b);
   const int L = a.L;
+  const int sp = xb / ((L + 127) / 128);  // key split of this block
+  xb -= sp * ((L + 127) / 128);
   const int64_t row0 = (int64_t)b * L;
   if (grp == 0 && tid < DH) kbar[tid] = a.ksum[((int64_t)b * a.H + h) * DH + tid] / (float)L;
   const T* Q = static_cast<const T*>(a.q) + row0 * a.ldq + h * DH;
@@ -1098,17 +1162,19 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
   TL tk, tv;
   tk.init(K, a.ldk, L, tid);
   tv.init(V, a.ldv, L, tid);
-  const int nt = (L + KT - 1) / KT;
-  // group grp takes key tiles grp, grp + QG, ...; both groups run the same
-  // number of iterations (shared barriers)
-  tk.load(grp * KT);
-  tv.load(grp * KT);
+  // this split's key tiles [t0, t1)
+  const int nt = (L + KT - 1) / KT, per = (nt + a.ns - 1) / a.ns;
+  const int t0 = sp * per, t1 = min(nt, t0 + per);
+  // group grp takes key tiles t0 + grp, t0 + grp + QG, ...; both groups run
+  // the same number of iterations (shared barriers)
+  tk.load((t0 + grp) * KT);
+  tv.load((t0 + grp) * KT);
   tk.store(ks[0]);
   tv.store(vs[0]);
   __syncthreads();
 
   auto tile = [&](int jt, int cur, auto mask) {
-    if (jt + QG < nt) {
+    if (jt + QG < t1) {
       tk.load((jt + QG) * KT);
       tv.load((jt + QG) * KT);
     }
@@ -1162,24 +1228,25 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
         mma16(dqt[c], af, sf);
       }
     }
-    if (jt + QG < nt) {
+    if (jt + QG < t1) {
       tk.store(ks[cur ^ 1]);
       tv.store(vs[cur ^ 1]);
     }
     __syncthreads();
   };
-  const int nfull = L / KT;
+  // full tiles of the range (the sequence's partial last tile, if any, comes last)
+  const int nfs = max(0, min(t1, L / KT) - t0), nts = t1 - t0;
   if constexpr (QG == 1) {
-    for (int jt = 0; jt < nfull; ++jt) tile(jt, jt & 1, std::false_type{});
-    if (nfull < nt) tile(nfull, nfull & 1, std::true_type{});
+    for (int i = 0; i < nfs; ++i) tile(t0 + i, i & 1, std::false_type{});
+    if (nfs < nts) tile(t0 + nfs, nfs & 1, std::true_type{});
   } else {
     // pairs of full tiles, then at most two more tiles (one may be partial;
     // a group past its last tile only joins the barrier)
-    const int pairs = nfull / QG;
-    for (int i = 0; i < pairs; ++i) tile(i * QG + grp, i & 1, std::false_type{});
-    for (int i = pairs; i < (nt + QG - 1) / QG; ++i) {
-      const int jt = i * QG + grp;
-      if (jt < nt) tile(jt, i & 1, std::true_type{});
+    const int pairs = nfs / QG;
+    for (int i = 0; i < pairs; ++i) tile(t0 + i * QG + grp, i & 1, std::false_type{});
+    for (int i = pairs; i < (nts + QG - 1) / QG; ++i) {
+      const int jt = t0 + i * QG + grp;
+      if (jt < t1) tile(jt, i & 1, std::true_type{});
       else __syncthreads();
     }
   }
@@ -1207,6 +1274,21 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
       for (int v = 0; v < 16; ++v) dqt[c][v] += rq[(c * 16 + v) * 64];
     rs += rr[0];
   }
+  if (a.ns > 1) {
+    // raw sums of this key range: dQ^T and the remainder sum
+    if (qi < L) {
+      const int64_t R = (int64_t)a.B * a.H * L, r = ((int64_t)b * a.H + h) * L + qi;
+      float* pq = a.part + ((int64_t)sp * R + r) * DH;
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          st4(pq + c * 32 + r4 * 8 + g * 4, dqt[c][r4 * 4], dqt[c][r4 * 4 + 1], dqt[c][r4 * 4 + 2],
+              dqt[c][r4 * 4 + 3]);
+      if (g == 0) a.part[(int64_t)a.ns * R * DH + (int64_t)sp * R + r] = rs;
+    }
+    return;
+  }
   if (qi < L) {
     T* dQ = static_cast<T*>(a.dq) + (row0 + qi) * a.ldg + h * DH;
 #pragma unroll
@@ -1222,6 +1304,122 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
   }
 }
 
+// ---------------------------------------------------------------------------
+// merges of the split partials (fixed order over the splits); one thread per
+// (row, 8 columns), rows in (sample, head, position) order
+// ---------------------------------------------------------------------------
+
+// O, o32 and lse: each split's unnormalised output is rescaled to the largest
+// of the splits' reference maxima, and the sum is divided by the combined row
+// sum
+template <int DH>
+__global__ void __launch_bounds__(256) attn_fwd_merge(FwdArgs a) {
+  constexpr int C8 = DH / 8;
+  const int64_t R = (int64_t)a.B * a.H * a.L;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= R * C8) return;
+  const int64_t r = idx / C8;
+  const int c0 = (int)(idx % C8) * 8;
+  const float* pm = a.part + (int64_t)a.ns * R * DH;
+  float M = -INFINITY;
+  for (int s = 0; s < a.ns; ++s) M = fmaxf(M, pm[(int64_t)s * R + r]);
+  float den = 0.f, acc[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) acc[u] = 0.f;
+  for (int s = 0; s < a.ns; ++s) {
+    const float w = __builtin_amdgcn_exp2f(pm[(int64_t)s * R + r] - M);
+    den += w * pm[(int64_t)(a.ns + s) * R + r];
+    const float* po = a.part + ((int64_t)s * R + r) * DH + c0;
+    const f32x4 x0 = *reinterpret_cast<const f32x4*>(po), x1 = *reinterpret_cast<const f32x4*>(po + 4);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc[u] += w * x0[u];
+      acc[4 + u] += w * x1[u];
+    }
+  }
+  const float inv = 1.f / den;
+  const int64_t bh = r / a.L;
+  const int qi = (int)(r - bh * a.L), h = (int)(bh % a.H);
+  const int64_t orow = (bh / a.H) * a.L + qi;
+  bf16* O = static_cast<bf16*>(a.o) + orow * a.ldo + h * DH + c0;
+  st4(O, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+  st4(O + 4, acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+  if (a.o32) {
+    float* O32 = a.o32 + orow * a.ldo32 + h * DH + c0;
+    st4(O32, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    st4(O32 + 4, acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+  }
+  if (c0 == 0) a.lse[r] = (M + __log2f(den)) * kLn2;
+}
+
+// dK = (sum of the splits' dK^T + qbar (sum cs - sum csr)) / sqrt(dh), dV = sum of dV^T
+template <int DH>
+__global__ void __launch_bounds__(256) attn_dkdv_merge(BwdArgs a) {
+  constexpr int C8 = DH / 8;
+  const int64_t R = (int64_t)a.B * a.H * a.L;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= R * C8) return;
+  const int64_t r = idx / C8;
+  const int c0 = (int)(idx % C8) * 8;
+  const float* pc = a.part + (int64_t)2 * a.ns * R * DH;
+  float cs = 0.f, csr = 0.f, k8[8], v8[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) k8[u] = v8[u] = 0.f;
+  for (int s = 0; s < a.ns; ++s) {
+    cs += pc[(int64_t)s * R + r];
+    csr += pc[(int64_t)(a.ns + s) * R + r];
+    const float* pk = a.part + ((int64_t)s * R + r) * DH + c0;
+    const float* pv = a.part + ((int64_t)(a.ns + s) * R + r) * DH + c0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      k8[u] += pk[u];
+      v8[u] += pv[u];
+    }
+  }
+  const float corr = cs - csr;
+  const int64_t bh = r / a.L;
+  const int kv = (int)(r - bh * a.L), h = (int)(bh % a.H);
+  const int64_t orow = (bh / a.H) * a.L + kv;
+  float dk[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) dk[u] = (k8[u] + a.qsum[bh * DH + c0 + u] / (float)a.L * corr) * a.scale;
+  bf16* dK = static_cast<bf16*>(a.dk) + orow * a.ldg + h * DH + c0;
+  bf16* dV = static_cast<bf16*>(a.dv) + orow * a.ldg + h * DH + c0;
+  st4(dK, dk[0], dk[1], dk[2], dk[3]);
+  st4(dK + 4, dk[4], dk[5], dk[6], dk[7]);
+  st4(dV, v8[0], v8[1], v8[2], v8[3]);
+  st4(dV + 4, v8[4], v8[5], v8[6], v8[7]);
+}
+
+// dQ = (sum of the splits' dQ^T - kbar sum rs) / sqrt(dh)
+template <int DH>
+__global__ void __launch_bounds__(256) attn_dq_merge(BwdArgs a) {
+  constexpr int C8 = DH / 8;
+  const int64_t R = (int64_t)a.B * a.H * a.L;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= R * C8) return;
+  const int64_t r = idx / C8;
+  const int c0 = (int)(idx % C8) * 8;
+  float rs = 0.f, q8[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) q8[u] = 0.f;
+  for (int s = 0; s < a.ns; ++s) {
+    rs += a.part[(int64_t)a.ns * R * DH + (int64_t)s * R + r];
+    const float* pq = a.part + ((int64_t)s * R + r) * DH + c0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) q8[u] += pq[u];
+  }
+  const int64_t bh = r / a.L;
+  const int qi = (int)(r - bh * a.L), h = (int)(bh % a.H);
+  const int64_t orow = (bh / a.H) * a.L + qi;
+  float dq[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) dq[u] = (q8[u] - a.ksum[bh * DH + c0 + u] / (float)a.L * rs) * a.scale;
+  bf16* dQ = static_cast<bf16*>(a.dq) + orow * a.ldg + h * DH + c0;
+  st4(dQ, dq[0], dq[1], dq[2], dq[3]);
+  st4(dQ + 4, dq[4], dq[5], dq[6], dq[7]);
+}
+
 // the bf16 kernels address one (sample, head) slice of q, k, v (and dO) with
 // 32-bit byte offsets, and the backward preprocess indexes head rows in 32 bits
 bool slices_fit(const AttnIO& io, int64_t ld_extra) {
@@ -1229,8 +1427,27 @@ bool slices_fit(const AttnIO& io, int64_t ld_extra) {
   return (int64_t)io.L * ld * 4 < ((int64_t)1 << 31) && (int64_t)io.B * io.L * io.H < ((int64_t)1 << 31);
 }
 
+// bf16 grids of fewer than 256 blocks of 128 positions (one sample-head pair
+// per block row) leave CUs idle: the sweep (keys for the forward and dQ,
+// queries for dK, dV) is then split over 2 blocks whose float32 partials a
+// merge kernel combines
+int attn_splits(int B, int H, int L) {
+  return cdiv(L, 128) * (int64_t)H * B < 256 && L >= 512 ? 2 : 1;
+}
+// the partials of a split launch: ns x rows x (2 dh + 2) floats covers the
+// backward's dK/dV partials (and, reused afterwards, its dQ partials) and the
+// forward's output partials
+size_t split_bytes(int B, int H, int L, int dh) {
+  const int ns = attn_splits(B, H, L);
+  return ns > 1 ? align_up((size_t)ns * B * H * L * (2 * dh + 2) * sizeof(float)) : 0;
+}
+size_t attn_bwd_base_bytes(int B, int H, int L, int dh) {
+  return align_up((size_t)B * H * (L + 2 * dh) * sizeof(float)) + 2 * colsum_part_bytes(L, H * dh, false, B);
+}
+
 template <typename T, int DH>
-orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32, hipStream_t s) {
+orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32, void* scratch,
+                   size_t scratch_bytes, hipStream_t s) {
   if (!slices_fit(io, 0)) {
     set_error("attention: sequence length %d x row stride too large for 32-bit slice offsets", io.L);
     return ORBIT_E_UNSUPPORTED;
@@ -1239,8 +1456,20 @@ orbit_status fwd_t(const AttnIO& io, void* o, int64_t ldo, float* lse, float* o3
   const double bh = (double)io.B * io.H;
   KernelInfo ki{sizeof(T) == 2 ? "attn_fwd_kernel<bf16>" : "attn_fwd_kernel<f32>",
                 4.0 * bh * io.L * (double)io.L * DH, 4.0 * bh * io.L * DH * sizeof(T)};
-  if constexpr (sizeof(T) == 2)
+  if constexpr (sizeof(T) == 2) {
+    const int ns = attn_splits(io.B, io.H, io.L);
+    if (ns > 1 && scratch && scratch_bytes >= split_bytes(io.B, io.H, io.L, DH)) {
+      a.B = io.B;
+      a.ns = ns;
+      a.part = static_cast<float*>(scratch);
+      ORBIT_TRY(launch(ki, attn_fwd_tr<DH>, dim3((unsigned)(cdiv(io.L, 128) * ns), io.H, io.B), dim3(256), 0, s, a));
+      const int64_t rows = (int64_t)io.B * io.H * io.L;
+      KernelInfo km{"attn_fwd_merge<bf16>", 0.0,
+                    (double)rows * (ns * (DH + 2) * 4.0 + DH * (sizeof(T) + (o32 ? 4.0 : 0.0)))};
+      return launch(km, attn_fwd_merge<DH>, dim3((unsigned)cdiv(rows * (DH / 8), 256)), dim3(256), 0, s, a);
+    }
     return launch(ki, attn_fwd_tr<DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
+  }
   return launch(ki, attn_fwd_kernel<T, DH>, dim3((unsigned)cdiv(io.L, 128), io.H, io.B), dim3(256), 0, s, a);
 }
 
@@ -1281,11 +1510,17 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
   }
   BwdArgs a{io.q, io.k, io.v, dO, lse, D, qsum, ksum, dq, dk, dv, io.ldq, io.ldk, io.ldv, lddo, ldg, io.H, io.L,
             kLog2e / sqrtf((float)DH), 1.f / sqrtf((float)DH)};
+  const int ns = sizeof(T) == 2 ? attn_splits(io.B, io.H, io.L) : 1;
+  if (ns > 1) {
+    a.B = io.B;
+    a.ns = ns;
+    a.part = reinterpret_cast<float*>(reinterpret_cast<char*>(D) + attn_bwd_base_bytes(io.B, io.H, io.L, DH));
+  }
   // algorithmic backward = 2x forward; kernels split it 3:2 (dK,dV: 4 products, dQ: 3 incl. recompute)
   const double fl = 4.0 * bh * io.L * (double)io.L * DH;
   KernelInfo k1{sizeof(T) == 2 ? "attn_bwd_dkdv<bf16>" : "attn_bwd_dkdv<f32>", 2 * fl * 0.6,
                 6.0 * bh * io.L * DH * sizeof(T)};
-  const dim3 grid((unsigned)cdiv(io.L, 128), io.H, io.B);
+  const dim3 grid((unsigned)(cdiv(io.L, 128) * ns), io.H, io.B);
   if constexpr (sizeof(T) == 2) {
     // at most one block per CU (few sample x head pairs): two wave groups per
     // block split the queries, so each SIMD still runs two waves
@@ -1302,22 +1537,38 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
   }
   KernelInfo k2{sizeof(T) == 2 ? "attn_bwd_dq<bf16>" : "attn_bwd_dq<f32>", 2 * fl * 0.4,
                 5.0 * bh * io.L * DH * sizeof(T)};
-  if constexpr (sizeof(T) == 2 && DH == 128) {
-    if ((int64_t)grid.x * grid.y * grid.z <= 256) return launch(k2, attn_bwd_dq_tr<DH, 2>, grid, dim3(512), 0, s, a);
+  if constexpr (sizeof(T) == 2) {
+    const dim3 gm((unsigned)cdiv(rows * (DH / 8), 256));
+    if (ns > 1) {
+      KernelInfo km{"attn_dkdv_merge<bf16>", 0.0, (double)rows * (ns * (2 * DH + 2) * 4.0 + 2 * DH * sizeof(T))};
+      ORBIT_TRY(launch(km, attn_dkdv_merge<DH>, gm, dim3(256), 0, s, a));
+    }
+    bool done = false;
+    if constexpr (DH == 128) {
+      if ((int64_t)grid.x * grid.y * grid.z <= 256) {
+        ORBIT_TRY(launch(k2, attn_bwd_dq_tr<DH, 2>, grid, dim3(512), 0, s, a));
+        done = true;
+      }
+    }
+    if (!done) ORBIT_TRY(launch(k2, attn_bwd_dq_tr<DH>, grid, dim3(256), 0, s, a));
+    if (ns == 1) return ORBIT_OK;
+    KernelInfo km{"attn_dq_merge<bf16>", 0.0, (double)rows * (ns * (DH + 1) * 4.0 + DH * sizeof(T))};
+    return launch(km, attn_dq_merge<DH>, gm, dim3(256), 0, s, a);
   }
-  if constexpr (sizeof(T) == 2) return launch(k2, attn_bwd_dq_tr<DH>, grid, dim3(256), 0, s, a);
   return launch(k2, attn_bwd_dq<T, DH>, grid, dim3(256), 0, s, a);
 }
 
 }  // namespace
 
+size_t attn_split_bytes(int B, int H, int L, int dh) { return split_bytes(B, H, L, dh); }
+
 size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh) {
-  return align_up((size_t)B * H * (L + 2 * dh) * sizeof(float)) + 2 * colsum_part_bytes(L, H * dh, false, B);
+  return attn_bwd_base_bytes(B, H, L, dh) + split_bytes(B, H, L, dh);
 }
 
 orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32,
-                      int64_t ldo32, hipStream_t s) {
-#define AF(TT, D) return fwd_t<TT, D>(io, o, ldo, lse, o32, ldo32, s)
+                      int64_t ldo32, void* scratch, size_t scratch_bytes, hipStream_t s) {
+#define AF(TT, D) return fwd_t<TT, D>(io, o, ldo, lse, o32, ldo32, scratch, scratch_bytes, s)
   if (dt == ORBIT_BF16) {
     if (io.dh == 32) AF(bf16, 32);
     if (io.dh == 64) AF(bf16, 64);

@@ -76,11 +76,15 @@ struct AttnIO {
   int64_t ldq, ldk, ldv;
   int B, H, L, dh;
 };
-// o32 (optional): float32 copy of O, used by the backward for rowsum(dO * O)
+// o32 (optional): float32 copy of O, used by the backward for rowsum(dO * O).
+// scratch (optional, scratch_bytes >= attn_split_bytes): with it, bf16 grids of
+// few blocks split the keys over two blocks and merge their partials
 orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32,
-                      hipStream_t s);
+                      void* scratch, size_t scratch_bytes, hipStream_t s);
+// float32 partials of a split launch (0 when the grid is not split)
+size_t attn_split_bytes(int B, int H, int L, int dh);
 // workspace of attn_bwd: D[b,h,l] = rowsum(dO * O), sums of q and k over the
-// sequence, and the column-reduction scratch
+// sequence, the column-reduction scratch and the partials of a split launch
 size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh);
 // validation of the attention backward's arguments other than its workspace
 // (shared by the entry points that take a workspace and the one that does not)

@@ -100,6 +100,14 @@ def test_attention_wide_heads(lib, dh, L):
     _attention_case(lib, "bf16", dh, L, 1.0)
 
 
+@pytest.mark.parametrize("dtype,dh", [("bf16", 64), ("bf16", 128), ("bf16", 192), ("bf16", 256), ("f32", 64)])
+def test_attention_split_backward(lib, dtype, dh):
+    """2 samples x 3 heads x 600 positions is a grid of 30 blocks: the bf16
+    backward splits its sweeps over two blocks each and merges the float32
+    partials; 600 leaves partial key and query tiles in the second split."""
+    _attention_case(lib, dtype, dh, 600, 1.0)
+
+
 def _attention_case(lib, dtype, dh, L, qk_scale):
     import torch
     B, H = 2, 3

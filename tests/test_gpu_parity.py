@@ -189,6 +189,11 @@ BLOCK_CASES = [
     # the paper's head widths (bf16): 192 and 256, ragged token counts
     ("bf16", 1, 130, 512, 2, 192, 512, 1),
     ("bf16", 2, 70, 512, 2, 256, 1032, 1),
+    # few blocks of 128 positions: attention splits its sweep over two blocks
+    # (forward and backward) and merges the partials; ragged sequence lengths
+    ("bf16", 1, 600, 512, 2, 128, 512, 1),
+    ("bf16", 1, 520, 512, 2, 192, 512, 1),
+    ("bf16", 1, 530, 512, 2, 256, 512, 0),
     ("bf16", 1, 300, 768, 4, 192, 512, 0),
 ]
 

@@ -67,8 +67,8 @@ def test_noalloc_two_calls_second_smaller(lib, dtype):
 
 def test_noalloc_rejects_sizes_beyond_its_scratch(lib):
     from paper_2404_14712_amd._lib import ORBIT_E_UNSUPPORTED
-    B, H, L, dh = 8, 64, 8192, 128
-    assert lib.orbit_attention_bwd_workspace_bytes(B, H, L, dh) > (16 << 20)
+    B, H, L, dh = 128, 64, 8192, 128
+    assert lib.orbit_attention_bwd_workspace_bytes(B, H, L, dh) > (160 << 20)
     st = lib.lib.orbit_attention_bwd_noalloc(1, B, H, L, dh, 0x1000, H * dh, 0x2000, H * dh, 0x3000, H * dh, 0x4000,
                                              H * dh, 1, 0x5000, 0x6000, H * dh, 0x7000, 0x8000, 0x9000, H * dh, None)
     assert st == ORBIT_E_UNSUPPORTED and "scratch" in lib.last_error()
