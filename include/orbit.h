@@ -346,12 +346,16 @@ const char* orbit_timing_kernel_name(int i);
  * `blocks` blocks of 4 waves; each wave keeps 8 independent bf16 32x32x16
  * matrix products in flight for `iters` rounds, which is
  * blocks * 4 * iters * 8 * 32768 flops; the caller times the launch on
- * `stream`. Every operand element is bf16(x), so each accumulator element
- * ends at 16 x^2 iters; out (device, float32, blocks * 4 elements, caller
- * owned) receives per wave the sum of one element of each of its 8
- * accumulators, 128 x^2 iters. blocks in [1, 2^20], iters in [1, 2^20];
- * otherwise ORBIT_E_ARG. */
-orbit_status orbit_mfma_probe(int32_t blocks, int32_t iters, float x, float* out, void* stream);
+ * `stream`. Both operands of every product are the lane's 8-element
+ * fragment: with seed 0 every element is bf16(x); otherwise element i of
+ * lane l is bf16(x * p) with p = ((h & 255) - 128) / 64 and h the 32-bit
+ * hash h0 = (seed ^ (8 l + i)) * 0x9E3779B1, h1 = h0 ^ (h0 >> 15),
+ * h2 = h1 * 0x85EBCA77, h = h2 ^ (h2 >> 13) (varied operand bits, as in real
+ * data; the clock is lower then). out (device, float32, blocks * 4 elements,
+ * caller owned) receives per wave 8 iters (s0 + s32), s_l the sum of the
+ * squares of lane l's fragment elements (accumulated in float32). blocks in
+ * [1, 2^20], iters in [1, 2^20]; otherwise ORBIT_E_ARG. */
+orbit_status orbit_mfma_probe(int32_t blocks, int32_t iters, uint32_t seed, float x, float* out, void* stream);
 
 #ifdef __cplusplus
 }

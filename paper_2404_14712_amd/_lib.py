@@ -125,7 +125,7 @@ _PROTOS = {
     "orbit_timing_summary": (c_int, [c_char_p, POINTER(c_int64), POINTER(c_double), POINTER(c_double),
                                      POINTER(c_double)]),
     "orbit_timing_kernel_name": (c_char_p, [c_int]),
-    "orbit_mfma_probe": (c_int, [c_int32, c_int32, c_float, P, P]),
+    "orbit_mfma_probe": (c_int, [c_int32, c_int32, ctypes.c_uint32, c_float, P, P]),
 }
 
 EXPORTS = tuple(_PROTOS)
@@ -309,9 +309,9 @@ class OrbitLib:
             _stream(stream)))
 
     # -- measurement aid -------------------------------------------------------
-    def orbit_mfma_probe(self, blocks, iters, x, out, stream=None):
-        self._check("orbit_mfma_probe", self.lib.orbit_mfma_probe(int(blocks), int(iters), float(x), _ptr(out),
-                                                                  _stream(stream)))
+    def orbit_mfma_probe(self, blocks, iters, seed, x, out, stream=None):
+        self._check("orbit_mfma_probe", self.lib.orbit_mfma_probe(int(blocks), int(iters), int(seed), float(x),
+                                                                  _ptr(out), _stream(stream)))
 
     # -- timing ----------------------------------------------------------------
     def orbit_timing_enable(self, on: bool):

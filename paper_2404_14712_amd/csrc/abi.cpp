@@ -804,13 +804,13 @@ orbit_status orbit_mse_loss(const float* pred, const float* tgt, int64_t n, floa
   return mse(pred, tgt, n, scale, loss, dpred, ws, S(stream));
 }
 
-orbit_status orbit_mfma_probe(int32_t blocks, int32_t iters, float x, float* out, void* stream) {
+orbit_status orbit_mfma_probe(int32_t blocks, int32_t iters, uint32_t seed, float x, float* out, void* stream) {
   const char* fn = "orbit_mfma_probe";
   clear_error();
   REQ(blocks >= 1 && blocks <= (1 << 20), ORBIT_E_ARG, "%s: blocks=%d outside [1, 2^20]", fn, blocks);
   REQ(iters >= 1 && iters <= (1 << 20), ORBIT_E_ARG, "%s: iters=%d outside [1, 2^20]", fn, iters);
   PTR(out, "out");
-  return mfma_probe(blocks, iters, x, out, S(stream));
+  return mfma_probe(blocks, iters, seed, x, out, S(stream));
 }
 
 static orbit_status wmse_check(const char* fn, const orbit_wmse_desc* d) {

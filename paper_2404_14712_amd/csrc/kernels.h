@@ -120,7 +120,7 @@ orbit_status wmse(const float* pred, const float* tgt, int B, int L, int Wp, int
 // blocks of 4 waves, each keeping 8 independent bf16 32x32x16 matrix products
 // in flight for `iters` rounds; out[blocks * 4] receives one value per wave
 double mfma_probe_flops(int blocks, int iters);
-orbit_status mfma_probe(int blocks, int iters, float x, float* out, hipStream_t s);
+orbit_status mfma_probe(int blocks, int iters, unsigned seed, float x, float* out, hipStream_t s);
 
 // ---- small helpers ------------------------------------------------------------
 // dst[i] = (dtype) src[i] (float32 -> dtype); used for dpred before the head GEMMs

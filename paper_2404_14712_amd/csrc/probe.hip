@@ -2,8 +2,11 @@
 // Each wave keeps eight independent bf16 32x32x16 products in flight for
 // `iters` rounds, the issue pattern that reaches the matrix cores' peak (an
 // accumulator is reused only every eighth product, well past the product's
-// latency). Every operand element is bf16(x), so each accumulator element
-// ends at 16 x^2 iters, which the caller can check exactly.
+// latency). Both operands of every product are the lane's fragment: all
+// elements bf16(x) (seed 0), or x times a seeded pattern of 8-bit mantissas
+// in [-2, 2) (the matrix cores draw more power, and the clock drops, when the
+// operand bits vary as in real data). Accumulator element (0, 0) ends at
+// iters times the sum of the squares of lanes 0 and 32's fragments.
 #include "kernels.h"
 
 namespace orbit {
@@ -11,10 +14,21 @@ namespace {
 
 constexpr int kProbeChains = 8;
 
-__global__ void __launch_bounds__(256) mfma_probe_kernel(int iters, float x, float* __restrict__ out) {
+// the pattern value of fragment element i of lane l: ((h & 255) - 128) / 64
+// with h a multiplicative hash of (seed, 8 l + i)
+ORBIT_DEV float probe_pattern(unsigned seed, int l, int i) {
+  unsigned h = (seed ^ (unsigned)(8 * l + i)) * 0x9E3779B1u;
+  h ^= h >> 15;
+  h *= 0x85EBCA77u;
+  h ^= h >> 13;
+  return (float)((int)(h & 255u) - 128) * (1.f / 64.f);
+}
+
+__global__ void __launch_bounds__(256) mfma_probe_kernel(int iters, unsigned seed, float x, float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
   bf16x8 a;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) a[i] = (bf16)x;
+  for (int i = 0; i < 8; ++i) a[i] = (bf16)(seed ? x * probe_pattern(seed, lane, i) : x);
   f32x16 acc[kProbeChains];
 #pragma unroll
   for (int c = 0; c < kProbeChains; ++c)
@@ -27,16 +41,16 @@ __global__ void __launch_bounds__(256) mfma_probe_kernel(int iters, float x, flo
   float s = 0.f;
 #pragma unroll
   for (int c = 0; c < kProbeChains; ++c) s += acc[c][0];
-  if ((threadIdx.x & 63) == 0) out[(int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)] = s;
+  if (lane == 0) out[(int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)] = s;
 }
 
 }  // namespace
 
 double mfma_probe_flops(int blocks, int iters) { return (double)blocks * 4 * iters * kProbeChains * 32.0 * 32 * 16 * 2; }
 
-orbit_status mfma_probe(int blocks, int iters, float x, float* out, hipStream_t s) {
+orbit_status mfma_probe(int blocks, int iters, unsigned seed, float x, float* out, hipStream_t s) {
   KernelInfo ki{"mfma_probe", mfma_probe_flops(blocks, iters), 0.0};
-  return launch(ki, mfma_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, s, iters, x, out);
+  return launch(ki, mfma_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, s, iters, seed, x, out);
 }
 
 }  // namespace orbit

@@ -119,9 +119,10 @@ def test_other_entry_validation(lib):
     assert lib.lib.orbit_attention_fwd(1, 1, 1, 8, 96, 0x100, 96, 0x200, 96, 0x300, 96, 0x400, 96, 0x500,
                                        None, 0, None) == L.ORBIT_E_UNSUPPORTED
     # the matrix-core probe validates its sizes and output before launching
-    assert lib.lib.orbit_mfma_probe(0, 16, 1.0, 0x100, None) == L.ORBIT_E_ARG and "blocks" in lib.last_error()
-    assert lib.lib.orbit_mfma_probe(16, (1 << 20) + 1, 1.0, 0x100, None) == L.ORBIT_E_ARG and "iters" in lib.last_error()
-    assert lib.lib.orbit_mfma_probe(16, 16, 1.0, None, None) == L.ORBIT_E_ARG and "out" in lib.last_error()
+    assert lib.lib.orbit_mfma_probe(0, 16, 0, 1.0, 0x100, None) == L.ORBIT_E_ARG and "blocks" in lib.last_error()
+    assert lib.lib.orbit_mfma_probe(16, (1 << 20) + 1, 0, 1.0, 0x100, None) == L.ORBIT_E_ARG and \
+        "iters" in lib.last_error()
+    assert lib.lib.orbit_mfma_probe(16, 16, 7, 1.0, None, None) == L.ORBIT_E_ARG and "out" in lib.last_error()
 
 
 def test_workspace_sizes_cover_the_configs(lib):

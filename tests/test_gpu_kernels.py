@@ -175,13 +175,29 @@ def test_layernorm(lib, dtype, rows, n):
     check("ln mean", host(mean), x.astype(np.float64).mean(-1), 1e-4)
 
 
+def _probe_pattern(seed, lane, i):
+    """The probe's operand pattern, from its definition in include/orbit.h."""
+    h = ((seed ^ (8 * lane + i)) * 0x9E3779B1) & 0xFFFFFFFF
+    h ^= h >> 15
+    h = (h * 0x85EBCA77) & 0xFFFFFFFF
+    h ^= h >> 13
+    return ((h & 255) - 128) / 64.0
+
+
 @pytest.mark.gpu
-@pytest.mark.parametrize("blocks,iters,x", [(1, 1, 1.0), (256, 64, 1.0), (37, 1000, 0.5), (1024, 3, -2.0)])
-def test_mfma_probe(lib, blocks, iters, x):
-    """The matrix-core probe computes what its contract states: each wave's
-    value is 8 accumulator elements of 16 x^2 per round, exact in float32."""
+@pytest.mark.parametrize("blocks,iters,seed,x", [(1, 1, 0, 1.0), (256, 64, 0, 1.0), (37, 1000, 0, 0.5),
+                                                  (1024, 3, 0, -2.0), (3, 16, 12345, 1.0), (64, 8, 7, 0.25)])
+def test_mfma_probe(lib, blocks, iters, seed, x):
+    """The matrix-core probe computes what its contract states: per wave,
+    8 iters times the summed squares of lanes 0 and 32's operand fragments
+    (16 iters x^2 per accumulator element when seed is 0; exact there)."""
     import torch
     out = torch.full((blocks * 4,), float("nan"), dtype=torch.float32, device="cuda")
-    lib.orbit_mfma_probe(blocks, iters, x, out)
+    lib.orbit_mfma_probe(blocks, iters, seed, x, out)
     torch.cuda.synchronize()
-    assert bool((out == 128.0 * x * x * iters).all())
+    if seed == 0:
+        assert bool((out == 128.0 * x * x * iters).all())
+    else:
+        sq = sum((x * _probe_pattern(seed, l, i)) ** 2 for l in (0, 32) for i in range(8))
+        want = 8.0 * iters * sq
+        assert np.allclose(out.cpu().numpy(), want, rtol=1e-6, atol=0), (out[:4], want)
