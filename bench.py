@@ -356,6 +356,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="113b-shard", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gemm-layouts", action="store_true",
+                    help="run one 4096x4096x8192 product per GEMM operand layout (for hardware counters) and exit")
     ap.add_argument("--no-secondary", action="store_true",
                     help="time only --workload (skip the 10B-shard gate and checkpoint measurements)")
     ap.add_argument("--cpu-baseline-only", action="store_true", help=argparse.SUPPRESS)
@@ -381,6 +383,33 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if a.gemm_layouts:
+        # one 4096x4096x8192 bf16 product per operand layout (forward: A K-major,
+        # B N-major; input gradient: both K-major; weight gradient: A M-major,
+        # B N-major, float32 out), 5 launches each: a short program for
+        # per-layout hardware counters
+        from paper_2404_14712_amd import load as _load
+        glib = _load()
+        M = N = 4096
+        K = 8192
+        res = {}
+        for nm, ak, bk, cf in (("forward", 1, 0, 0), ("input_gradient", 1, 1, 0), ("weight_gradient", 0, 0, 1)):
+            A = torch.randn(M * K, device=dev).to(torch.bfloat16)
+            Bm = torch.randn(K * N, device=dev).to(torch.bfloat16)
+            C = torch.empty(M * N, dtype=torch.float32 if cf else torch.bfloat16, device=dev)
+            ws = torch.empty(max(256, glib.orbit_gemm_workspace_bytes(1, M, N, K, ak, bk)), dtype=torch.uint8,
+                             device=dev)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+            ev[0].record()
+            for i in range(5):
+                glib.orbit_gemm(1, M, N, K, A, K if ak else M, ak, Bm, K if bk else N, bk, C, N, cf, 1.0, None, 0, ws)
+                ev[i + 1].record()
+            torch.cuda.synchronize()
+            ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(5))[2]
+            res[nm] = {"ms": round(ms, 4), "tflops": round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)}
+            del A, Bm, C, ws
+        print(json.dumps({"gemm_layouts": res, "M": M, "N": N, "K": K}), flush=True)
+        return
     if a.copy_calibration:
         # a streaming elementwise kernel that reads and writes exactly 1 GiB each
         n = 1 << 28
