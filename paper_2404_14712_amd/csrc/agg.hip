@@ -219,8 +219,9 @@ __global__ void __launch_bounds__(256) agg_xbar(const bf16* __restrict__ ab, con
     for (int j = 0; j < 8; ++j) acc[h][j] = 0.f;
 #pragma unroll 2
   for (int v = 0; v < V; v += 2) {
-    const u32x4 x0 = __builtin_amdgcn_raw_buffer_load_b128(rx, voff, (unsigned)v * row, 0);
-    const u32x4 x1 = __builtin_amdgcn_raw_buffer_load_b128(rx, voff, (unsigned)(v + 1) * row, 0);
+    // non-temporal loads (cache policy bit 1): the tokens are read once here
+    const u32x4 x0 = __builtin_amdgcn_raw_buffer_load_b128(rx, voff, (unsigned)v * row, 2);
+    const u32x4 x1 = __builtin_amdgcn_raw_buffer_load_b128(rx, voff, (unsigned)(v + 1) * row, 2);
     unsigned p[8];
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -549,6 +550,7 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
     g.C = S; g.ldc = z.H; g.out_f32 = true;
     g.M = (int)TV; g.N = z.H; g.K = z.d;
     g.alpha = 1.f / sqrtf((float)z.dh);
+    g.stream = true;  // the token tensor is read once here
     ORBIT_TRY(gemm(g, gws, gws_bytes, s));
   }
   // 3. softmax over variables

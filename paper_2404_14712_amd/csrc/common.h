@@ -36,6 +36,11 @@ template <typename T> struct E16c { static constexpr int v = 16 / (int)sizeof(T)
 struct alignas(16) U128 { uint32_t w[4]; };
 
 ORBIT_DEV U128 ld128(const void* p) { return *reinterpret_cast<const U128*>(p); }
+// non-temporal load (data read once: streamed past the caches' normal retention)
+ORBIT_DEV U128 ld128nt(const void* p) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(U128, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+}
 ORBIT_DEV void st128(void* p, const U128& v) { *reinterpret_cast<U128*>(p) = v; }
 ORBIT_DEV U128 zero128() { U128 z; z.w[0] = z.w[1] = z.w[2] = z.w[3] = 0u; return z; }
 

@@ -33,6 +33,9 @@ struct Gemm {
   float* bsum = nullptr;
   int bsum_max_parts = 1;
   orbit_dtype dtype = ORBIT_BF16;                // operand type of A and B
+  // operands read once by this product (bf16, both K-major, 64x64 tiles): their
+  // tiles are loaded non-temporally
+  bool stream = false;
   const char* tag = "gemm";                      // name prefix for timing
 };
 

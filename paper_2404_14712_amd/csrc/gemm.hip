@@ -124,11 +124,14 @@ ORBIT_DEV void epi_apply8(const Epi& e, int64_t bz, int r, int c0, float* v, Out
 
 // operand staging: K-major tiles (and every float32 tile) as K-contiguous LDS
 // rows; bf16 M/N-major tiles as they are, read through transposing LDS reads
-template <typename T, bool KMAJ, int ROWS, int KD, int NT>
+template <typename T, bool KMAJ, int ROWS, int KD, int NT, bool NTL = false>
 using StageOf = std::conditional_t<(!KMAJ && sizeof(T) == 2), GemmStageMN<ROWS, KD, NT>,
-                                   GemmStage<T, ROWS, KD, NT, KMAJ>>;
+                                   GemmStage<T, ROWS, KD, NT, KMAJ, NTL>>;
 
-template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+// STREAM: the K-major operand tiles are loaded non-temporally (products whose
+// operands are read once, e.g. the aggregation's score product over the
+// token tensor)
+template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM, bool STREAM = false>
 __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   constexpr int NT = WM * WN * 64;
   constexpr int BKE = 128 / (int)sizeof(T);
@@ -136,8 +139,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_kernel(GemmKArgs g) {
   static_assert(TM >= 1 && TN >= 1, "wave tile must be at least 32x32");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T* lds = reinterpret_cast<T*>(smem);
-  using SA = StageOf<T, AK, BM, BKE, NT>;
-  using SB = StageOf<T, BKM, BN, BKE, NT>;
+  using SA = StageOf<T, AK, BM, BKE, NT, STREAM>;
+  using SB = StageOf<T, BKM, BN, BKE, NT, STREAM>;
   constexpr int STAGE = SA::SIZE + SB::SIZE;
   static_assert((WM * WN) * 32 * (BN / WN + 8) * 4 <= 2 * STAGE * (int)sizeof(T), "epilogue fits the stages");
 
@@ -826,36 +829,37 @@ orbit_status run_dma(const Gemm& g, GemmKArgs& a, hipStream_t s) {
   return a.splits > 1 ? splitk_finish<OutT>(g, a, s) : ORBIT_OK;
 }
 
-template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM, bool STREAM>
 const char* kname() {
   static std::string s = [] {
     char b[160];
-    snprintf(b, sizeof b, "gemm_kernel<%s,%s,%d,%d,%d,%d,%s,%s>", sizeof(T) == 2 ? "bf16" : "f32",
-             sizeof(OutT) == 2 ? "bf16" : "f32", BM, BN, WM, WN, AK ? "AK" : "AM", BKM ? "BK" : "BN");
+    snprintf(b, sizeof b, "gemm_kernel<%s,%s,%d,%d,%d,%d,%s,%s%s>", sizeof(T) == 2 ? "bf16" : "f32",
+             sizeof(OutT) == 2 ? "bf16" : "f32", BM, BN, WM, WN, AK ? "AK" : "AM", BKM ? "BK" : "BN",
+             STREAM ? ",stream" : "");
     return std::string(b);
   }();
   return s.c_str();
 }
 
-template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+template <typename T, typename OutT, int BM, int BN, int WM, int WN, bool AK, bool BKM, bool STREAM = false>
 orbit_status run_cfg(const Gemm& g, GemmKArgs& a, hipStream_t s) {
   const double flops = 2.0 * g.M * g.N * (double)g.K * g.batch;
   const double bytes = ((double)g.M * g.K + (double)g.K * g.N) * sizeof(T) * g.batch +
                        (double)g.M * g.N * sizeof(OutT) * g.batch;
-  KernelInfo ki{kname<T, OutT, BM, BN, WM, WN, AK, BKM>(), flops, bytes};
+  KernelInfo ki{kname<T, OutT, BM, BN, WM, WN, AK, BKM, STREAM>(), flops, bytes};
   dim3 grid((unsigned)(cdiv(g.N, BN) * cdiv(g.M, BM)), 1, (unsigned)(g.batch * a.splits));
   constexpr int NT = WM * WN * 64, BKE = 128 / (int)sizeof(T);
   constexpr size_t lds = 2 * (size_t)(StageOf<T, AK, BM, BKE, NT>::SIZE + StageOf<T, BKM, BN, BKE, NT>::SIZE) * sizeof(T);
   static const bool attr = [] {
     // lift the default dynamic-LDS cap for this instantiation (a failure here
     // surfaces as a launch error below)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM, STREAM>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     (void)hipGetLastError();
     return true;
   }();
   (void)attr;
-  ORBIT_TRY(launch(ki, gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM>, grid, dim3(WM * WN * 64), lds, s, a));
+  ORBIT_TRY(launch(ki, gemm_kernel<T, OutT, BM, BN, WM, WN, AK, BKM, STREAM>, grid, dim3(WM * WN * 64), lds, s, a));
   return a.splits > 1 ? splitk_finish<OutT>(g, a, s) : ORBIT_OK;
 }
 
@@ -883,6 +887,9 @@ orbit_status run_layout(const Gemm& g, GemmKArgs& a, const TileCfg& t, hipStream
     if (t.BM == 256 && t.BN == 256 && t.WM == 4) return run_cfg<T, OutT, 256, 256, 4, 2, AK, BKM>(g, a, s);
   }
   if (t.BM == 128 && t.BN == 128) return run_cfg<T, OutT, 128, 128, 2, 2, AK, BKM>(g, a, s);
+  if constexpr (sizeof(T) == 2 && AK && BKM) {
+    if (g.stream && t.BM == 64 && t.BN == 64) return run_cfg<T, OutT, 64, 64, 2, 2, AK, BKM, true>(g, a, s);
+  }
   if (t.BM == 128 && t.BN == 32) return run_cfg<T, OutT, 128, 32, 4, 1, AK, BKM>(g, a, s);
   if (t.BM == 32 && t.BN == 128) return run_cfg<T, OutT, 32, 128, 1, 4, AK, BKM>(g, a, s);
   return run_cfg<T, OutT, 64, 64, 2, 2, AK, BKM>(g, a, s);

@@ -145,7 +145,8 @@ namespace orbit {
 // source each thread owns an E x E block (E k-rows of E row-elements), loads
 // it as E 16-byte reads (a wave reads 8 rows x 128 contiguous bytes per
 // instruction), transposes it in registers and writes E 16-byte k-runs.
-template <typename T, int ROWS, int KD, int NT, bool KMAJ>
+// NTL: K-major tiles loaded non-temporally (operands the product reads once)
+template <typename T, int ROWS, int KD, int NT, bool KMAJ, bool NTL = false>
 struct GemmStage {
   static constexpr int E = 16 / (int)sizeof(T);
   static constexpr int KC = KD / E;                 // 16-byte chunks per row
@@ -170,7 +171,8 @@ struct GemmStage {
       if (KMAJ) {
         const int row = c / KC, kc = c % KC;
         const int gr = row0 + row, gk = k0 + kc * E;
-        r[i] = (c < NCH && gr < rlim && gk < kend) ? ld128(X + (int64_t)gr * ld + gk) : zero128();
+        const T* src = X + (int64_t)gr * ld + gk;
+        r[i] = (c < NCH && gr < rlim && gk < kend) ? (NTL ? ld128nt(src) : ld128(src)) : zero128();
       } else {
         const int kc = c % KC, rc = c / KC;
         const int gr = row0 + rc * E;
