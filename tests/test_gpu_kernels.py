@@ -104,11 +104,13 @@ def test_attention_wide_heads(lib, dh, L):
 def test_attention_split_backward(lib, dtype, dh):
     """2 samples x 3 heads x 600 positions is a grid of 30 blocks: the bf16
     backward splits its sweeps over two blocks each and merges the float32
-    partials; 600 leaves partial key and query tiles in the second split."""
-    _attention_case(lib, dtype, dh, 600, 1.0)
+    partials; 600 leaves partial key and query tiles in the second split.
+    Two runs give bitwise-identical gradients (the merges add in a fixed
+    order)."""
+    _attention_case(lib, dtype, dh, 600, 1.0, repeat=True)
 
 
-def _attention_case(lib, dtype, dh, L, qk_scale):
+def _attention_case(lib, dtype, dh, L, qk_scale, repeat=False):
     import torch
     B, H = 2, 3
     A = H * dh
@@ -131,6 +133,14 @@ def _attention_case(lib, dtype, dh, L, qk_scale):
     lib.orbit_attention_bwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o32, A, 1, lse, dOd, A, ge,
                             ge + A * e, ge + 2 * A * e, 3 * A, Dws)
     torch.cuda.synchronize()
+    if repeat:
+        # a second run on the same inputs into a fresh buffer: bitwise equal
+        g2 = torch.zeros_like(g)
+        g2e = g2.data_ptr()
+        lib.orbit_attention_bwd(CODE[dtype], B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o32, A, 1, lse, dOd, A, g2e,
+                                g2e + A * e, g2e + 2 * A * e, 3 * A, Dws)
+        torch.cuda.synchronize()
+        assert torch.equal(g, g2), "attention backward is not bitwise reproducible"
     hd = lambda x: x.reshape(B, L, H, dh).transpose(0, 2, 1, 3)
     Q, K_, V_ = hd(qkv[:, :A]), hd(qkv[:, A:2 * A]), hd(qkv[:, 2 * A:])
     ref_o, P = O.attention_fwd(Q, K_, V_)
