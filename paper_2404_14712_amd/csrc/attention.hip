@@ -1560,8 +1560,6 @@ orbit_status bwd_t(const AttnIO& io, const void* o, int64_t ldo, int o_f32, cons
 
 }  // namespace
 
-size_t attn_split_bytes(int B, int H, int L, int dh) { return split_bytes(B, H, L, dh); }
-
 size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh) {
   return attn_bwd_base_bytes(B, H, L, dh) + split_bytes(B, H, L, dh);
 }

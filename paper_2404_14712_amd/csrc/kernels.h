@@ -77,12 +77,10 @@ struct AttnIO {
   int B, H, L, dh;
 };
 // o32 (optional): float32 copy of O, used by the backward for rowsum(dO * O).
-// scratch (optional, scratch_bytes >= attn_split_bytes): with it, bf16 grids of
-// few blocks split the keys over two blocks and merge their partials
+// scratch (optional; attn_bwd_workspace_bytes always suffices): with it, bf16
+// grids of few blocks split the keys over two blocks and merge their partials
 orbit_status attn_fwd(orbit_dtype dt, const AttnIO& io, void* o, int64_t ldo, float* lse, float* o32, int64_t ldo32,
                       void* scratch, size_t scratch_bytes, hipStream_t s);
-// float32 partials of a split launch (0 when the grid is not split)
-size_t attn_split_bytes(int B, int H, int L, int dh);
 // workspace of attn_bwd: D[b,h,l] = rowsum(dO * O), sums of q and k over the
 // sequence, the column-reduction scratch and the partials of a split launch
 size_t attn_bwd_workspace_bytes(int B, int H, int L, int dh);
