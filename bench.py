@@ -39,8 +39,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-WORKLOADS = {"115m": 2, "1b": 3, "10b-shard": 4, "113b-shard": 5, "tiny": 1, "10b-paper-tp8": 6,
-             "113b-paper-tp8": 7}
+import synth  # noqa: E402  (seeded shapes and inputs; no arithmetic of the model)
+
 GATE_PCT = 50.0
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3      # MI355X fp32
@@ -75,7 +75,6 @@ def device_inputs(c, device):
     import numpy as np
     import torch
 
-    import synth
 
     def D(a, dt=None):
         dt = dt or c.dtype
@@ -96,13 +95,13 @@ def device_inputs(c, device):
         inputs["tgt"] = D(synth.target(c), "f32")
     else:
         # activations and the upstream gradient N(0, 1), drawn on the device (seeded)
-        inputs["dy"] = synth.device_normal(c.cfg, "dy", (c.B, c.L, c.d), c.dtype, device)
+        inputs["dy"] = synth.device_normal(c.seed, "dy", (c.B, c.L, c.d), c.dtype, device)
         if z.mode == "agg_blocks":
             params["agg"] = P(synth.agg_params(c))
-            inputs["tok"] = synth.device_normal(c.cfg, "tok", (c.B * c.L, c.V, c.d), c.dtype, device,
+            inputs["tok"] = synth.device_normal(c.seed, "tok", (c.B * c.L, c.V, c.d), c.dtype, device,
                                                 chunk_rows=256).view(c.B, c.L, c.V, c.d)
         else:
-            inputs["x"] = synth.device_normal(c.cfg, "x", (c.B, c.L, c.d), c.dtype, device)
+            inputs["x"] = synth.device_normal(c.seed, "x", (c.B, c.L, c.d), c.dtype, device)
     return params, inputs
 
 
@@ -130,9 +129,8 @@ def cpu_baseline_child(workload: str) -> dict:
     import numpy as np
 
     import oracle as O
-    import synth
 
-    c = synth.CONFIGS[WORKLOADS[workload]]
+    c = synth.CONFIGS[workload]
     mode = "full" if c.full_model else ("agg_blocks" if c.agg_only_prefix else "blocks")
     if mode == "full":
         Hg, Wg = c.grid
@@ -152,7 +150,7 @@ def cpu_baseline_child(workload: str) -> dict:
                 synth.head_params(s))
     else:
         x0 = synth.activations(s, "x")
-        dy = synth.normal(s.cfg, "dy", x0.shape)
+        dy = synth.normal(s.seed, "dy", x0.shape)
         if mode == "agg_blocks":
             tok = np.stack([synth.tokens_chunk(s, b, 0, s.L) for b in range(s.B)])
             agg = synth.agg_params(s)
@@ -354,7 +352,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="113b-shard", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="113b-shard", choices=sorted(synth.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm-layouts", action="store_true",
                     help="run one 4096x4096x8192 product per GEMM operand layout (for hardware counters) and exit")
@@ -377,7 +375,6 @@ def main():
 
     import torch
 
-    import synth
     from paper_2404_14712_amd import load
     from paper_2404_14712_amd.model import recompute_flops
 
@@ -422,7 +419,7 @@ def main():
                                                "read_bytes_per_launch": 4 * n, "write_bytes_per_launch": 4 * n}}))
         return
     lib = load()
-    c = synth.CONFIGS[WORKLOADS[a.workload]]
+    c = synth.CONFIGS[a.workload]
     peak = PEAK_BF16_TFLOPS if c.dtype == "bf16" else PEAK_F32_TFLOPS
     r = measure(lib, c, a.steps, a.warmup, dev)
     flops, tot, dominant = r["flops"], r["kernels"], r["dominant"]
@@ -512,7 +509,7 @@ def main():
         if a.workload in ("113b-shard", "10b-shard"):
             gate[a.workload + " blocks"] = dict(blocks, **{"pass": blocks["pct_peak"] >= GATE_PCT})
             del gate[a.workload + " blocks"]["note"]
-        c4 = synth.CONFIGS[WORKLOADS["10b-shard"]]
+        c4 = synth.CONFIGS["10b-shard"]
         z4 = dims_for(c4)
         if a.workload != "10b-shard":
             r4 = measure(lib, c4, a.steps, a.warmup, dev, instrument=False)

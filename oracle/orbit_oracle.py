@@ -25,8 +25,8 @@ Every function is the plain definition in float64 with NumPy: a matmul is the
 only library primitive used (plus ``scipy.special.erf`` for the Gaussian CDF).
 Attention is materialised, the aggregation runs its full key/value projections
 (no algebraic folding), and every backward is the hand-derived adjoint of the
-forward written next to it. Readings of points the paper leaves open are
-listed in the design doc and restated at each function.
+forward written next to it. Each function states the reading it takes of
+any point the paper leaves open.
 
 Pins (tests/test_oracle_*.py): central finite differences for every backward,
 a float64 PyTorch-CPU autograd cross-check (independent library code), softmax

@@ -11,7 +11,7 @@ i.i.d. normal fields per variable reproduce the shapes and the unit dynamic
 range of normalised climate variables.
 
 Seeding: every tensor has a name; its generator is
-``numpy.random.Generator(PCG64(SeedSequence([240414712, cfg, crc32(name)])))``,
+``numpy.random.Generator(PCG64(SeedSequence([240414712, seed, crc32(name)])))``,
 so any tensor can be regenerated alone, in any order.
 """
 from __future__ import annotations
@@ -29,7 +29,7 @@ PATCH = 4
 @dataclasses.dataclass(frozen=True)
 class Config:
     """One workload. ``heads``/``mlp``/``attn_dim`` are the LOCAL (per-GPU) sizes."""
-    cfg: int
+    seed: int             # seed stream of the workload's tensors
     name: str
     dtype: str            # "f32" or "bf16"
     B: int
@@ -67,34 +67,34 @@ class Config:
         return self.V * PATCH * PATCH
 
 
-CONFIGS: Dict[int, Config] = {
-    1: Config(1, "tiny ClimaX-style ViT, fp32", "f32", B=2, L=128, d=128, blocks=2,
+CONFIGS: Dict[str, Config] = {
+    "tiny": Config(1, "tiny ClimaX-style ViT, fp32", "f32", B=2, L=128, d=128, blocks=2,
               heads=4, head_dim=32, mlp=512, sigma=0.02, V=4, grid=(32, 64),
               agg_heads=4, agg_head_dim=32, full_model=True),
-    2: Config(2, "115M-scale ViT (d=1024, 8 blocks, V=48)", "bf16", B=4, L=2048, d=1024,
+    "115m": Config(2, "115M-scale ViT (d=1024, 8 blocks, V=48)", "bf16", B=4, L=2048, d=1024,
               blocks=8, heads=16, head_dim=64, mlp=4096, sigma=0.02, V=48,
               grid=(128, 256), agg_heads=16, agg_head_dim=64, full_model=True),
-    3: Config(3, "1B-scale ViT (d=2048, 16 blocks, V=91)", "bf16", B=2, L=2048, d=2048,
+    "1b": Config(3, "1B-scale ViT (d=2048, 16 blocks, V=91)", "bf16", B=2, L=2048, d=2048,
               blocks=16, heads=16, head_dim=128, mlp=8192, sigma=0.02, V=91,
               grid=(128, 256), agg_heads=16, agg_head_dim=128, full_model=True,
               var_scale=True),
-    4: Config(4, "10B-scale tensor-parallel shard (d=8192, TP 8), 4 blocks", "bf16", B=2,
+    "10b-shard": Config(4, "10B-scale tensor-parallel shard (d=8192, TP 8), 4 blocks", "bf16", B=2,
               L=2048, d=8192, blocks=4, heads=8, head_dim=128, mlp=4096, sigma=0.01),
-    5: Config(5, "113B-scale tensor-parallel shard (d=16384, TP 16), aggregation + 2 blocks",
+    "113b-shard": Config(5, "113B-scale tensor-parallel shard (d=16384, TP 16), aggregation + 2 blocks",
               "bf16", B=1, L=2048, d=16384, blocks=2, heads=8, head_dim=128, mlp=4096,
               sigma=0.005, V=91, agg_heads=8, agg_head_dim=128, agg_only_prefix=True),
     # the paper's own widths (Sec. IV) under tensor parallelism over the 8 GPUs
     # of a node (the paper's best 113B layout, Sec. V-C, is FSDP x TP 8)
-    6: Config(6, "10B model's tensor-parallel shard at the paper's widths (d=8192, 4 of 32 heads of 256, TP 8), "
+    "10b-paper-tp8": Config(6, "10B model's tensor-parallel shard at the paper's widths (d=8192, 4 of 32 heads of 256, TP 8), "
                  "4 blocks", "bf16", B=2, L=2048, d=8192, blocks=4, heads=4, head_dim=256, mlp=4096, sigma=0.01),
-    7: Config(7, "113B model's tensor-parallel shard at the paper's widths (d=12288, 8 of 64 heads of 192, TP 8), "
+    "113b-paper-tp8": Config(7, "113B model's tensor-parallel shard at the paper's widths (d=12288, 8 of 64 heads of 192, TP 8), "
                  "2 blocks", "bf16", B=1, L=2048, d=12288, blocks=2, heads=8, head_dim=192, mlp=6144,
               sigma=0.005),
 }
 
 
-def rng(cfg: int, name: str) -> np.random.Generator:
-    ss = np.random.SeedSequence([BASE_SEED, int(cfg), zlib.crc32(name.encode())])
+def rng(seed: int, name: str) -> np.random.Generator:
+    ss = np.random.SeedSequence([BASE_SEED, int(seed), zlib.crc32(name.encode())])
     return np.random.Generator(np.random.PCG64(ss))
 
 
@@ -117,9 +117,9 @@ def _cast(a: np.ndarray, dtype: str) -> np.ndarray:
     return bf16_round(a) if dtype == "bf16" else a
 
 
-def normal(cfg: int, name: str, shape, std: float = 1.0, mean: float = 0.0,
+def normal(seed: int, name: str, shape, std: float = 1.0, mean: float = 0.0,
            dtype: str = "f32") -> np.ndarray:
-    g = rng(cfg, name)
+    g = rng(seed, name)
     a = g.standard_normal(size=shape, dtype=np.float32)
     if std != 1.0:
         a *= np.float32(std)
@@ -171,7 +171,7 @@ def _is_ln_gain(name: str) -> bool:
     return name.endswith("_g")
 
 
-def make_params(cfg: int, prefix: str, shapes: Dict[str, tuple], sigma: float,
+def make_params(seed: int, prefix: str, shapes: Dict[str, tuple], sigma: float,
                 dtype: str) -> Dict[str, np.ndarray]:
     """Every matrix, bias, embedding and the query ~ N(0, sigma);
     LayerNorm gains ~ 1 + N(0, sigma) and shifts ~ N(0, sigma)."""
@@ -179,9 +179,9 @@ def make_params(cfg: int, prefix: str, shapes: Dict[str, tuple], sigma: float,
     for name, shape in shapes.items():
         full = f"{prefix}.{name}"
         if _is_ln_gain(name):
-            out[name] = normal(cfg, full, shape, std=sigma, mean=1.0, dtype=dtype)
+            out[name] = normal(seed, full, shape, std=sigma, mean=1.0, dtype=dtype)
         else:
-            out[name] = normal(cfg, full, shape, std=sigma, dtype=dtype)
+            out[name] = normal(seed, full, shape, std=sigma, dtype=dtype)
     return out
 
 
@@ -190,39 +190,39 @@ def block_params(c: Config, i: int, d=None, A=None, F=None, dh=None) -> Dict[str
     A = c.A if A is None else A
     F = c.mlp if F is None else F
     dh = c.head_dim if dh is None else dh
-    return make_params(c.cfg, f"block{i}", block_param_shapes(d, A, F, dh), c.sigma, c.dtype)
+    return make_params(c.seed, f"block{i}", block_param_shapes(d, A, F, dh), c.sigma, c.dtype)
 
 
 def agg_params(c: Config) -> Dict[str, np.ndarray]:
-    return make_params(c.cfg, "agg", agg_param_shapes(c.d, c.agg_A, c.L), c.sigma, c.dtype)
+    return make_params(c.seed, "agg", agg_param_shapes(c.d, c.agg_A, c.L), c.sigma, c.dtype)
 
 
 def embed_params(c: Config) -> Dict[str, np.ndarray]:
-    return make_params(c.cfg, "embed", embed_param_shapes(c.V, c.d), c.sigma, c.dtype)
+    return make_params(c.seed, "embed", embed_param_shapes(c.V, c.d), c.sigma, c.dtype)
 
 
 def head_params(c: Config, hidden: int = 0) -> Dict[str, np.ndarray]:
-    return make_params(c.cfg, "head", head_param_shapes(c.d, c.out_dim, hidden), c.sigma, c.dtype)
+    return make_params(c.seed, "head", head_param_shapes(c.d, c.out_dim, hidden), c.sigma, c.dtype)
 
 
 def image(c: Config) -> np.ndarray:
-    """img[B, V, Hg, Wg] float32; cfg3-style per-variable scale s_v ~ U(0.5, 2)."""
+    """img[B, V, Hg, Wg] float32; with var_scale, a per-variable scale s_v ~ U(0.5, 2)."""
     Hg, Wg = c.grid
-    img = normal(c.cfg, "img", (c.B, c.V, Hg, Wg))
+    img = normal(c.seed, "img", (c.B, c.V, Hg, Wg))
     if c.var_scale:
-        s = rng(c.cfg, "img.var_scale").uniform(0.5, 2.0, size=c.V).astype(np.float32)
+        s = rng(c.seed, "img.var_scale").uniform(0.5, 2.0, size=c.V).astype(np.float32)
         img *= s[None, :, None, None]
     return img
 
 
 def target(c: Config) -> np.ndarray:
     """tgt[B, L, V*p*p] float32, token layout."""
-    return normal(c.cfg, "tgt", (c.B, c.L, c.out_dim))
+    return normal(c.seed, "tgt", (c.B, c.L, c.out_dim))
 
 
 def activations(c: Config, name: str = "x") -> np.ndarray:
     """x[B, L, d] ~ N(0, 1) in the config's dtype."""
-    return normal(c.cfg, name, (c.B, c.L, c.d), dtype=c.dtype)
+    return normal(c.seed, name, (c.B, c.L, c.d), dtype=c.dtype)
 
 
 def tokens_chunk(c: Config, b: int, l0: int, l1: int) -> np.ndarray:
@@ -233,19 +233,19 @@ def tokens_chunk(c: Config, b: int, l0: int, l1: int) -> np.ndarray:
     out = np.empty((l1 - l0, c.V, c.d), np.float32)
     for ch in range(l0 // CH, (l1 + CH - 1) // CH):
         a, bnd = ch * CH, min((ch + 1) * CH, c.L)
-        blk = normal(c.cfg, f"tok.b{b}.c{ch}", (bnd - a, c.V, c.d), dtype=c.dtype)
+        blk = normal(c.seed, f"tok.b{b}.c{ch}", (bnd - a, c.V, c.d), dtype=c.dtype)
         s0, s1 = max(a, l0), min(bnd, l1)
         out[s0 - l0:s1 - l0] = blk[s0 - a:s1 - a]
     return out
 
 
-def small_config(cfg: int, **over) -> Config:
+def small_config(workload: str, **over) -> Config:
     """A copy of a config with some sizes replaced (parity cases that the oracle
     finishes in seconds)."""
-    return dataclasses.replace(CONFIGS[cfg], **over)
+    return dataclasses.replace(CONFIGS[workload], **over)
 
 
-def device_normal(cfg: int, name: str, shape, dtype: str, device, chunk_rows: int = 0):
+def device_normal(seed: int, name: str, shape, dtype: str, device, chunk_rows: int = 0):
     """N(0, 1) tensor drawn on the device by torch's seeded generator, for
     inputs too large to draw on the host (full-size token and activation
     tensors). Drawn in float32 and rounded to the dtype. With ``chunk_rows``,
@@ -253,7 +253,7 @@ def device_normal(cfg: int, name: str, shape, dtype: str, device, chunk_rows: in
     temporary). Deterministic for a given device type and torch version."""
     import torch
     gen = torch.Generator(device=device)
-    gen.manual_seed((BASE_SEED * 1000 + int(cfg) * 7919 + zlib.crc32(name.encode())) % (2 ** 63))
+    gen.manual_seed((BASE_SEED * 1000 + int(seed) * 7919 + zlib.crc32(name.encode())) % (2 ** 63))
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     out = torch.empty(*shape, dtype=tdt, device=device)
     n0 = shape[0]

@@ -41,7 +41,7 @@ def _rel(got, ref, sib):
 
 
 def test_bf16_floor_reduced_model():
-    c = synth.small_config(2, B=2, L=128, grid=(32, 64), V=12, d=256, blocks=2, heads=4, head_dim=64, mlp=1024,
+    c = synth.small_config("115m", B=2, L=128, grid=(32, 64), V=12, d=256, blocks=2, heads=4, head_dim=64, mlp=1024,
                            agg_heads=8, agg_head_dim=32, sigma=0.05)
     args = (synth.image(c), synth.target(c), synth.embed_params(c), synth.agg_params(c),
             [synth.block_params(c, i) for i in range(c.blocks)], synth.head_params(c))

@@ -98,14 +98,14 @@ def _shard_chain(lib, key, c, keep=(0,)):
     from paper_2404_14712_amd.model import ViTPass
     try:
         blocks = [synth.block_params(c, i) for i in range(c.blocks)]
-        dy = synth.normal(c.cfg, "dy", (c.B, c.L, c.d), dtype=c.dtype)
+        dy = synth.normal(c.seed, "dy", (c.B, c.L, c.d), dtype=c.dtype)
         drop = [b for b in range(c.B) if b not in keep]
         dy[drop] = 0.0
         keep = list(keep)
         params = {"blocks": [_dev_params(b, c.dtype) for b in blocks]}
         tok = agg = x = None
         if c.agg_only_prefix:
-            tok = synth.normal(c.cfg, "tok", (c.B, c.L, c.V, c.d), dtype=c.dtype)
+            tok = synth.normal(c.seed, "tok", (c.B, c.L, c.V, c.d), dtype=c.dtype)
             agg = synth.agg_params(c)
             params["agg"] = _dev_params(agg, c.dtype)
             mode, inputs = "agg_blocks", {"tok": dev(tok, c.dtype), "dy": dev(dy, c.dtype)}
@@ -142,10 +142,10 @@ def _shard_chain(lib, key, c, keep=(0,)):
 
 
 CHAINS = {
-    "115m": lambda lib: _full_model(lib, "115m", synth.small_config(2, B=1)),
-    "1b": lambda lib: _full_model(lib, "1b", synth.small_config(3, B=1)),
-    "10b-shard": lambda lib: _shard_chain(lib, "10b-shard", synth.CONFIGS[4]),
-    "113b-shard": lambda lib: _shard_chain(lib, "113b-shard", synth.small_config(5, L=512)),
+    "115m": lambda lib: _full_model(lib, "115m", synth.small_config("115m", B=1)),
+    "1b": lambda lib: _full_model(lib, "1b", synth.small_config("1b", B=1)),
+    "10b-shard": lambda lib: _shard_chain(lib, "10b-shard", synth.CONFIGS["10b-shard"]),
+    "113b-shard": lambda lib: _shard_chain(lib, "113b-shard", synth.small_config("113b-shard", L=512)),
 }
 
 
@@ -175,10 +175,10 @@ def test_chain_qkln(lib, key):
 def test_shard_sum_gpu(lib, K, branch):
     import torch
     from paper_2404_14712_amd._lib import BlockDesc
-    c = synth.small_config(4, B=1, L=512)
+    c = synth.small_config("10b-shard", B=1, L=512)
     H, F, d, dh = c.heads, c.mlp, c.d, c.head_dim
     x = synth.activations(c, "x")
-    dy = synth.normal(c.cfg, "dy", x.shape, dtype=c.dtype)
+    dy = synth.normal(c.seed, "dy", x.shape, dtype=c.dtype)
     prm = synth.block_params(c, 0)
     # one sub-layer at a time: the other branch's output weights and bias are zero
     zero = ("w_fc2", "b_fc2") if branch == "attention" else ("w_proj", "b_proj")

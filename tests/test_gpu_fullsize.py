@@ -26,7 +26,7 @@ def _dev_params(p: dict, dtype: str):
 
 def _sample_patches(c: synth.Config, per_batch: int):
     """(batch, patch) pairs: the first and last patch of every sample plus seeded others."""
-    r = synth.rng(c.cfg, "fullsize.patches")
+    r = synth.rng(c.seed, "fullsize.patches")
     bs, ls = [], []
     for b in range(c.B):
         pick = {0, c.L - 1} | set(r.choice(c.L, size=per_batch - 2, replace=False).tolist())
@@ -40,16 +40,16 @@ def _sample_patches(c: synth.Config, per_batch: int):
 # transformer block: 115M (B=4, d=1024), 1B (B=2, d=2048), 10B shard
 # (d=8192, 8 of 64 heads, MLP 4096 of 32768), 113B shard (d=16384)
 # ---------------------------------------------------------------------------
-BLOCK_FULL = [(2, (0, 3)), (3, (1,)), (4, (0,)), (5, (0,))]
+BLOCK_FULL = [("115m", (0, 3)), ("1b", (1,)), ("10b-shard", (0,)), ("113b-shard", (0,))]
 
 
-@pytest.mark.parametrize("cfg,keep", BLOCK_FULL, ids=["115m", "1b", "10b-shard", "113b-shard"])
-def test_block_full_size(lib, cfg, keep):
+@pytest.mark.parametrize("workload,keep", BLOCK_FULL, ids=[w for w, _ in BLOCK_FULL])
+def test_block_full_size(lib, workload, keep):
     import torch
     from paper_2404_14712_amd._lib import BlockDesc
-    c = synth.CONFIGS[cfg]
+    c = synth.CONFIGS[workload]
     x = synth.activations(c, "x")
-    dy = synth.normal(c.cfg, "dy", x.shape, dtype=c.dtype)
+    dy = synth.normal(c.seed, "dy", x.shape, dtype=c.dtype)
     drop = [b for b in range(c.B) if b not in keep]
     dy[drop] = 0.0
     prm = synth.block_params(c, 0)
@@ -94,9 +94,9 @@ PAPER_SHAPES = {
 def test_block_paper_shapes(lib, name):
     import torch
     from paper_2404_14712_amd._lib import BlockDesc
-    c = synth.small_config(4, B=1, L=2048, **PAPER_SHAPES[name])
+    c = synth.small_config("10b-shard", B=1, L=2048, **PAPER_SHAPES[name])
     x = synth.activations(c, "x")
-    dy = synth.normal(c.cfg, "dy", x.shape, dtype=c.dtype)
+    dy = synth.normal(c.seed, "dy", x.shape, dtype=c.dtype)
     prm = synth.block_params(c, 0)
     desc = BlockDesc(c.B, c.L, c.d, c.heads, c.head_dim, c.mlp, c.qk_norm, c.eps, 1)
     saved = torch.empty(lib.orbit_vit_block_saved_bytes(desc), dtype=torch.uint8, device="cuda")
@@ -123,16 +123,17 @@ def test_block_paper_shapes(lib, name):
 # ---------------------------------------------------------------------------
 # aggregation: 115M (V=48), 1B (V=91), 113B shard (V=91, d=16384, 8 of 128 heads)
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("cfg,per_batch", [(2, 8), (3, 8), (5, 12)], ids=["115m", "1b", "113b-shard"])
-def test_var_aggregate_full_size(lib, cfg, per_batch):
+@pytest.mark.parametrize("workload,per_batch", [("115m", 8), ("1b", 8), ("113b-shard", 12)],
+                         ids=["115m", "1b", "113b-shard"])
+def test_var_aggregate_full_size(lib, workload, per_batch):
     import torch
     from paper_2404_14712_amd._lib import AggDesc
-    c = synth.CONFIGS[cfg]
+    c = synth.CONFIGS[workload]
     B, L, V, d, H = c.B, c.L, c.V, c.d, c.agg_heads
-    tok = synth.device_normal(c.cfg, "tok", (B * L, V, d), c.dtype, "cuda", chunk_rows=256).view(B, L, V, d)
+    tok = synth.device_normal(c.seed, "tok", (B * L, V, d), c.dtype, "cuda", chunk_rows=256).view(B, L, V, d)
     prm = synth.agg_params(c)
     bs, ls = _sample_patches(c, per_batch)
-    dz_s = synth.normal(c.cfg, "fullsize.dz", (len(bs), d), dtype=c.dtype)
+    dz_s = synth.normal(c.seed, "fullsize.dz", (len(bs), d), dtype=c.dtype)
     dz = torch.zeros(B, L, d, dtype=torch.bfloat16, device="cuda")
     dz[torch.from_numpy(bs), torch.from_numpy(ls)] = dev(dz_s, c.dtype)
     desc = AggDesc(B, L, V, d, H, c.agg_head_dim, 1)
@@ -173,17 +174,17 @@ def test_var_aggregate_full_size(lib, cfg, per_batch):
 # ---------------------------------------------------------------------------
 # patch embedding: 115M (4 x 48 variables), 1B (2 x 91 variables, scaled fields)
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("cfg", [2, 3], ids=["115m", "1b"])
-def test_patch_embed_full_size(lib, cfg):
+@pytest.mark.parametrize("workload", ["115m", "1b"])
+def test_patch_embed_full_size(lib, workload):
     import torch
     from paper_2404_14712_amd._lib import EmbedDesc
-    c = synth.CONFIGS[cfg]
+    c = synth.CONFIGS[workload]
     B, L, V, d = c.B, c.L, c.V, c.d
     Hg, Wg = c.grid
     img = synth.image(c)
     e = synth.embed_params(c)
     bs, ls = _sample_patches(c, 8)
-    dtok_s = synth.normal(c.cfg, "fullsize.dtok", (len(bs), V, d), dtype=c.dtype)
+    dtok_s = synth.normal(c.seed, "fullsize.dtok", (len(bs), V, d), dtype=c.dtype)
     desc = EmbedDesc(B, V, Hg, Wg, 4, d, 1)
     tok = torch.empty(B, L, V, d, dtype=torch.bfloat16, device="cuda")
     dtok = torch.zeros_like(tok)
@@ -218,11 +219,11 @@ def test_patch_embed_full_size(lib, cfg):
 # ---------------------------------------------------------------------------
 # head: 115M (out 768), 1B (out 1456); the oracle covers every output
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("cfg", [2, 3], ids=["115m", "1b"])
-def test_head_full_size(lib, cfg):
+@pytest.mark.parametrize("workload", ["115m", "1b"])
+def test_head_full_size(lib, workload):
     import torch
     from paper_2404_14712_amd._lib import HeadDesc
-    c = synth.CONFIGS[cfg]
+    c = synth.CONFIGS[workload]
     B, L, d, out = c.B, c.L, c.d, c.out_dim
     x = synth.activations(c, "x")
     prm = synth.head_params(c)
@@ -233,7 +234,7 @@ def test_head_full_size(lib, cfg):
     pd = _dev_params(prm, c.dtype)
     xd = dev(x, c.dtype)
     lib.orbit_head_fwd(desc, xd, pd, pred, saved, ws)
-    dpred = synth.normal(c.cfg, "dpred", (B, L, out))
+    dpred = synth.normal(c.seed, "dpred", (B, L, out))
     dx = torch.empty_like(xd)
     g = {k: torch.full(v.shape, 5.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
     lib.orbit_head_bwd(desc, xd, pd, saved, dev(dpred, "f32"), dx, g, 0, ws)

@@ -33,7 +33,7 @@ def _dev_params(p: dict, dtype: str):
 def test_patch_embed(lib, dtype, B, V, Hg, Wg, d):
     import torch
     from paper_2404_14712_amd._lib import EmbedDesc
-    c = synth.small_config(1, dtype=dtype, B=B, V=V, grid=(Hg, Wg), d=d, L=(Hg // 4) * (Wg // 4))
+    c = synth.small_config("tiny", dtype=dtype, B=B, V=V, grid=(Hg, Wg), d=d, L=(Hg // 4) * (Wg // 4))
     img = synth.image(c)
     e = synth.embed_params(c)
     desc = EmbedDesc(B, V, Hg, Wg, 4, d, 1 if dtype == "bf16" else 0)
@@ -42,7 +42,7 @@ def test_patch_embed(lib, dtype, B, V, Hg, Wg, d):
     imgd = dev(img, "f32")
     lib.orbit_patch_embed(desc, imgd, ed["w_pe"], ed["b_pe"], ed["ve"], tok)
     ref = O.patch_embed_fwd(img, e["w_pe"], e["b_pe"], e["ve"], 4)
-    dtok = synth.normal(c.cfg, "dtok", ref.shape, dtype=dtype)
+    dtok = synth.normal(c.seed, "dtok", ref.shape, dtype=dtype)
     ws = torch.empty(lib.orbit_patch_embed_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
     g = {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in e.items()}
     lib.orbit_patch_embed_bwd(desc, imgd, dev(dtok, dtype), g["w_pe"], g["b_pe"], g["ve"], 0, ws)
@@ -76,10 +76,10 @@ def test_var_aggregate(lib, case):
     import torch
     from paper_2404_14712_amd._lib import AggDesc
     dtype, B, L, V, d, H, dh = case
-    c = synth.small_config(2, dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
+    c = synth.small_config("115m", dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
     A = H * dh
-    tok = synth.normal(c.cfg, "tok", (B, L, V, d), dtype=dtype)
-    prm = synth.make_params(c.cfg, "agg", synth.agg_param_shapes(d, A, L), 0.2, dtype)
+    tok = synth.normal(c.seed, "tok", (B, L, V, d), dtype=dtype)
+    prm = synth.make_params(c.seed, "agg", synth.agg_param_shapes(d, A, L), 0.2, dtype)
     desc = AggDesc(B, L, V, d, H, dh, 1 if dtype == "bf16" else 0)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     z = torch.zeros(B, L, d, dtype=tdt, device="cuda")
@@ -88,7 +88,7 @@ def test_var_aggregate(lib, case):
     pd = _dev_params(prm, dtype)
     tokd = dev(tok, dtype)
     lib.orbit_var_aggregate(desc, tokd, pd, z, saved, ws)
-    dz = synth.normal(c.cfg, "dz", (B, L, d), dtype=dtype)
+    dz = synth.normal(c.seed, "dz", (B, L, d), dtype=dtype)
     dtok = torch.zeros(B, L, V, d, dtype=tdt, device="cuda")
     g = {k: torch.full(v.shape, 7.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
     lib.orbit_var_aggregate_bwd(desc, tokd, pd, saved, dev(dz, dtype), dtok, g, 0, ws)
@@ -110,10 +110,10 @@ def test_var_aggregate_identical_tokens(lib, dtype):
     import torch
     from paper_2404_14712_amd._lib import AggDesc
     B, L, V, d, H, dh = 2, 21, 48, 256, 8, 32
-    c = synth.small_config(2, dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
-    one = synth.normal(c.cfg, "tok.one", (B, L, 1, d), dtype=dtype)
+    c = synth.small_config("115m", dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
+    one = synth.normal(c.seed, "tok.one", (B, L, 1, d), dtype=dtype)
     tok = np.repeat(one, V, axis=2)
-    prm = synth.make_params(c.cfg, "agg", synth.agg_param_shapes(d, H * dh, L), 0.2, dtype)
+    prm = synth.make_params(c.seed, "agg", synth.agg_param_shapes(d, H * dh, L), 0.2, dtype)
     desc = AggDesc(B, L, V, d, H, dh, 1 if dtype == "bf16" else 0)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     z = torch.zeros(B, L, d, dtype=tdt, device="cuda")
@@ -122,7 +122,7 @@ def test_var_aggregate_identical_tokens(lib, dtype):
     pd = _dev_params(prm, dtype)
     tokd = dev(tok, dtype)
     lib.orbit_var_aggregate(desc, tokd, pd, z, saved, ws)
-    dz = synth.normal(c.cfg, "dz", (B, L, d), dtype=dtype)
+    dz = synth.normal(c.seed, "dz", (B, L, d), dtype=dtype)
     dtok = torch.zeros(B, L, V, d, dtype=tdt, device="cuda")
     g = {k: torch.full(v.shape, 7.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
     lib.orbit_var_aggregate_bwd(desc, tokd, pd, saved, dev(dz, dtype), dtok, g, 0, ws)
@@ -144,10 +144,10 @@ def test_var_aggregate_accumulate(lib, case):
     import torch
     from paper_2404_14712_amd._lib import AggDesc
     dtype, B, L, V, d, H, dh = case
-    c = synth.small_config(2, dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
+    c = synth.small_config("115m", dtype=dtype, B=B, L=L, V=V, d=d, agg_heads=H, agg_head_dim=dh, sigma=0.2)
     A = H * dh
-    tok = synth.normal(c.cfg, "tok", (B, L, V, d), dtype=dtype)
-    prm = synth.make_params(c.cfg, "agg", synth.agg_param_shapes(d, A, L), 0.2, dtype)
+    tok = synth.normal(c.seed, "tok", (B, L, V, d), dtype=dtype)
+    prm = synth.make_params(c.seed, "agg", synth.agg_param_shapes(d, A, L), 0.2, dtype)
     desc = AggDesc(B, L, V, d, H, dh, 1 if dtype == "bf16" else 0)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     z = torch.zeros(B, L, d, dtype=tdt, device="cuda")
@@ -156,7 +156,7 @@ def test_var_aggregate_accumulate(lib, case):
     pd = _dev_params(prm, dtype)
     tokd = dev(tok, dtype)
     lib.orbit_var_aggregate(desc, tokd, pd, z, saved, ws)
-    dz = synth.normal(c.cfg, "dz", (B, L, d), dtype=dtype)
+    dz = synth.normal(c.seed, "dz", (B, L, d), dtype=dtype)
     dzd = dev(dz, dtype)
     dtok = torch.zeros(B, L, V, d, dtype=tdt, device="cuda")
     g = {k: torch.full(v.shape, 7.0, dtype=torch.float32, device="cuda") for k, v in prm.items()}
@@ -202,9 +202,9 @@ def _run_block(lib, case, accumulate=0):
     import torch
     from paper_2404_14712_amd._lib import BlockDesc
     dtype, B, L, d, H, dh, F, qk = case
-    c = synth.small_config(4, dtype=dtype, B=B, L=L, d=d, heads=H, head_dim=dh, mlp=F, qk_norm=qk, sigma=0.05)
+    c = synth.small_config("10b-shard", dtype=dtype, B=B, L=L, d=d, heads=H, head_dim=dh, mlp=F, qk_norm=qk, sigma=0.05)
     x = synth.activations(c, "x")
-    dy = synth.normal(c.cfg, "dy", x.shape, dtype=dtype)
+    dy = synth.normal(c.seed, "dy", x.shape, dtype=dtype)
     prm = synth.block_params(c, 0)
     desc = BlockDesc(B, L, d, H, dh, F, qk, 1e-5, 1 if dtype == "bf16" else 0)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -307,11 +307,11 @@ def test_vit_block_inference_and_determinism(lib):
 def test_head(lib, dtype, B, L, d, out, final_ln, hidden):
     import torch
     from paper_2404_14712_amd._lib import HeadDesc
-    c = synth.small_config(1, dtype=dtype, B=B, L=L, d=d, V=out // 16, sigma=0.05)
+    c = synth.small_config("tiny", dtype=dtype, B=B, L=L, d=d, V=out // 16, sigma=0.05)
     x = synth.activations(c, "x")
     prm = synth.head_params(c, hidden)
     if hidden:  # hidden-layer weights of the scale that keeps the activations O(1)
-        prm["w_hid"] = synth.normal(c.cfg, "head.w_hid.unit", prm["w_hid"].shape, std=1.0 / np.sqrt(d),
+        prm["w_hid"] = synth.normal(c.seed, "head.w_hid.unit", prm["w_hid"].shape, std=1.0 / np.sqrt(d),
                                     dtype=dtype)
     desc = HeadDesc(B, L, d, out, final_ln, 1e-5, 1 if dtype == "bf16" else 0, hidden)
     saved = torch.empty(lib.orbit_head_saved_bytes(desc), dtype=torch.uint8, device="cuda")
@@ -320,7 +320,7 @@ def test_head(lib, dtype, B, L, d, out, final_ln, hidden):
     pd = _dev_params(prm, dtype)
     xd = dev(x, dtype)
     lib.orbit_head_fwd(desc, xd, pd, pred, saved, ws)
-    dpred = synth.normal(c.cfg, "dpred", (B, L, out))
+    dpred = synth.normal(c.seed, "dpred", (B, L, out))
     dx = torch.zeros_like(xd)
     g = {k: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for k, v in prm.items()}
     lib.orbit_head_bwd(desc, xd, pd, saved, dev(dpred, "f32"), dx, g, 0, ws)
@@ -467,7 +467,7 @@ def test_graph_replay_matches_eager(lib):
     launches: three replays, each after eager work that overwrites every
     output."""
     import torch
-    c = synth.small_config(2, B=2, L=64, grid=(32, 32), V=6, d=256, blocks=2, heads=4, head_dim=64, mlp=512,
+    c = synth.small_config("115m", B=2, L=64, grid=(32, 32), V=6, d=256, blocks=2, heads=4, head_dim=64, mlp=512,
                            agg_heads=8, agg_head_dim=32, sigma=0.05)
     vp, loss, inputs = _run_model(lib, c)
     img, tgt = dev(inputs[0], "f32"), dev(inputs[1], "f32")
@@ -501,7 +501,7 @@ def test_full_model_checkpoint_bitwise(lib):
     """The whole pass with activation checkpointing of the blocks gives
     bitwise the same loss, prediction and gradients as with stored tensors."""
     import torch
-    c = synth.small_config(2, B=2, L=128, grid=(32, 64), V=12, d=256, blocks=3, heads=4, head_dim=64, mlp=1024,
+    c = synth.small_config("115m", B=2, L=128, grid=(32, 64), V=12, d=256, blocks=3, heads=4, head_dim=64, mlp=1024,
                            agg_heads=8, agg_head_dim=32, sigma=0.05)
     vp, loss, _ = _run_model(lib, c)
     vc, lossc, _ = _run_model(lib, c, checkpoint=True)
@@ -521,9 +521,9 @@ def test_full_model_decoder_head_wmse(lib, dtype):
     and a two-layer decoder head: the tiny configuration in fp32, a reduced
     115M-structure model in bf16 (one block, so no block past the first)."""
     if dtype == "f32":
-        c = synth.CONFIGS[1]
+        c = synth.CONFIGS["tiny"]
     else:
-        c = synth.small_config(2, B=2, L=128, grid=(32, 64), V=12, d=256, blocks=1, heads=4, head_dim=64,
+        c = synth.small_config("115m", B=2, L=128, grid=(32, 64), V=12, d=256, blocks=1, heads=4, head_dim=64,
                                mlp=1024, agg_heads=8, agg_head_dim=32, sigma=0.05)
     vp, loss, inputs = _run_model(lib, c, head_hidden=2, loss="wmse")
     assert vp.z.loss == "wmse" and "w_hid" in vp.grads["head"]
@@ -533,7 +533,7 @@ def test_full_model_decoder_head_wmse(lib, dtype):
 
 def test_full_model_tiny_fp32(lib):
     """The tiny configuration exactly: 2 x 4 variables on 32x64, d=128, 2 blocks, fp32."""
-    c = synth.CONFIGS[1]
+    c = synth.CONFIGS["tiny"]
     vp, loss, inputs = _run_model(lib, c)
     _check_model(vp, loss, inputs, c, TOL["f32"])
 
@@ -543,7 +543,7 @@ _REDUCED = {}
 
 def _reduced_bf16(lib):
     if "run" not in _REDUCED:
-        c = synth.small_config(2, B=2, L=128, grid=(32, 64), V=12, d=256, blocks=2, heads=4, head_dim=64,
+        c = synth.small_config("115m", B=2, L=128, grid=(32, 64), V=12, d=256, blocks=2, heads=4, head_dim=64,
                                mlp=1024, agg_heads=8, agg_head_dim=32, sigma=0.05)
         vp, loss, inputs = _run_model(lib, c)
         try:
