@@ -140,7 +140,7 @@ struct BlockWs {
   void* dO;    // [T, A]
   void* dqkv;  // [T, 3A]
   float* D;    // attention backward workspace
-  float *p_fc1, *p_fc2, *p_ln2, *p_proj, *p_qkv, *p_ln1;  // column-sum partials
+  float *p_fc1, *p_fc2, *p_ln2, *p_qkv, *p_ln1;  // column-sum partials
   void* qws;
   void* gws;
   size_t gws_bytes;
@@ -179,10 +179,9 @@ size_t block_ws_layout(const BlockDims& z, void* base, size_t bytes, BlockWs* w,
   const int T = (int)z.T;
   t.p_fc1 = c.take<float>(colsum_part_bytes(T, z.F, false) / sizeof(float));
   t.p_fc2 = c.take<float>(colsum_part_bytes(T, z.d, false) / sizeof(float));
-  t.p_ln2 = c.take<float>(colsum_part_bytes(T, z.d, true) / sizeof(float));
-  t.p_proj = c.take<float>(colsum_part_bytes(T, z.d, false) / sizeof(float));
+  t.p_ln2 = c.take<float>(ln_bwd_cols_part_bytes(T, z.d, true) / sizeof(float));
   t.p_qkv = c.take<float>(colsum_part_bytes(T, 3 * z.A, false) / sizeof(float));
-  t.p_ln1 = c.take<float>(colsum_part_bytes(T, z.d, true) / sizeof(float));
+  t.p_ln1 = c.take<float>(ln_bwd_cols_part_bytes(T, z.d, false) / sizeof(float));
   t.qws = c.take<char>(qk_norm_bwd_workspace_bytes(z.dh));
   const size_t g = block_gemm_ws(z);
   t.gws = c.take<char>(g);
@@ -388,30 +387,16 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.C = w.dh; g.ldc = z.d; g.M = T; g.N = z.d; g.K = z.F;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, sv.x1, z.d, sv.mu2, sv.r2, p->ln2_g, dy, w.dx1, z.d, T, z.d, s));
-  {
-    // LN2 parameter gradients right after the LN backward, which has just
-    // streamed the same dh and x1 through the caches
-    ColJob j[1];
-    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = sv.x1; j[0].ldx = z.d; j[0].mean = sv.mu2;
-    j[0].rstd = sv.r2; j[0].part = w.p_ln2; j[0].out_sum = gr->ln2_b; j[0].out_xsum = gr->ln2_g;
-    ORBIT_TRY(colsum_partials(dt, j, 1, T, s));
-    fin.add_job(j[0], T);
-  }
-  bool fused_proj;
+  // LN2 backward; the chunk sums of its rows give the LN2 parameter gradients
+  // and, summed over its output dx1, the projection's bias gradient
+  ORBIT_TRY(layernorm_bwd_cols(dt, w.dh, z.d, sv.x1, z.d, sv.mu2, sv.r2, p->ln2_g, dy, w.dx1, z.d, T, z.d, w.p_ln2,
+                               gr->ln2_b, gr->ln2_g, gr->b_proj, fin, s));
   {
     Gemm g; g.dtype = dt; g.tag = "proj_dw";
     g.A = sv.o; g.lda = z.A; g.a_kmajor = false; g.B = w.dx1; g.ldb = z.d; g.b_kmajor = false;
     g.C = gr->w_proj; g.ldc = z.d; g.out_f32 = true; g.accumulate = acc;
     g.M = z.A; g.N = z.d; g.K = T;
-    fused_proj = dw_bias(g, w.p_proj, gr->b_proj);
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
-  }
-  if (!fused_proj) {
-    ColJob j[1];
-    bias_job(j[0], w.dx1, z.d, w.p_proj, gr->b_proj);
-    ORBIT_TRY(colsum_partials(dt, j, 1, T, s));
-    fin.add_job(j[0], T);
   }
   // attention sub-layer
   {
@@ -457,15 +442,13 @@ orbit_status orbit_vit_block_bwd(const orbit_block_desc* desc, const orbit_block
     g.C = w.dh; g.ldc = z.d; g.M = T; g.N = z.d; g.K = 3 * z.A;
     ORBIT_TRY(gemm(g, w.gws, w.gws_bytes, s));
   }
-  ORBIT_TRY(layernorm_bwd(dt, w.dh, z.d, x, z.d, sv.mu1, sv.r1, p->ln1_g, w.dx1, dx, z.d, T, z.d, s));
-  {
-    ColJob j[2];
-    j[0].src = w.dh; j[0].ld = z.d; j[0].n = z.d; j[0].x = x; j[0].ldx = z.d; j[0].mean = sv.mu1;
-    j[0].rstd = sv.r1; j[0].part = w.p_ln1; j[0].out_sum = gr->ln1_b; j[0].out_xsum = gr->ln1_g;
-    int nj = 1;
-    if (!fused_qkv) bias_job(j[nj++], w.dqkv, 3 * z.A, w.p_qkv, gr->b_qkv);
-    ORBIT_TRY(colsum_partials(dt, j, nj, T, s));
-    for (int i = 0; i < nj; ++i) fin.add_job(j[i], T);
+  ORBIT_TRY(layernorm_bwd_cols(dt, w.dh, z.d, x, z.d, sv.mu1, sv.r1, p->ln1_g, w.dx1, dx, z.d, T, z.d, w.p_ln1,
+                               gr->ln1_b, gr->ln1_g, nullptr, fin, s));
+  if (!fused_qkv) {
+    ColJob j[1];
+    bias_job(j[0], w.dqkv, 3 * z.A, w.p_qkv, gr->b_qkv);
+    ORBIT_TRY(colsum_partials(dt, j, 1, T, s));
+    fin.add_job(j[0], T);
   }
   return fin.run(accumulate, s);
 }
@@ -639,7 +622,8 @@ static size_t head_ws_layout(const orbit_head_desc& d, void* base, size_t bytes,
   t.dpb = c.take<char>(T * d.out * esz(d.dtype));
   t.dh[0] = c.take<char>(T * d.d * esz(d.dtype));
   t.dh[1] = d.hidden > 0 ? c.take<char>(T * d.d * esz(d.dtype)) : nullptr;
-  t.cws = c.take<char>(std::max(colsum_workspace_bytes((int)T, d.out), colsum_workspace_bytes((int)T, d.d)));
+  t.cws = c.take<char>(std::max({colsum_workspace_bytes((int)T, d.out), colsum_workspace_bytes((int)T, d.d),
+                                  ln_bwd_cols_part_bytes((int)T, d.d, false)}));
   const size_t g = head_gemm_ws(d);
   t.gws = c.take<char>(g);
   const size_t used = c.used();
@@ -780,8 +764,10 @@ orbit_status orbit_head_bwd(const orbit_head_desc* desc, const void* x, const or
     dcur = dnext;
   }
   if (d.final_ln) {
-    ORBIT_TRY(layernorm_bwd(dt, dcur, d.d, x, d.d, sv.mu, sv.r, p->lnf_g, nullptr, dx, d.d, T, d.d, s));
-    ORBIT_TRY(colsum(dt, dcur, d.d, T, d.d, x, d.d, sv.mu, sv.r, gr->lnf_b, gr->lnf_g, accumulate, w.cws, s));
+    ColFinal f;
+    ORBIT_TRY(layernorm_bwd_cols(dt, dcur, d.d, x, d.d, sv.mu, sv.r, p->lnf_g, nullptr, dx, d.d, T, d.d,
+                                 reinterpret_cast<float*>(w.cws), gr->lnf_b, gr->lnf_g, nullptr, f, s));
+    ORBIT_TRY(f.run(accumulate, s));
   } else if (!accumulate) {
     if (gr->lnf_g) ORBIT_TRY(fill_f32(gr->lnf_g, d.d, 0.f, s));
     if (gr->lnf_b) ORBIT_TRY(fill_f32(gr->lnf_b, d.d, 0.f, s));

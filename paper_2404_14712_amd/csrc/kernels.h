@@ -12,10 +12,6 @@ namespace orbit {
 orbit_status layernorm_fwd(orbit_dtype dt, const void* x, int64_t ldx, const void* g, const void* b,
                            void* y, int64_t ldy, float* mean, float* rstd, int rows, int n,
                            float eps, hipStream_t s);
-// dx = rstd * (dy*g - mean(dy*g) - xhat * mean(dy*g*xhat)) [+ dres]; dx may alias dres.
-orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const void* x, int64_t ldx,
-                           const float* mean, const float* rstd, const void* g, const void* dres,
-                           void* dx, int64_t lddx, int rows, int n, hipStream_t s);
 
 // ---- deterministic column reductions over rows ----------------------------
 // Phase 1 (colsum_partials, one launch for up to kColMaxJobs jobs over the
@@ -47,6 +43,16 @@ class ColFinal {
   struct Item { const float* part; int64_t ldp; float* out; int chunks, n; };
   std::vector<Item> items;
 };
+// LayerNorm backward, dx = rstd * (dy*g - mean(dy*g) - xhat * mean(dy*g*xhat))
+// [+ dres] (n a multiple of 8 up to 16384; dx may alias dres), that also forms,
+// per chunk of 8 or 16 rows, the column sums of dy (-> out_b), dy * xhat
+// (-> out_g) and, when out_o is given, of the output dx (-> out_o); their
+// fixed-order final sums are queued on `fin`. part: ln_bwd_cols_part_bytes.
+size_t ln_bwd_cols_part_bytes(int rows, int n, bool osum);
+orbit_status layernorm_bwd_cols(orbit_dtype dt, const void* dy, int64_t lddy, const void* x, int64_t ldx,
+                                const float* mean, const float* rstd, const void* g, const void* dres, void* dx,
+                                int64_t lddx, int rows, int n, float* part, float* out_b, float* out_g,
+                                float* out_o, ColFinal& fin, hipStream_t s);
 // both phases for one (optionally LN) job; workspace: colsum_workspace_bytes
 size_t colsum_workspace_bytes(int rows, int n);
 orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int n,

@@ -137,105 +137,6 @@ __global__ void __launch_bounds__(256) ln_fwd_wave(const T* __restrict__ x, int6
   }
 }
 
-template <typename T, int PER>
-__global__ void __launch_bounds__(256) ln_bwd_wave(const T* __restrict__ dy, int64_t lddy, const T* __restrict__ x,
-                                                   int64_t ldx, const float* __restrict__ mean,
-                                                   const float* __restrict__ rstd, const T* __restrict__ g,
-                                                   const T* dres, T* dx, int64_t lddx, int rows, int n) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const float mu = mean[row], r = rstd[row];
-  float gh[PER][8], xh[PER][8];
-  float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-  for (int c = 0; c < PER; ++c) {
-    const int idx = (lane + c * 64) * 8;
-    if (idx < n) {
-      float d8[8], x8[8], g8[8];
-      load8(dy + row * lddy + idx, d8);
-      load8(x + row * ldx + idx, x8);
-      load8(g + idx, g8);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        xh[c][i] = (x8[i] - mu) * r;
-        gh[c][i] = d8[i] * g8[i];
-        s1 += gh[c][i];
-        s2 += gh[c][i] * xh[c][i];
-      }
-    }
-  }
-  const float inv_n = 1.f / (float)n;
-  const float m1 = wave_sum(s1) * inv_n;
-  const float m2 = wave_sum(s2) * inv_n;
-#pragma unroll
-  for (int c = 0; c < PER; ++c) {
-    const int idx = (lane + c * 64) * 8;
-    if (idx < n) {
-      float o[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[i] = r * (gh[c][i] - m1 - xh[c][i] * m2);
-      if (dres) {
-        float rr[8];
-        load8(dres + row * lddx + idx, rr);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[i] += rr[i];
-      }
-      store8(dx + row * lddx + idx, o);
-    }
-  }
-}
-
-template <typename T, int NCH>
-__global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, int64_t lddy,
-                                                     const T* __restrict__ x, int64_t ldx,
-                                                     const float* __restrict__ mean,
-                                                     const float* __restrict__ rstd,
-                                                     const T* __restrict__ g, const T* dres, T* dx,
-                                                     int64_t lddx, int n) {
-  __shared__ float red[4];
-  const int64_t row = blockIdx.x;
-  const float mu = mean[row], r = rstd[row];
-  float gh[NCH][8], xh[NCH][8];
-  float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int idx = (threadIdx.x + c * 256) * 8;
-    if (idx < n) {
-      float d8[8], x8[8], g8[8];
-      load8(dy + row * lddy + idx, d8);
-      load8(x + row * ldx + idx, x8);
-      load8(g + idx, g8);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        xh[c][i] = (x8[i] - mu) * r;
-        gh[c][i] = d8[i] * g8[i];
-        s1 += gh[c][i];
-        s2 += gh[c][i] * xh[c][i];
-      }
-    }
-  }
-  const float inv_n = 1.f / (float)n;
-  const float m1 = block_sum256(s1, red) * inv_n;
-  const float m2 = block_sum256(s2, red) * inv_n;
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int idx = (threadIdx.x + c * 256) * 8;
-    if (idx < n) {
-      float o[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[i] = r * (gh[c][i] - m1 - xh[c][i] * m2);
-      if (dres) {
-        float rr[8];
-        load8(dres + row * lddx + idx, rr);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[i] += rr[i];
-      }
-      store8(dx + row * lddx + idx, o);
-    }
-  }
-}
-
 // ---- column sums ------------------------------------------------------------
 // Phase 1: a grid of (column block, row chunk) blocks, 1024 threads each: 64
 // lanes x 8 consecutive columns, 16 row lanes striding over the chunk with 4
@@ -391,6 +292,223 @@ __global__ void __launch_bounds__(256) colsum_final_kernel(CsFinalArgs a) {
       for (int k = 0; k < CL; ++k) t += red[k][el];
       I.out[e] = a.accumulate ? I.out[e] + t : t;
     }
+  }
+}
+
+// ---- LayerNorm backward fused with its column sums ---------------------------
+// A block takes a chunk of rpb rows. Besides dx it stores one partial row per
+// column sum over the chunk: of dy (the shift's gradient), of dy * xhat (the
+// gain's) and, with OSUM, of the output dx (the bias gradient of the layer
+// whose output the residual stream carries into this LayerNorm). The
+// partials are added in a fixed order afterwards, so the sums never re-read
+// dy, x or dx. The block's G groups of TPR threads (TPR a multiple of 64 up
+// to 512, 8 NCH TPR >= n) take the chunk's rows in turn: group q rows r0 + q,
+// r0 + q + G, ...; thread t of a group owns the NCH 8-column pieces starting
+// at 8(t + c TPR). A group loads RB rows at once (dy, x and the residual
+// gradient all in flight together) and forms their statistics with one
+// block barrier; every group runs the same number of batches, so the
+// barriers line up.
+struct LnColArgs {
+  const void *dy, *x, *g, *dres;
+  void* dx;
+  const float *mean, *rstd;
+  int64_t lddy, ldx, lddx;
+  float* part;  // sum k (0: dy, 1: dy * xhat, 2: dx) of chunk c at part[(k * chunks + c) * n]
+  int rows, n, tpr, rpb;
+};
+
+// 8 values of T as loaded (bf16 stays packed: 4 registers instead of 8)
+template <typename T>
+struct Raw8 {
+  U128 v[sizeof(T) / 2];
+  ORBIT_DEV void load(const T* p) {
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(T) / 2); ++i) v[i] = ld128(p + i * (8 / (sizeof(T) / 2)));
+  }
+  ORBIT_DEV void zero() {
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(T) / 2); ++i) v[i] = zero128();
+  }
+  ORBIT_DEV void get(float* f) const {
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(T) / 2); ++i) unpack(v[i], f + i * (8 / (sizeof(T) / 2)), (T*)nullptr);
+  }
+};
+
+template <typename T, int NCH>
+constexpr int ln_cols_rb() { return NCH == 2 ? 2 : 1; }
+
+// one batch of RB rows of a group: their positions, statistics and data
+template <typename T, int NCH, int RB>
+struct LnBatch {
+  int64_t r[RB];
+  bool rv[RB];
+  float mu[RB], rs[RB];
+  Raw8<T> d[RB][NCH], x[RB][NCH], e[RB][NCH];
+};
+
+template <typename T, int NCH, bool OSUM>
+__global__ void __launch_bounds__(512) ln_bwd_cols_kernel(LnColArgs a) {
+  constexpr int RB = ln_cols_rb<T, NCH>();
+  using Batch = LnBatch<T, NCH, RB>;
+  __shared__ float red[2][8][RB][2];
+  const int tpr = a.tpr, G = (int)blockDim.x / tpr, wpg = tpr >> 6;
+  const int q = (int)threadIdx.x / tpr, t = (int)threadIdx.x % tpr;
+  const int wave = (int)threadIdx.x >> 6, lane = (int)threadIdx.x & 63;
+  const int n = a.n, chunks = (int)gridDim.x;
+  const int r0 = (int)blockIdx.x * a.rpb, r1 = min(a.rows, r0 + a.rpb);
+  const T* dy = static_cast<const T*>(a.dy);
+  const T* x = static_cast<const T*>(a.x);
+  const T* dres = static_cast<const T*>(a.dres);
+  const T* gp = static_cast<const T*>(a.g);
+  T* dx = static_cast<T*>(a.dx);
+  int col[NCH];
+  bool on[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    col[c] = 8 * (t + c * tpr);
+    on[c] = col[c] < n;
+  }
+  float cs[NCH][8], cx[NCH][8], co[NCH][8];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cs[c][i] = cx[c][i] = co[c][i] = 0.f;
+  const float inv_n = 1.f / (float)n;
+  const int steps = (a.rpb + G - 1) / G;  // rows per group
+  // batch `it` (rows it .. it + RB - 1 of this group): the next batch is
+  // fetched before the current one is reduced, so loads stay in flight
+  auto fetch = [&](int it, Batch& B) {
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      B.r[b] = r0 + q + (int64_t)(it + b) * G;
+      B.rv[b] = it + b < steps && B.r[b] < r1;
+      B.mu[b] = B.rv[b] ? a.mean[B.r[b]] : 0.f;
+      B.rs[b] = B.rv[b] ? a.rstd[B.r[b]] : 0.f;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        if (B.rv[b] && on[c]) {
+          B.d[b][c].load(dy + B.r[b] * a.lddy + col[c]);
+          B.x[b][c].load(x + B.r[b] * a.ldx + col[c]);
+          if (dres) B.e[b][c].load(dres + B.r[b] * a.lddx + col[c]);
+          else B.e[b][c].zero();
+        } else {
+          B.d[b][c].zero();
+          B.x[b][c].zero();
+          B.e[b][c].zero();
+        }
+      }
+    }
+  };
+  // bf16 rows hold the next batch in registers as well (float32 rows and
+  // the widest rows with three sums would spill)
+  constexpr bool DB = sizeof(T) == 2 && !(NCH == 4 && OSUM);
+  Batch cur;
+  if (DB) fetch(0, cur);
+  int par = 0;
+  for (int it = 0; it < steps; it += RB, par ^= 1) {
+    Batch nxt;
+    if (DB) fetch(it + RB, nxt);
+    else fetch(it, cur);
+    float s1[RB], s2[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      s1[b] = s2[b] = 0.f;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        if (cur.rv[b] && on[c]) {
+          Raw8<T> gr;
+          gr.load(gp + col[c]);
+          float d8[8], x8[8], g8[8];
+          cur.d[b][c].get(d8);
+          cur.x[b][c].get(x8);
+          gr.get(g8);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const float gh = d8[i] * g8[i];
+            s1[b] += gh;
+            s2[b] += gh * ((x8[i] - cur.mu[b]) * cur.rs[b]);
+          }
+        }
+      }
+      s1[b] = wave_sum(s1[b]);
+      s2[b] = wave_sum(s2[b]);
+    }
+    if (wpg > 1) {
+      // the group's wave sums, added in wave order
+      if (lane == 0) {
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+          red[par][wave][b][0] = s1[b];
+          red[par][wave][b][1] = s2[b];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        s1[b] = s2[b] = 0.f;
+        for (int w = q * wpg; w < (q + 1) * wpg; ++w) {
+          s1[b] += red[par][w][b][0];
+          s2[b] += red[par][w][b][1];
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const float m1 = s1[b] * inv_n, m2 = s2[b] * inv_n;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        if (cur.rv[b] && on[c]) {
+          float d8[8], x8[8], g8[8], e8[8], o[8];
+          Raw8<T> gr;
+          gr.load(gp + col[c]);
+          cur.d[b][c].get(d8);
+          cur.x[b][c].get(x8);
+          cur.e[b][c].get(e8);
+          gr.get(g8);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            x8[i] = (x8[i] - cur.mu[b]) * cur.rs[b];
+            o[i] = cur.rs[b] * (d8[i] * g8[i] - m1 - x8[i] * m2) + e8[i];
+          }
+          store8(dx + cur.r[b] * a.lddx + col[c], o);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            cs[c][i] += d8[i];
+            cx[c][i] += d8[i] * x8[i];
+            if (OSUM) co[c][i] += o[i];
+          }
+        }
+      }
+    }
+    if (DB) cur = nxt;
+  }
+  // the groups' sums of the chunk, added in group order through LDS (rows of
+  // up to 8192 elements, where a block holds more than one group), then one
+  // partial row per sum
+  __shared__ float comb[NCH == 2 ? 512 * 16 : 1];
+#pragma unroll
+  for (int k = 0; k < (OSUM ? 3 : 2); ++k) {
+    float (*v)[8] = k == 0 ? cs : k == 1 ? cx : co;
+    if (NCH == 2 && G > 1) {
+      __syncthreads();
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) comb[threadIdx.x * 16 + c * 8 + i] = v[c][i];
+      __syncthreads();
+      if (q == 0) {
+        for (int gq = 1; gq < G; ++gq)
+#pragma unroll
+          for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[c][i] += comb[(gq * tpr + t) * 16 + c * 8 + i];
+      }
+    }
+    if (q != 0) continue;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      if (on[c]) store8(a.part + ((int64_t)k * chunks + blockIdx.x) * n + col[c], v[c]);
   }
 }
 
@@ -585,16 +703,6 @@ orbit_status ln_fwd_t(const void* x, int64_t ldx, const void* g, const void* b, 
                 (const T*)b, (T*)y, ldy, mean, rstd, n, eps);
 }
 
-template <typename T, int NCH>
-orbit_status ln_bwd_t(const void* dy, int64_t lddy, const void* x, int64_t ldx, const float* mean,
-                      const float* rstd, const void* g, const void* dres, void* dx, int64_t lddx, int rows,
-                      int n, hipStream_t s) {
-  KernelInfo ki{sizeof(T) == 2 ? "ln_bwd_kernel<bf16>" : "ln_bwd_kernel<f32>", 12.0 * rows * n,
-                (dres ? 4.0 : 3.0) * rows * n * sizeof(T)};
-  return launch(ki, ln_bwd_kernel<T, NCH>, dim3(rows), dim3(256), 0, s, (const T*)dy, lddy, (const T*)x, ldx,
-                mean, rstd, (const T*)g, (const T*)dres, (T*)dx, lddx, n);
-}
-
 template <typename T>
 orbit_status ln_fwd_dispatch(const void* x, int64_t ldx, const void* g, const void* b, void* y, int64_t ldy,
                              float* mean, float* rstd, int rows, int n, float eps, hipStream_t s) {
@@ -613,29 +721,6 @@ orbit_status ln_fwd_dispatch(const void* x, int64_t ldx, const void* g, const vo
   if (nch <= 2) return ln_fwd_t<T, 2>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
   if (nch <= 4) return ln_fwd_t<T, 4>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
   if (nch <= 8) return ln_fwd_t<T, 8>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
-  set_error("layernorm: row length %d exceeds 16384", n);
-  return ORBIT_E_UNSUPPORTED;
-}
-
-template <typename T>
-orbit_status ln_bwd_dispatch(const void* dy, int64_t lddy, const void* x, int64_t ldx, const float* mean,
-                             const float* rstd, const void* g, const void* dres, void* dx, int64_t lddx,
-                             int rows, int n, hipStream_t s) {
-  if (n <= 4096) {
-    KernelInfo ki{sizeof(T) == 2 ? "ln_bwd_wave<bf16>" : "ln_bwd_wave<f32>", 12.0 * rows * n,
-                  (dres ? 4.0 : 3.0) * rows * n * sizeof(T)};
-    const int per = (int)cdiv(n, 512);
-    const dim3 grid((unsigned)cdiv(rows, 4));
-#define LNB(P) if (per <= P) return launch(ki, ln_bwd_wave<T, P>, grid, dim3(256), 0, s, (const T*)dy, lddy, (const T*)x, \
-                                           ldx, mean, rstd, (const T*)g, (const T*)dres, (T*)dx, lddx, rows, n)
-    LNB(1); LNB(2); LNB(4); LNB(8);
-#undef LNB
-  }
-  const int nch = (int)cdiv(n, 2048);
-  if (nch <= 1) return ln_bwd_t<T, 1>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
-  if (nch <= 2) return ln_bwd_t<T, 2>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
-  if (nch <= 4) return ln_bwd_t<T, 4>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
-  if (nch <= 8) return ln_bwd_t<T, 8>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
   set_error("layernorm: row length %d exceeds 16384", n);
   return ORBIT_E_UNSUPPORTED;
 }
@@ -677,13 +762,6 @@ orbit_status layernorm_fwd(orbit_dtype dt, const void* x, int64_t ldx, const voi
                            int64_t ldy, float* mean, float* rstd, int rows, int n, float eps, hipStream_t s) {
   if (dt == ORBIT_BF16) return ln_fwd_dispatch<bf16>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
   return ln_fwd_dispatch<float>(x, ldx, g, b, y, ldy, mean, rstd, rows, n, eps, s);
-}
-
-orbit_status layernorm_bwd(orbit_dtype dt, const void* dy, int64_t lddy, const void* x, int64_t ldx,
-                           const float* mean, const float* rstd, const void* g, const void* dres, void* dx,
-                           int64_t lddx, int rows, int n, hipStream_t s) {
-  if (dt == ORBIT_BF16) return ln_bwd_dispatch<bf16>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
-  return ln_bwd_dispatch<float>(dy, lddy, x, ldx, mean, rstd, g, dres, dx, lddx, rows, n, s);
 }
 
 // ---- column sums: host side ------------------------------------------------
@@ -800,6 +878,53 @@ orbit_status colsum(orbit_dtype dt, const void* dy, int64_t lddy, int rows, int 
   ColFinal f;
   f.add_job(J, rows);
   return f.run(accumulate, s);
+}
+
+// ---- LayerNorm backward with its column sums: host side ---------------------
+int ln_cols_nch(int n) { return n <= 8192 ? 2 : 4; }
+int ln_cols_tpr(int n) { return (int)(cdiv(cdiv(n, 8 * ln_cols_nch(n)), 64) * 64); }
+// rows per chunk: 16, or 8 where 16-row chunks would leave CUs without a block
+int ln_cols_rpb(int rows) { return cdiv(rows, 16) >= 256 ? 16 : 8; }
+
+size_t ln_bwd_cols_part_bytes(int rows, int n, bool osum) {
+  return align_up((size_t)(osum ? 3 : 2) * cdiv(rows, ln_cols_rpb(rows)) * (size_t)n * sizeof(float));
+}
+
+orbit_status layernorm_bwd_cols(orbit_dtype dt, const void* dy, int64_t lddy, const void* x, int64_t ldx,
+                                const float* mean, const float* rstd, const void* g, const void* dres, void* dx,
+                                int64_t lddx, int rows, int n, float* part, float* out_b, float* out_g,
+                                float* out_o, ColFinal& fin, hipStream_t s) {
+  if (rows <= 0 || n <= 0) return ORBIT_OK;
+  if (n % 8 != 0 || n > 16384) {
+    set_error("layernorm_bwd_cols: row length %d must be a multiple of 8 and at most 16384", n);
+    return ORBIT_E_UNSUPPORTED;
+  }
+  LnColArgs a{};
+  a.dy = dy; a.x = x; a.g = g; a.dres = dres; a.dx = dx; a.mean = mean; a.rstd = rstd;
+  a.lddy = lddy; a.ldx = ldx; a.lddx = lddx; a.part = part; a.rows = rows; a.n = n;
+  a.tpr = ln_cols_tpr(n);
+  a.rpb = ln_cols_rpb(rows);
+  const int G = 512 / a.tpr;
+  const int chunks = (int)cdiv(rows, a.rpb);
+  const bool osum = out_o != nullptr;
+  const double e = dt == ORBIT_BF16 ? 2.0 : 4.0;
+  KernelInfo ki{dt == ORBIT_BF16 ? "ln_bwd_cols<bf16>" : "ln_bwd_cols<f32>", 14.0 * rows * n,
+                (dres ? 4.0 : 3.0) * rows * n * e + (osum ? 3.0 : 2.0) * chunks * n * 4.0};
+  const dim3 grid((unsigned)chunks), block((unsigned)(G * a.tpr));
+#define LNC(TT, C, O) ORBIT_TRY(launch(ki, ln_bwd_cols_kernel<TT, C, O>, grid, block, 0, s, a))
+  const bool wide = ln_cols_nch(n) == 4;
+  if (dt == ORBIT_BF16) {
+    if (wide) { if (osum) LNC(bf16, 4, true); else LNC(bf16, 4, false); }
+    else { if (osum) LNC(bf16, 2, true); else LNC(bf16, 2, false); }
+  } else {
+    if (wide) { if (osum) LNC(float, 4, true); else LNC(float, 4, false); }
+    else { if (osum) LNC(float, 2, true); else LNC(float, 2, false); }
+  }
+#undef LNC
+  fin.add(part, n, chunks, n, out_b);
+  fin.add(part + (int64_t)chunks * n, n, chunks, n, out_g);
+  if (osum) fin.add(part + (int64_t)2 * chunks * n, n, chunks, n, out_o);
+  return ORBIT_OK;
 }
 
 orbit_status colsum_f32(const float* dy, int64_t lddy, int rows, int n, float* out_sum, int accumulate, void* ws,
