@@ -241,6 +241,99 @@ __global__ void __launch_bounds__(256) agg_xbar(const bf16* __restrict__ ab, con
   for (int h = 0; h < H; ++h) st128(xbar + ((int64_t)t * H + h) * d + c0, pack(acc[h], (bf16*)nullptr));
 }
 
+// Dot products of each token's V rows with H weight rows over the embedding,
+// out[t][v][h] = alpha * sum_c w_t[h][c] x[t][v][c] (float32, element
+// (t, v, h) at out[t * o_t + v * o_v + h * o_h]): the scores (w = the folded
+// query keys u, shared by every token) and their backward (w_t = dxbar of
+// token t). A block per token; its four waves take a quarter of the embedding
+// each and run 16x16x32 bf16 MFMAs, heads as rows and 16 variables per tile
+// as columns; the token rows are loaded straight into MFMA fragments (loads
+// past the last variable read zeros; default cache policy, since a load
+// covers half of each row's 128-byte line and its partner the other half),
+// and the quarters' sums are added in order through LDS.
+template <int H, int NT>
+__global__ void __launch_bounds__(256) agg_rowdot(const bf16* __restrict__ tok, const bf16* __restrict__ w,
+                                                  int64_t w_tstride, float* __restrict__ out, int64_t o_t, int o_v,
+                                                  int o_h, float alpha, int V, int d) {
+  static_assert(H == 8 || H == 16, "heads");
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const int t = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // a 64-deep K step: lane group g = lane / 16 holds k = 16 g .. 16 g + 15 of
+  // its row (two 16-byte loads; each row's 128 bytes come in one pair), the
+  // first half for the step's first product, the second for its second
+  const int lr = lane & 15, lk = (lane >> 4) * 16;
+  const int q = d / 4, kb = wave * q;
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16*>(tok + (int64_t)t * V * d), 0, V * d * 2, 0x00020000);
+  unsigned vo[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) vo[n] = (unsigned)((n * 16 + lr) * d + kb + lk) * 2u;
+  // heads past H (H = 8) are zero rows of the A fragment: their lanes load
+  // row 0 and mask it, so the loop carries no branch
+  const unsigned amask = lr < H ? ~0u : 0u;
+  const bf16* wp = w + t * w_tstride + (int64_t)(lr < H ? lr : 0) * d + kb + lk;
+  f32x4 acc[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  struct Step { u32x4 a[2], b[NT][2]; };
+  auto load = [&](Step& f, int k) {
+    f.a[0] = *reinterpret_cast<const u32x4*>(wp + k);
+    f.a[1] = *reinterpret_cast<const u32x4*>(wp + k + 8);
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      f.b[n][0] = __builtin_amdgcn_raw_buffer_load_b128(rx, vo[n] + (unsigned)k * 2u, 0, 0);
+      f.b[n][1] = __builtin_amdgcn_raw_buffer_load_b128(rx, vo[n] + (unsigned)k * 2u + 16u, 0, 0);
+    }
+  };
+  auto mma = [&](const Step& f) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, f.a[u] & amask);
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, f.b[n][u]), acc[n], 0, 0, 0);
+    }
+  };
+  // two steps per iteration, the next step's loads in flight during the
+  // current step's products. Each token starts its sweep at its own step
+  // (and wraps), so the blocks in flight do not all read the same column
+  // offsets of their rows at once; the summation order is fixed per token.
+  const int S = q / 64, rot = t % S;
+  auto kof = [&](int i) { const int j = i + rot; return (j < S ? j : j - S) * 64; };
+  Step f0, f1;
+  load(f0, kof(0));
+  int i = 0;
+  for (; i + 1 < S; i += 2) {
+    load(f1, kof(i + 1));
+    mma(f0);
+    if (i + 2 < S) load(f0, kof(i + 2));
+    mma(f1);
+  }
+  if (i < S) mma(f0);
+  __shared__ f32x4 part[3][NT][64];
+  if (wave > 0) {
+#pragma unroll
+    for (int n = 0; n < NT; ++n) part[wave - 1][n][lane] = acc[n];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w2 = 0; w2 < 3; ++w2)
+#pragma unroll
+    for (int n = 0; n < NT; ++n) acc[n] += part[w2][n][lane];
+  // lane l holds heads 4 (l / 16) .. + 3 of variable column l % 16
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int v = n * 16 + lr;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = (lane >> 4) * 4 + r;
+      if (h < H && v < V) out[t * o_t + (int64_t)v * o_v + (int64_t)h * o_h] = alpha * acc[n][r];
+    }
+  }
+}
+
 // softmax backward per (t, h): ds = a (da - sum a da) * scale.
 // ac[(t*V + v)*2H + h] = a, ac[(t*V + v)*2H + H + h] = ds   (dtype); one wave per
 // token, lanes as in agg_softmax
@@ -466,6 +559,35 @@ Gemm base_gemm(orbit_dtype dt) {
   return g;
 }
 
+// agg_rowdot's domain: bf16, 8 or 16 heads, at most 96 variables, an
+// embedding of whole 256-column quarters and 16-byte aligned rows
+bool rowdot_ok(orbit_dtype dt, const Sizes& z, const void* tok, const void* w) {
+  return dt == ORBIT_BF16 && (z.H == 8 || z.H == 16) && z.V <= 96 && z.d % 256 == 0 &&
+         (int64_t)z.V * z.d * 2 < ((int64_t)1 << 31) && (reinterpret_cast<uintptr_t>(tok) & 15) == 0 &&
+         (reinterpret_cast<uintptr_t>(w) & 15) == 0;
+}
+
+// out[t * o_t + v * o_v + h * o_h] = alpha * x_{t,v} . w_{t,h} over all tokens
+orbit_status rowdot(const char* name, const Sizes& z, const void* tok, const void* w, int64_t w_tstride, float* out,
+                    int64_t o_t, int o_v, int o_h, float alpha, hipStream_t s) {
+  const int nt = (int)cdiv(z.V, 16);
+  KernelInfo k{name, 2.0 * z.T * z.V * (double)z.H * z.d,
+               (double)z.T * z.V * z.d * 2.0 + (w_tstride ? (double)z.T * z.H * z.d * 2.0 : 0.0) +
+                   4.0 * z.T * z.V * z.H};
+  const dim3 grid((unsigned)z.T);
+  const bf16* tp = static_cast<const bf16*>(tok);
+  const bf16* wp = static_cast<const bf16*>(w);
+#define RD(HH, N) \
+  if (z.H == HH && nt == N) \
+  return launch(k, agg_rowdot<HH, N>, grid, dim3(256), 0, s, tp, wp, w_tstride, out, o_t, o_v, o_h, \
+                alpha, z.V, z.d)
+  RD(8, 1); RD(8, 2); RD(8, 3); RD(8, 4); RD(8, 5); RD(8, 6);
+  RD(16, 1); RD(16, 2); RD(16, 3); RD(16, 4); RD(16, 5); RD(16, 6);
+#undef RD
+  set_error("%s: %d heads x %d variables outside the row-dot kernel's range", name, z.H, z.V);
+  return ORBIT_E_UNSUPPORTED;
+}
+
 }  // namespace
 
 size_t agg_saved_bytes(const orbit_agg_desc& a) {
@@ -542,7 +664,9 @@ orbit_status agg_forward(const orbit_agg_desc& a, const void* tok, const orbit_a
                      (const float*)p.w_k, (const float*)sv.q, (float*)sv.Ut, z.d, z.H, z.dh));
   }
   // 2. scores S[t*V+v][h] = x_{t,v} . u_h / sqrt(dh)
-  {
+  if (rowdot_ok(dt, z, tok, sv.Ut)) {
+    ORBIT_TRY(rowdot("agg_scores", z, tok, sv.Ut, 0, S, (int64_t)z.V * z.H, z.H, 1, 1.f / sqrtf((float)z.dh), s));
+  } else {
     Gemm g = base_gemm(dt);
     g.tag = "agg_scores";
     g.A = tok; g.lda = z.d; g.a_kmajor = true;
@@ -684,7 +808,9 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
     ORBIT_TRY(gemm(g, gws, gws_bytes, s));
   }
   // da_t [H, V] = dxbar_t [H, d] X_t^T
-  {
+  if (rowdot_ok(dt, z, tok, dxbar)) {
+    ORBIT_TRY(rowdot("agg_da", z, tok, dxbar, (int64_t)z.H * z.d, da, (int64_t)z.H * z.V, 1, z.V, 1.f, s));
+  } else {
     Gemm g = base_gemm(dt);
     g.tag = "agg_da";
     g.A = dxbar; g.lda = z.d; g.a_kmajor = true; g.sA = (int64_t)z.H * z.d;
