@@ -195,6 +195,15 @@ BLOCK_CASES = [
     ("bf16", 1, 520, 512, 2, 192, 512, 1),
     ("bf16", 1, 530, 512, 2, 256, 512, 0),
     ("bf16", 1, 300, 768, 4, 192, 512, 0),
+    # wide rows in the LayerNorm backward with its column sums: several waves
+    # per row (2048: 4 row groups per block; 8192: one 512-thread group;
+    # 16384: four 8-column pieces per thread), ragged last row chunks. With
+    # QK-LayerNorm, as the shard configurations use it: without it, logits of
+    # tens at these widths saturate the softmax and bf16 rounding moves the
+    # weight between near-tied keys (y off by ~3e-2 at 16384)
+    ("bf16", 1, 45, 2048, 2, 128, 512, 1),
+    ("bf16", 1, 37, 8192, 2, 128, 512, 1),
+    ("bf16", 2, 21, 16384, 1, 128, 256, 1),
 ]
 
 
