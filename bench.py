@@ -369,8 +369,8 @@ def main():
         print(json.dumps(cpu_baseline_child(a.workload)), flush=True)
         return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU's share of the model; runs on more than one GPU are not part "
-              "of this build (the multi-GPU layout is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU's share of the model (one tensor-parallel shard at its real "
+              "shape) on a single GPU; it has no multi-GPU mode: --gpus must be 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
