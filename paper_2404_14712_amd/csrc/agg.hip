@@ -334,6 +334,98 @@ __global__ void __launch_bounds__(256) agg_rowdot(const bf16* __restrict__ tok, 
   }
 }
 
+// dxbar[t][h][c] = sum_j dzh[t][h*DH + j] w_v[c][h*DH + j] (bf16): the value
+// path's input gradient, a reduction over only head_dim whose output has the
+// size of patches x heads x embedding. A block takes head h, 256 columns and
+// a range of patch rows, walked in chunks of 32 rows. Each wave keeps its 64
+// columns of W_v^h as MFMA fragments for the whole range; a chunk's dzh rows
+// (32 x DH) are copied once into LDS (two buffers, one barrier per chunk) and
+// read by all four waves; the 32x32x16 products' results go out through a
+// per-wave LDS stage as 16-byte row pieces (128 contiguous bytes per row).
+template <int DH>
+__global__ void __launch_bounds__(256) agg_value_dx(const bf16* __restrict__ dzh, const bf16* __restrict__ wv,
+                                                    bf16* __restrict__ dxbar, int T_, int H, int d, int rows) {
+  constexpr int KS = DH / 16;
+  constexpr int AP = DH + 8;  // LDS row pitch of the dzh chunk (elements)
+  __shared__ __attribute__((aligned(16))) bf16 abuf[2][32 * AP];
+  __shared__ __attribute__((aligned(16))) float stage[4][32][68];
+  const int A = H * DH;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int h = blockIdx.y;
+  const int c0 = blockIdx.x * 256 + wave * 64;
+  // the wave's 64 columns of W_v^h: two 32-column fragments per 16-deep step
+  bf16x8 bf[2][KS];
+#pragma unroll
+  for (int n = 0; n < 2; ++n) {
+    const bf16* wrow = wv + (int64_t)(c0 + n * 32 + lr) * A + h * DH + 8 * lg;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) bf[n][kk] = *reinterpret_cast<const bf16x8*>(wrow + 16 * kk);
+  }
+  const int tbeg = blockIdx.z * rows, tend = min(T_, tbeg + rows);
+  // chunk copy: 32 rows x DH / 8 pieces of 16 bytes over 256 threads, loaded
+  // into registers at the top of an iteration and written to LDS at its end
+  constexpr int PIECES = 32 * DH / 8, PPT = PIECES / 256;
+  static_assert(PIECES % 256 == 0, "whole pieces per thread");
+  bf16x8 pre[PPT];
+  auto load = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int pc = tid + i * 256, r = pc / (DH / 8), cc = (pc % (DH / 8)) * 8;
+      const int t = min(t0 + r, T_ - 1);  // rows past the last patch repeat it (never stored)
+      pre[i] = *reinterpret_cast<const bf16x8*>(dzh + (int64_t)t * A + h * DH + cc);
+    }
+  };
+  auto store = [&](bf16* dst) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int pc = tid + i * 256, r = pc / (DH / 8), cc = (pc % (DH / 8)) * 8;
+      *reinterpret_cast<bf16x8*>(dst + r * AP + cc) = pre[i];
+    }
+  };
+  if (tbeg < tend) {
+    load(tbeg);
+    store(abuf[0]);
+  }
+  __syncthreads();
+  int cur = 0;
+  for (int t0 = tbeg; t0 < tend; t0 += 32, cur ^= 1) {
+    const bool more = t0 + 32 < tend;
+    if (more) load(t0 + 32);
+    const bf16* as = abuf[cur] + lr * AP + 8 * lg;
+    f32x16 acc[2];
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[n][v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const bf16x8 af = *reinterpret_cast<const bf16x8*>(as + 16 * kk);
+#pragma unroll
+      for (int n = 0; n < 2; ++n) acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf[n][kk], acc[n], 0, 0, 0);
+    }
+    // acc[n][v]: chunk row 8 (v / 4) + 4 lg + v % 4, column 32 n + lr
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) stage[wave][(v >> 2) * 8 + lg * 4 + (v & 3)][n * 32 + lr] = acc[n][v];
+    __builtin_amdgcn_wave_barrier();
+    // 8 lanes per row, 8 columns each: 8 rows per pass
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int rl = it * 8 + (lane >> 3), cl = (lane & 7) * 8;
+      const int t = t0 + rl;
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(&stage[wave][rl][cl]);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[wave][rl][cl + 4]);
+      float o[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      if (t < tend) st128(dxbar + ((int64_t)t * H + h) * d + c0 + cl, pack(o, (bf16*)nullptr));
+    }
+    if (more) store(abuf[cur ^ 1]);
+    // the next chunk's rows are in LDS, and every wave is done with this one
+    __syncthreads();
+  }
+}
+
 // softmax backward per (t, h): ds = a (da - sum a da) * scale.
 // ac[(t*V + v)*2H + h] = a, ac[(t*V + v)*2H + H + h] = ds   (dtype); one wave per
 // token, lanes as in agg_softmax
@@ -798,7 +890,22 @@ orbit_status agg_backward(const orbit_agg_desc& a, const void* tok, const orbit_
     g.M = z.d; g.N = z.dh; g.K = (int)z.T; g.batch = z.H;
     ORBIT_TRY(gemm(g, gws, gws_bytes, s));
   }
-  {
+  if (dt == ORBIT_BF16 && (z.dh == 64 || z.dh == 128) && z.d % 256 == 0 && z.A % 8 == 0 &&
+      (reinterpret_cast<uintptr_t>(p.w_v) & 15) == 0) {
+    // row ranges: enough blocks for two per CU, whole 32-row chunks
+    const int64_t cols = (int64_t)(z.d / 256) * z.H;
+    const int64_t ranges = std::max<int64_t>(1, std::min<int64_t>(cdiv(z.T, 32), cdiv(512, cols)));
+    const int rows = (int)(cdiv(cdiv(z.T, ranges), 32) * 32);
+    KernelInfo kv{"agg_value_dx", 2.0 * z.T * z.H * (double)z.dh * z.d,
+                  (double)z.T * z.H * z.d * 2.0 + (double)z.d * z.A * 2.0 + (double)z.T * z.A * 2.0};
+    const dim3 grid((unsigned)(z.d / 256), (unsigned)z.H, (unsigned)cdiv(z.T, rows));
+    if (z.dh == 64)
+      ORBIT_TRY(launch(kv, agg_value_dx<64>, grid, dim3(256), 0, s, (const bf16*)dzh, (const bf16*)p.w_v,
+                       (bf16*)dxbar, (int)z.T, z.H, z.d, rows));
+    else
+      ORBIT_TRY(launch(kv, agg_value_dx<128>, grid, dim3(256), 0, s, (const bf16*)dzh, (const bf16*)p.w_v,
+                       (bf16*)dxbar, (int)z.T, z.H, z.d, rows));
+  } else {
     Gemm g = base_gemm(dt);
     g.tag = "agg_value_dx";
     g.A = dzh; g.lda = z.A; g.a_kmajor = true; g.sA = z.dh;

@@ -68,6 +68,7 @@ AGG_CASES = [
     ("bf16", 2, 9, 91, 512, 16, 64),       # 16 heads, odd V, A = 2d
     ("f32", 2, 11, 1, 64, 4, 16),          # one variable: the softmax is 1, two linears
     ("bf16", 1, 40, 1, 256, 8, 32),
+    ("bf16", 2, 37, 20, 512, 8, 128),      # head_dim 128, ragged 32-patch chunks
 ]
 
 
