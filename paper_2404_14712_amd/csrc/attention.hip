@@ -634,6 +634,58 @@ struct RowTile {
   }
 };
 
+// ROWS rows of one head's DH-column slices of two bf16 [L][ld] matrices
+// (sharing a row range), copied by the buffer unit straight into LDS in the
+// RowTile layout, [row][PITCH], with no staging registers: 1 KB wave copies,
+// copy c of a matrix filling 16-byte chunks 64c .. 64c + 63 of its area. The
+// copies are dealt round-robin over NW waves. A chunk in a row's padding or
+// in the last copy's slack, and every chunk of a row at or past L, is read at
+// an offset at or past the resource's extent, which the range check turns
+// into zeros (the copy then writes zeros).
+#define ORBIT_LDS __attribute__((address_space(3)))
+template <int ROWS, int DH, int NW>
+struct DmaRows {
+  static constexpr int PITCH = RowTile<ROWS, DH>::PITCH;
+  static constexpr int CPP = PITCH / 8;               // 16-byte chunks per LDS row
+  static constexpr int NC = (ROWS * CPP + 63) / 64;   // copies per matrix
+  static constexpr int BYTES = NC * 1024;             // LDS area of one matrix
+  static constexpr int PW = (2 * NC + NW - 1) / NW;   // copies per wave (the last may be idle)
+  static_assert(PITCH % 8 == 0, "whole chunks per row");
+  // (members, not arrays: the copy's matrix depends on the wave, and an
+  // array indexed by it would be kept in memory)
+  __amdgpu_buffer_rsrc_t rsrc0, rsrc1;
+  unsigned rb0, rb1;
+  unsigned voff[PW];
+  ORBIT_DEV void init(const bf16* x0, int64_t ld0, const bf16* x1, int64_t ld1, int L, int wave, int lane) {
+    rb0 = (unsigned)(ld0 * 2);
+    rb1 = (unsigned)(ld1 * 2);
+    rsrc0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(x0), 0, (int)(((int64_t)(L - 1) * ld0 + DH) * 2),
+                                              0x00020000);
+    rsrc1 = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(x1), 0, (int)(((int64_t)(L - 1) * ld1 + DH) * 2),
+                                              0x00020000);
+#pragma unroll
+    for (int i = 0; i < PW; ++i) {
+      const int cp = wave + NW * i, c = cp % NC;
+      const int p = c * 64 + lane, row = p / CPP, col = p % CPP;
+      const bool ok = cp < 2 * NC && row < ROWS && col < DH / 8;
+      voff[i] = ok ? (unsigned)row * (cp >= NC ? rb1 : rb0) + col * 16 : 0x80000000u;
+    }
+  }
+  // copies of rows row0 .. row0 + ROWS - 1; matrix m goes to LDS byte
+  // address lds + m * BYTES
+  ORBIT_DEV void issue(unsigned lds, int row0, int wave) const {
+#pragma unroll
+    for (int i = 0; i < PW; ++i) {
+      const int cp = wave + NW * i;
+      if (cp < 2 * NC) {
+        const bool m1 = cp >= NC;
+        const int c = m1 ? cp - NC : cp;
+        dma16(m1 ? rsrc1 : rsrc0, lds + (m1 ? BYTES : 0) + c * 1024, voff[i] + (unsigned)row0 * (m1 ? rb1 : rb0));
+      }
+    }
+  }
+};
+
 // sum of the 8 values of a bf16 fragment added to acc (two per instruction)
 ORBIT_DEV float frag_sum(const Frag<bf16>& f, float acc) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -846,6 +898,9 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 1) attn_fwd_tr(FwdArgs a) 
 // back exactly: dK_j += qbar (sum_i dS_ij - sum_i bf16(dS_ij)), both sums in
 // float32, which equals the centred form sum_i bf16(dS_ij) (q_i - qbar) +
 // qbar sum_i dS_ij.
+// The Q and dO tiles come in by LDS copies (no staging registers), which
+// leaves the registers to read each product's fragments one step ahead of
+// the product that uses them.
 // QG = 2 (grids of at most one block per CU): two groups of 4 waves share the
 // block's 128 keys and take alternate query tiles; group 1's dK, dV partials
 // are added to group 0's through LDS at the end (fixed order).
@@ -854,23 +909,22 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : DH == 128 ? 2 : DH == 
 attn_bwd_dkdv_tr(BwdArgs a) {
   using T = bf16;
   constexpr int QT = 32 * QS;  // queries per LDS tile: QS sub-tiles of 32 per barrier
-  using TL = RowTile<QT, DH>;  // Q and dO rows [q][c]
-  constexpr int RP = TL::PITCH;
+  using DT = DmaRows<QT, DH, 4>;  // Q and dO rows [q][c] of a query tile
+  constexpr int RP = DT::PITCH;
+  constexpr int TE = DT::BYTES / 2;  // elements of one matrix area
   // the block's V rows stay in LDS rather than in registers, which brings the
   // kernel within the register budget of three waves per SIMD at head_dim 64
   // and two at head_dim 128
   constexpr bool VLDS = DH >= 64;
-  __shared__ __attribute__((aligned(16))) T qs_all[QG][2][QT * RP];
-  __shared__ __attribute__((aligned(16))) T os_all[QG][2][QT * RP];
+  __shared__ __attribute__((aligned(16))) T tiles[QG][2][2][TE];  // [group][buffer][Q, dO]
   __shared__ __attribute__((aligned(16))) T vsh[VLDS ? 128 * RP : 8];
   __shared__ float lse_all[QG][2][QT], d_all[QG][2][QT];
   __shared__ float qbar[DH];
 
   const int lane = threadIdx.x & 63, g = lane >> 5;
   const int grp = QG == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8);
-  const int tid = threadIdx.x & 255, wave = tid >> 6;
-  auto& qs = qs_all[grp];
-  auto& os = os_all[grp];
+  const int tid = threadIdx.x & 255;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   auto& lse_s = lse_all[grp];
   auto& d_s = d_all[grp];
   int xb, h, b;
@@ -914,9 +968,10 @@ attn_bwd_dkdv_tr(BwdArgs a) {
     for (int v = 0; v < 16; ++v) dvt[c][v] = dkt[c][v] = 0.f;
 
   float cs = 0.f, csr = 0.f;
-  TL tq, to;
-  tq.init(Q, a.ldq, L, tid);
-  to.init(dO, a.lddo, L, tid);
+  DT dma;
+  dma.init(Q, a.ldq, dO, a.lddo, L, wave, lane);
+  const unsigned tlds = (unsigned)(uintptr_t)(ORBIT_LDS void*)&tiles[grp][0][0][0];
+  constexpr unsigned BUF = 2 * DT::BYTES;
   // this split's query tiles qt0 .. qt0 + nq - 1
   const int nqa = (L + QT - 1) / QT, qper = (nqa + a.ns - 1) / a.ns, qt0 = sp * qper;
   const int nq = max(0, min(nqa, qt0 + qper) - qt0);
@@ -926,107 +981,129 @@ attn_bwd_dkdv_tr(BwdArgs a) {
   const int iters = (nq + QG - 1) / QG;
   {
     const int q0 = (qt0 + grp) * QT;
-    tq.load(q0);
-    to.load(q0);
-    tq.store(qs[0]);
-    to.store(os[0]);
+    dma.issue(tlds, q0, wave);
     if (tid < QT) {
       lse_s[0][tid] = q0 + tid < L ? lse[q0 + tid] * kLog2e : INFINITY;
       d_s[0][tid] = q0 + tid < L ? Dv[q0 + tid] : 0.f;
     }
   }
+  wait_vmcnt<0>();
   __syncthreads();
+  constexpr int KS = DH / 16, NC3 = DH / 32;
   for (int i = 0; i < iters; ++i) {
     const int it = i * QG + grp;
     const int cur = i & 1;
     float lse_n = 0.f, d_n = 0.f;
     if (it + QG < nq) {
       const int q1 = (qt0 + it + QG) * QT;
-      tq.load(q1);
-      to.load(q1);
+      dma.issue(tlds + (cur ^ 1) * BUF, q1, wave);
       if (tid < QT) {
         lse_n = q1 + tid < L ? lse[q1 + tid] * kLog2e : INFINITY;
         d_n = q1 + tid < L ? Dv[q1 + tid] : 0.f;
       }
     }
     if (QG == 1 || it < nq) {
-    f32x16 s[QS], dp[QS];
+      const T* Qs = &tiles[grp][cur][0][0];
+      const T* Os = &tiles[grp][cur][1][0];
+      // S = Q K^T and dP = dO V^T; step kk + 1's fragments are read before
+      // step kk's products are issued
+      f32x16 s[QS], dp[QS];
 #pragma unroll
-    for (int q = 0; q < QS; ++q) {
-      const T* Qs = qs[cur] + q * 32 * RP;
-      const T* Os = os[cur] + q * 32 * RP;
+      for (int q = 0; q < QS; ++q)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[q][v] = dp[q][v] = 0.f;
+        for (int v = 0; v < 16; ++v) s[q][v] = dp[q][v] = 0.f;
+      // (fragments rotate through named variables: arrays indexed by the
+      // buffer parity would be placed in memory before unrolling)
+      Frag<T> cq[QS], co[QS], cv, nq[QS], no[QS], nv;
+      auto ld1 = [&](int kk) {
 #pragma unroll
-      for (int kk = 0; kk < DH / 16; ++kk) {
-        Frag<T> af;
-        ld_frag(af, Qs + (lane & 31) * RP + kk * 16 + g * 8);
-        mma16(s[q], af, kf[kk]);
-        ld_frag(af, Os + (lane & 31) * RP + kk * 16 + g * 8);
-        if constexpr (VLDS) {
-          Frag<T> vk;
-          ld_frag(vk, vrow + kk * 16);
-          mma16(dp[q], af, vk);
-        } else {
-          mma16(dp[q], af, vf[kk]);
+        for (int q = 0; q < QS; ++q) {
+          ld_frag(nq[q], Qs + (q * 32 + (lane & 31)) * RP + kk * 16 + g * 8);
+          ld_frag(no[q], Os + (q * 32 + (lane & 31)) * RP + kk * 16 + g * 8);
         }
-      }
-    }
+        if constexpr (VLDS) ld_frag(nv, vrow + kk * 16);
+      };
+      auto rot1 = [&]() {
 #pragma unroll
-    for (int q = 0; q < QS; ++q) {
-      const T* Qs = qs[cur] + q * 32 * RP;
-      const T* Os = os[cur] + q * 32 * RP;
-      // rows: query 8*(v/4) + 4g + v%4 of the sub-tile; column: this lane's key
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int qr = q * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[q][v], a.sl2, -lse_s[cur][qr]));
-        s[q][v] = p;
-        dp[q][v] = p * (dp[q][v] - d_s[cur][qr]);
-        cs += dp[q][v];
-      }
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        Frag<T> pf, sf;
-        acc_frag(pf, s[q], kk * 8);
-        acc_frag(sf, dp[q], kk * 8);
-        csr = frag_sum(sf, csr);
-#pragma unroll
-        for (int c = 0; c < DH / 32; ++c) {
-          Frag<T> af;
-          ld_frag_tr(af, Os + kk * 16 * RP + c * 32, RP, lane);
-          mma16(dvt[c], af, pf);
-          ld_frag_tr(af, Qs + kk * 16 * RP + c * 32, RP, lane);
-          mma16(dkt[c], af, sf);
+        for (int q = 0; q < QS; ++q) {
+          cq[q] = nq[q];
+          co[q] = no[q];
         }
+        cv = nv;
+      };
+      ld1(0);
+      rot1();
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        if (kk + 1 < KS) ld1(kk + 1);
+#pragma unroll
+        for (int q = 0; q < QS; ++q) {
+          mma16(s[q], cq[q], kf[kk]);
+          if constexpr (VLDS) mma16(dp[q], co[q], cv);
+          else mma16(dp[q], co[q], vf[kk]);
+        }
+        rot1();
+      }
+      // P and dS; rows: query 8*(v/4) + 4g + v%4 of the sub-tile, column:
+      // this lane's key
+#pragma unroll
+      for (int q = 0; q < QS; ++q)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int qr = q * 32 + (v >> 2) * 8 + g * 4 + (v & 3);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[q][v], a.sl2, -lse_s[cur][qr]));
+          s[q][v] = p;
+          dp[q][v] = p * (dp[q][v] - d_s[cur][qr]);
+          cs += dp[q][v];
+        }
+      // dV^T += dO^T P and dK^T += Q^T dS, step n + 1's transposed fragments
+      // read before step n's products
+      constexpr int N3 = QS * 2 * NC3;
+      Frag<T> to, tq, tno, tnq, pf, sf;
+      auto ld3 = [&](int n) {
+        const int q = n / (2 * NC3), kk = (n / NC3) & 1, c = n % NC3;
+        const int off = (q * 32 + kk * 16) * RP + c * 32;
+        ld_frag_tr(tno, Os + off, RP, lane);
+        ld_frag_tr(tnq, Qs + off, RP, lane);
+      };
+      ld3(0);
+      to = tno;
+      tq = tnq;
+#pragma unroll
+      for (int n = 0; n < N3; ++n) {
+        const int q = n / (2 * NC3), kk = (n / NC3) & 1, c = n % NC3;
+        if (c == 0) {
+          acc_frag(pf, s[q], kk * 8);
+          acc_frag(sf, dp[q], kk * 8);
+          csr = frag_sum(sf, csr);
+        }
+        if (n + 1 < N3) ld3(n + 1);
+        mma16(dvt[c], to, pf);
+        mma16(dkt[c], tq, sf);
+        to = tno;
+        tq = tnq;
       }
     }
+    if (it + QG < nq && tid < QT) {
+      lse_s[cur ^ 1][tid] = lse_n;
+      d_s[cur ^ 1][tid] = d_n;
     }
-    if (it + QG < nq) {
-      tq.store(qs[cur ^ 1]);
-      to.store(os[cur ^ 1]);
-      if (tid < QT) {
-        lse_s[cur ^ 1][tid] = lse_n;
-        d_s[cur ^ 1][tid] = d_n;
-      }
-    }
+    wait_vmcnt<0>();
     __syncthreads();
   }
 
   cs += __shfl_xor(cs, 32, 64);
   csr += __shfl_xor(csr, 32, 64);
   if constexpr (QG == 2) {
-    // group 1 hands its partials to group 0 through the idle tile areas (the
-    // Q tiles, the dO tiles and the V rows: separate arrays, each holds 32
-    // floats per thread), dV^T first, then dK^T and the remainder sums;
-    // group 0 adds them in that fixed order
+    // group 1 hands its partials to group 0 through the idle tile areas (two
+    // regions of the tile buffers and the V rows: each holds 32 floats per
+    // thread), dV^T first, then dK^T and the remainder sums; group 0 adds
+    // them in that fixed order
     static_assert(VLDS, "the exchange uses the V-row area");
-    constexpr int C = DH / 32, CPR = (C + 1) / 2;
-    static_assert(CPR * 16 * 256 * 4 <= (int)sizeof(qs_all) && CPR * 16 * 256 * 4 <= (int)sizeof(os_all) &&
-                      2 * 256 * 4 <= (int)sizeof(vsh),
-                  "exchange areas");
-    float* region[3] = {reinterpret_cast<float*>(&qs_all[0][0][0]), reinterpret_cast<float*>(&os_all[0][0][0]),
-                        reinterpret_cast<float*>(vsh)};
+    constexpr int C = DH / 32, CPR = (C + 1) / 2, RB = CPR * 16 * 256 * 4;
+    static_assert(2 * RB <= (int)sizeof(tiles) && 2 * 256 * 4 <= (int)sizeof(vsh), "exchange areas");
+    float* region[3] = {reinterpret_cast<float*>(&tiles[0][0][0][0]),
+                        reinterpret_cast<float*>(&tiles[0][0][0][0]) + RB / 4, reinterpret_cast<float*>(vsh)};
     auto slot = [&](int c, int v) -> float& {
       return region[c / CPR][(wave * CPR * 16 + (c % CPR) * 16 + v) * 64 + lane];
     };
@@ -1106,6 +1183,8 @@ attn_bwd_dkdv_tr(BwdArgs a) {
 // dQ_i = sum_j dS_ij k_j = sum_j dS_ij (k_j - kbar) since sum_j dS_ij = 0; the
 // product runs on the uncentred keys and kbar sum_j bf16(dS_ij) (float32) is
 // subtracted, which equals the centred form sum_j bf16(dS_ij) (k_j - kbar).
+// The K and V tiles come in by LDS copies (no staging registers), and each
+// product's fragments are read one step ahead of the product.
 // QG = 2 (grids of at most one block per CU): two groups of 4 waves share the
 // block's 128 queries and take alternate key tiles; group 1's dQ partials are
 // added to group 0's through LDS at the end (fixed order).
@@ -1113,17 +1192,16 @@ template <int DH, int QG = 1>
 __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdArgs a) {
   using T = bf16;
   constexpr int KT = 64;
-  using TL = RowTile<KT, DH>;  // K and V rows [kv][c]
-  constexpr int KP = TL::PITCH;
-  __shared__ __attribute__((aligned(16))) T ks_all[QG][2][KT * KP];
-  __shared__ __attribute__((aligned(16))) T vs_all[QG][2][KT * KP];
+  using DT = DmaRows<KT, DH, 4>;  // K and V rows [kv][c] of a key tile
+  constexpr int KP = DT::PITCH;
+  constexpr int TE = DT::BYTES / 2;
+  __shared__ __attribute__((aligned(16))) T tiles[QG][2][2][TE];  // [group][buffer][K, V]
   __shared__ float kbar[DH];
 
   const int lane = threadIdx.x & 63, g = lane >> 5;
   const int grp = QG == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8);
-  const int tid = threadIdx.x & 255, wave = tid >> 6;
-  auto& ks = ks_all[grp];
-  auto& vs = vs_all[grp];
+  const int tid = threadIdx.x & 255;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int xb, h, b;
   attn_block_coords(xb, h, b);
   const int L = a.L;
@@ -1159,27 +1237,24 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
     for (int v = 0; v < 16; ++v) dqt[c][v] = 0.f;
   float rs = 0.f;
 
-  TL tk, tv;
-  tk.init(K, a.ldk, L, tid);
-  tv.init(V, a.ldv, L, tid);
+  DT dma;
+  dma.init(K, a.ldk, V, a.ldv, L, wave, lane);
+  const unsigned tlds = (unsigned)(uintptr_t)(ORBIT_LDS void*)&tiles[grp][0][0][0];
+  constexpr unsigned BUF = 2 * DT::BYTES;
   // this split's key tiles [t0, t1)
   const int nt = (L + KT - 1) / KT, per = (nt + a.ns - 1) / a.ns;
   const int t0 = sp * per, t1 = min(nt, t0 + per);
   // group grp takes key tiles t0 + grp, t0 + grp + QG, ...; both groups run
   // the same number of iterations (shared barriers)
-  tk.load((t0 + grp) * KT);
-  tv.load((t0 + grp) * KT);
-  tk.store(ks[0]);
-  tv.store(vs[0]);
+  dma.issue(tlds, (t0 + grp) * KT, wave);
+  wait_vmcnt<0>();
   __syncthreads();
 
+  constexpr int KS = DH / 16, NC3 = DH / 32;
   auto tile = [&](int jt, int cur, auto mask) {
-    if (jt + QG < t1) {
-      tk.load((jt + QG) * KT);
-      tv.load((jt + QG) * KT);
-    }
-    const T* Ks = ks[cur];
-    const T* Vs = vs[cur];
+    if (jt + QG < t1) dma.issue(tlds + (cur ^ 1) * BUF, (jt + QG) * KT, wave);
+    const T* Ks = &tiles[grp][cur][0][0];
+    const T* Vs = &tiles[grp][cur][1][0];
     f32x16 s[2], dp[2];
     // the softmax of a 32-key half; at head_dim 64 both halves' products are
     // issued before either half's softmax (the register budget allows it)
@@ -1197,41 +1272,56 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
       }
     };
     constexpr bool kBoth = DH == 64;
+    // S^T = K Q^T and dP^T = V dO^T over the two 32-key halves, step n + 1's
+    // fragments read before step n's products
+    Frag<T> ck, cv, nk, nv;
+    auto ld1 = [&](int n) {
+      const int mt = n / KS, kk = n % KS;
+      ld_frag(nk, Ks + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+      ld_frag(nv, Vs + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
+    };
+    ld1(0);
+    ck = nk;
+    cv = nv;
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
+    for (int n = 0; n < 2 * KS; ++n) {
+      const int mt = n / KS, kk = n % KS;
+      if (kk == 0)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[mt][v] = dp[mt][v] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < DH / 16; ++kk) {
-        Frag<T> af;
-        ld_frag(af, Ks + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
-        mma16(s[mt], af, qf[kk]);
-        ld_frag(af, Vs + (mt * 32 + (lane & 31)) * KP + kk * 16 + g * 8);
-        mma16(dp[mt], af, of[kk]);
-      }
-      if constexpr (!kBoth) soft(mt);
+        for (int v = 0; v < 16; ++v) s[mt][v] = dp[mt][v] = 0.f;
+      if (n + 1 < 2 * KS) ld1(n + 1);
+      mma16(s[mt], ck, qf[kk]);
+      mma16(dp[mt], cv, of[kk]);
+      ck = nk;
+      cv = nv;
+      if (!kBoth && kk == KS - 1) soft(mt);
     }
     if constexpr (kBoth) {
       soft(0);
       soft(1);
     }
-    // dQ^T[c][q] += K^T[c][kv] dS^T[kv][q]
+    // dQ^T[c][q] += K^T[c][kv] dS^T[kv][q], step n + 1's transposed K
+    // fragment read before step n's product
+    constexpr int N3 = (KT / 16) * NC3;
+    Frag<T> ct, nt3, sf;
+    auto ld3 = [&](int n) {
+      const int kk = n / NC3, c = n % NC3;
+      ld_frag_tr(nt3, Ks + kk * 16 * KP + c * 32, KP, lane);
+    };
+    ld3(0);
+    ct = nt3;
 #pragma unroll
-    for (int kk = 0; kk < KT / 16; ++kk) {
-      Frag<T> sf;
-      acc_frag(sf, dp[kk >> 1], (kk & 1) * 8);
-      rs = frag_sum(sf, rs);
-#pragma unroll
-      for (int c = 0; c < DH / 32; ++c) {
-        Frag<T> af;
-        ld_frag_tr(af, Ks + kk * 16 * KP + c * 32, KP, lane);
-        mma16(dqt[c], af, sf);
+    for (int n = 0; n < N3; ++n) {
+      const int kk = n / NC3, c = n % NC3;
+      if (c == 0) {
+        acc_frag(sf, dp[kk >> 1], (kk & 1) * 8);
+        rs = frag_sum(sf, rs);
       }
+      if (n + 1 < N3) ld3(n + 1);
+      mma16(dqt[c], ct, sf);
+      ct = nt3;
     }
-    if (jt + QG < t1) {
-      tk.store(ks[cur ^ 1]);
-      tv.store(vs[cur ^ 1]);
-    }
+    wait_vmcnt<0>();
     __syncthreads();
   };
   // full tiles of the range (the sequence's partial last tile, if any, comes last)
@@ -1253,12 +1343,12 @@ __global__ void __launch_bounds__(256 * QG, QG == 2 ? 1 : 1) attn_bwd_dq_tr(BwdA
 
   rs += __shfl_xor(rs, 32, 64);
   if constexpr (QG == 2) {
-    // group 1's dQ^T partials and remainder sum to group 0 through the idle
-    // K-tile area (dQ^T) and V-tile area (sums)
+    // group 1's dQ^T partials and remainder sums to group 0 through the idle
+    // tile buffers
     constexpr int C = DH / 32;
-    static_assert(C * 16 * 256 * 4 <= (int)sizeof(ks_all) && 256 * 4 <= (int)sizeof(vs_all), "exchange areas");
-    float* rq = reinterpret_cast<float*>(&ks_all[0][0][0]) + wave * C * 16 * 64 + lane;
-    float* rr = reinterpret_cast<float*>(&vs_all[0][0][0]) + wave * 64 + lane;
+    static_assert(C * 16 * 256 * 4 + 256 * 4 <= (int)sizeof(tiles), "exchange areas");
+    float* rq = reinterpret_cast<float*>(&tiles[0][0][0][0]) + wave * C * 16 * 64 + lane;
+    float* rr = reinterpret_cast<float*>(&tiles[0][0][0][0]) + C * 16 * 256 + wave * 64 + lane;
     if (grp == 1) {
 #pragma unroll
       for (int c = 0; c < C; ++c)
@@ -1421,10 +1511,12 @@ __global__ void __launch_bounds__(256) attn_dq_merge(BwdArgs a) {
 }
 
 // the bf16 kernels address one (sample, head) slice of q, k, v (and dO) with
-// 32-bit byte offsets, and the backward preprocess indexes head rows in 32 bits
+// 32-bit byte offsets (tiles reach up to 256 rows past the last one, and an
+// out-of-range marker of 2^31 is added to such offsets), and the backward
+// preprocess indexes head rows in 32 bits
 bool slices_fit(const AttnIO& io, int64_t ld_extra) {
   const int64_t ld = std::max(std::max(io.ldq, io.ldk), std::max(io.ldv, ld_extra));
-  return (int64_t)io.L * ld * 4 < ((int64_t)1 << 31) && (int64_t)io.B * io.L * io.H < ((int64_t)1 << 31);
+  return ((int64_t)io.L + 256) * ld * 4 < ((int64_t)1 << 31) && (int64_t)io.B * io.L * io.H < ((int64_t)1 << 31);
 }
 
 // bf16 grids of fewer than 256 blocks of 128 positions (one sample-head pair

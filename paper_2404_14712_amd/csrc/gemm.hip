@@ -282,15 +282,6 @@ ORBIT_DEV __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
 }
 
-// one wave copies 64 x 16 bytes from rsrc + voff (per lane) to LDS byte address
-// lds + 16 * lane. M0 carries the wave-uniform LDS address; the copy is
-// written as inline assembly so that the compiler does not order LDS reads
-// behind it (completion is awaited explicitly with s_waitcnt vmcnt).
-ORBIT_DEV void dma16(__amdgpu_buffer_rsrc_t r, unsigned lds, unsigned voff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff), "s"(r)
-               : "memory");
-}
-template <int N> ORBIT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
 // Copy plan of one operand slice (ROWS rows x 32 k) over NW waves, per lane.
 //  K-major source X[row*ld + k]: LDS row r holds 64 bytes (4 chunks of 8 k);

@@ -1,5 +1,6 @@
-// HBM -> register -> LDS staging of one operand tile, shared by the GEMM and
-// the attention kernels.
+// HBM -> LDS staging shared by the GEMM and the attention kernels: the
+// buffer unit's direct 1 KB wave copies (dma16), and the register-staged
+// copy of one operand tile (TileLoader).
 //
 // The LDS copy is always K-contiguous: S[row][k] with a row pitch of KD + 16
 // bytes (the padding spreads the 16-byte fragment reads of 32 consecutive
@@ -12,6 +13,16 @@
 #include "common.h"
 
 namespace orbit {
+
+// one wave copies 64 x 16 bytes from rsrc + voff (per lane) to LDS byte address
+// lds + 16 * lane. M0 carries the wave-uniform LDS address; the copy is
+// written as inline assembly so that the compiler does not order LDS reads
+// behind it (completion is awaited explicitly with s_waitcnt vmcnt).
+ORBIT_DEV void dma16(__amdgpu_buffer_rsrc_t r, unsigned lds, unsigned voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
+template <int N> ORBIT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
 template <typename T, int ROWS, int KD, int NT, bool KMAJ>
 struct TileLoader {
