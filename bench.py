@@ -361,6 +361,9 @@ def main():
     ap.add_argument("--cpu-baseline-only", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (reference for HBM byte counters) and exit")
+    ap.add_argument("--attention-shape", default=None, metavar="B,H,L,DH",
+                    help="run the bf16 attention forward once and its backward 8 times on one shape "
+                         "(for hardware counters of the attention kernels alone) and exit")
     ap.add_argument("--kernel-table", action="store_true",
                     help="print, instead of the JSON line, a markdown table of every kernel of one "
                          "instrumented step: time, algorithmic flops and bytes, achieved rate against peak")
@@ -406,6 +409,37 @@ def main():
             res[nm] = {"ms": round(ms, 4), "tflops": round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)}
             del A, Bm, C, ws
         print(json.dumps({"gemm_layouts": res, "M": M, "N": N, "K": K}), flush=True)
+        return
+    if a.attention_shape:
+        # q, k, v as column slices of one [T, 3A] bf16 buffer (as in a block),
+        # O in float32 (as the block hands it to the backward), N(0, 1/4)
+        # scores-scale inputs; times the backward with events
+        from paper_2404_14712_amd import load as _load
+        alib = _load()
+        B, H, L, dh = (int(v) for v in a.attention_shape.split(","))
+        A = H * dh
+        gen = torch.Generator(device=dev).manual_seed(0)
+        qkv = (torch.randn(B * L, 3 * A, device=dev, generator=gen) * 0.5).to(torch.bfloat16)
+        dO = torch.randn(B * L, A, device=dev, generator=gen).to(torch.bfloat16)
+        e = qkv.element_size()
+        q, k, v = qkv.data_ptr(), qkv.data_ptr() + A * e, qkv.data_ptr() + 2 * A * e
+        o = torch.empty(B * L, A, dtype=torch.bfloat16, device=dev)
+        o32 = torch.empty(B * L, A, dtype=torch.float32, device=dev)
+        lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
+        alib.orbit_attention_fwd(1, B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o, A, lse, o32, A)
+        g = torch.empty(B * L, 3 * A, dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(alib.orbit_attention_bwd_workspace_bytes(B, H, L, dh), dtype=torch.uint8, device=dev)
+        gp = g.data_ptr()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(9)]
+        ev[0].record()
+        for i in range(8):
+            alib.orbit_attention_bwd(1, B, H, L, dh, q, 3 * A, k, 3 * A, v, 3 * A, o32, A, 1, lse, dO, A,
+                                     gp, gp + A * e, gp + 2 * A * e, 3 * A, ws)
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(8))[4]
+        print(json.dumps({"attention_backward": {"B": B, "H": H, "L": L, "head_dim": dh, "ms_median": round(ms, 4),
+                                                 "launches": 8}}), flush=True)
         return
     if a.copy_calibration:
         # a streaming elementwise kernel that reads and writes exactly 1 GiB each
