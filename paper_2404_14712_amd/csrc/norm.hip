@@ -594,48 +594,58 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
   const unsigned nr = 2u * H;
   const unsigned nrows = (unsigned)T_ * nr;
   // every row group of every block runs the same number of iterations
-  // (shuffles); each iteration takes kQkRows rows, loads first
+  // (shuffles); each iteration takes kQkRows rows, whose loads were issued
+  // during the previous iteration (packed, as loaded)
   constexpr int kQkRows = 4;
   const unsigned stride = gridDim.x * (unsigned)NG;
   const unsigned iters = (nrows + stride * kQkRows - 1) / (stride * kQkRows);
   const unsigned st = stride / nr, sj = stride - st * nr;
   unsigned row = blockIdx.x * (unsigned)NG + grp;
   unsigned tc = row / nr, jc = row - tc * nr;
-  for (unsigned it = 0; it < iters; ++it) {
-    float dy[kQkRows][8], xv[kQkRows][8];
+  struct Batch {
+    Raw8<T> dy[kQkRows], xv[kQkRows];
     int64_t off_d[kQkRows];
-    int sidx[kQkRows];
-    bool valid[kQkRows];
+    bool k[kQkRows], valid[kQkRows];
     float mu[kQkRows], r[kQkRows];
+  };
+  auto fetch = [&](Batch& B) {
 #pragma unroll
     for (int u = 0; u < kQkRows; ++u) {
-      valid[u] = row < nrows;
-      sidx[u] = (int)jc >= H;
-      off_d[u] = (int64_t)tc * ldd + jc * DH + li * 8;
+      B.valid[u] = row < nrows;
+      B.k[u] = (int)jc >= H;
+      B.off_d[u] = (int64_t)tc * ldd + jc * DH + li * 8;
       const int64_t off_s = (int64_t)tc * lds + jc * DH + li * 8;
       const unsigned rcur = row;
       row += stride;
       jc += sj;
       tc += st;
       if (jc >= nr) { jc -= nr; ++tc; }
-      if (valid[u] && lv) {
-        load8(d + off_d[u], dy[u]);
-        load8(src + off_s, xv[u]);
+      if (B.valid[u] && lv) {
+        B.dy[u].load(d + B.off_d[u]);
+        B.xv[u].load(src + off_s);
       } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) dy[u][i] = xv[u][i] = 0.f;
+        B.dy[u].zero();
+        B.xv[u].zero();
       }
-      mu[u] = valid[u] ? mean[rcur] : 0.f;
-      r[u] = valid[u] ? rstd[rcur] : 0.f;
+      B.mu[u] = B.valid[u] ? mean[rcur] : 0.f;
+      B.r[u] = B.valid[u] ? rstd[rcur] : 0.f;
     }
+  };
+  Batch cur;
+  if (iters > 0) fetch(cur);
+  for (unsigned it = 0; it < iters; ++it) {
+    Batch nxt;
+    if (it + 1 < iters) fetch(nxt);
 #pragma unroll
     for (int u = 0; u < kQkRows; ++u) {
-      float xh[8], gh[8];
+      float dy[8], xv[8], xh[8], gh[8];
+      cur.dy[u].get(dy);
+      cur.xv[u].get(xv);
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        xh[i] = (xv[u][i] - mu[u]) * r[u];
-        gh[i] = dy[u][i] * (sidx[u] ? gk[i] : gq[i]);
+        xh[i] = (xv[i] - cur.mu[u]) * cur.r[u];
+        gh[i] = dy[i] * (cur.k[u] ? gk[i] : gq[i]);
         s1 += gh[i];
         s2 += gh[i] * xh[i];
       }
@@ -644,19 +654,20 @@ __global__ void __launch_bounds__(256) qkln_bwd_kernel(T* d, int64_t ldd, const 
         s1 += __shfl_xor(s1, o, 64);
         s2 += __shfl_xor(s2, o, 64);
       }
-      if (valid[u] && lv) {
+      if (cur.valid[u] && lv) {
         const float m1 = s1 / (float)DH, m2 = s2 / (float)DH;
         float o8[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) o8[i] = r[u] * (gh[i] - m1 - xh[i] * m2);
-        store8(d + off_d[u], o8);
+        for (int i = 0; i < 8; ++i) o8[i] = cur.r[u] * (gh[i] - m1 - xh[i] * m2);
+        store8(d + cur.off_d[u], o8);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          if (sidx[u]) { ag[1][i] += dy[u][i] * xh[i]; ab[1][i] += dy[u][i]; }
-          else         { ag[0][i] += dy[u][i] * xh[i]; ab[0][i] += dy[u][i]; }
+          if (cur.k[u]) { ag[1][i] += dy[i] * xh[i]; ab[1][i] += dy[i]; }
+          else          { ag[0][i] += dy[i] * xh[i]; ab[0][i] += dy[i]; }
         }
       }
     }
+    cur = nxt;
   }
   if (lv) {
 #pragma unroll
