@@ -110,6 +110,47 @@ def test_attention_split_backward(lib, dtype, dh):
     _attention_case(lib, dtype, dh, 600, 1.0, repeat=True)
 
 
+@pytest.mark.parametrize("dh", [64, 128, 192])
+def test_attention_separate_strides(lib, dh):
+    """q, k, v, dO and the gradients in separate buffers with five different
+    row strides (all multiples of 8), columns past each matrix's heads
+    filled with NaN: the tiles copied into LDS take each matrix's own
+    stride and read no padding (a NaN there would reach the results); 130
+    positions leave a partial last tile. bf16."""
+    import torch
+    B, H, L = 2, 3, 130
+    A = H * dh
+    T = B * L
+    ld = {"q": A + 8, "k": A + 24, "v": 2 * A, "dO": A + 40, "g": A + 16}
+    data = {n: _mat((T, A), "bf16", 1.0) for n in ("q", "k", "v", "dO")}
+    buf = {}
+    for n, a in data.items():
+        full = np.full((T, ld[n]), np.nan, np.float32)
+        full[:, :A] = a
+        buf[n] = dev(full, "bf16")
+    o = torch.zeros(T, A, dtype=torch.bfloat16, device="cuda")
+    o32 = torch.zeros(T, A, dtype=torch.float32, device="cuda")
+    lse = torch.zeros(B, H, L, dtype=torch.float32, device="cuda")
+    lib.orbit_attention_fwd(1, B, H, L, dh, buf["q"], ld["q"], buf["k"], ld["k"], buf["v"], ld["v"], o, A, lse,
+                            o32, A)
+    grads = {n: torch.full((T, ld["g"]), float("nan"), dtype=torch.bfloat16, device="cuda") for n in ("q", "k", "v")}
+    ws = torch.zeros(lib.orbit_attention_bwd_workspace_bytes(B, H, L, dh), dtype=torch.uint8, device="cuda")
+    lib.orbit_attention_bwd(1, B, H, L, dh, buf["q"], ld["q"], buf["k"], ld["k"], buf["v"], ld["v"], o32, A, 1, lse,
+                            buf["dO"], ld["dO"], grads["q"], grads["k"], grads["v"], ld["g"], ws)
+    torch.cuda.synchronize()
+    hd = lambda x: x.reshape(B, L, H, dh).transpose(0, 2, 1, 3)
+    un = lambda x: x.transpose(0, 2, 1, 3).reshape(T, A)
+    Q, K_, V_ = hd(data["q"]), hd(data["k"]), hd(data["v"])
+    ref_o, P = O.attention_fwd(Q, K_, V_)
+    dq, dk, dv = O.attention_bwd(hd(data["dO"]), Q, K_, V_, P)
+    tol = TOL["bf16"]
+    check("o", host(o), un(ref_o), tol)
+    for n, ref in (("q", dq), ("k", dk), ("v", dv)):
+        gh = host(grads[n])
+        check("d" + n, gh[:, :A], un(ref), tol)
+        assert np.isnan(gh[:, A:]).all(), f"d{n}: columns past the heads were written"
+
+
 def _attention_case(lib, dtype, dh, L, qk_scale, repeat=False):
     import torch
     B, H = 2, 3
