@@ -75,6 +75,47 @@ def test_gemm(lib, dtype, layout, shape):
           else 1e-2)
 
 
+STRIDED_SHAPES = [(200, 136, 72), (304, 520, 256), (520, 1032, 1024), (1000, 264, 4096), (2048, 1024, 1024)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", list(LAYOUTS))
+@pytest.mark.parametrize("shape", STRIDED_SHAPES, ids=[f"{m}x{n}x{k}" for m, n, k in STRIDED_SHAPES])
+def test_gemm_strided(lib, dtype, layout, shape):
+    """Operands and output as row slices of wider buffers (row strides past
+    the contiguous dimension, as the block's q/k/v views of one QKV buffer
+    are), the columns past each matrix filled with NaN: a read of them
+    would reach the product, a write past N would overwrite them. Covers
+    the direct-to-LDS tiles, split K and the register-staged kernel."""
+    import torch
+    M, N, K = shape
+    a_k, b_k = LAYOUTS[layout]
+    A = _mat((M, K), dtype)
+    B = _mat((K, N), dtype)
+    lda = (K if a_k else M) + 24
+    ldb = (K if b_k else N) + 40
+    ldc = N + 8
+
+    def padded(x, ld):
+        full = np.full((x.shape[0], ld), np.nan, np.float32)
+        full[:, :x.shape[1]] = x
+        return dev(full, dtype)
+
+    Adev = padded(A if a_k else A.T.copy(), lda)
+    Bdev = padded(B.T.copy() if b_k else B, ldb)
+    for c_f32 in ([1] if dtype == "f32" else [0, 1]):
+        C = torch.full((M, ldc), float("nan"), dtype=torch.float32 if c_f32 else torch.bfloat16, device="cuda")
+        C[:, :N] = 0
+        nb = lib.orbit_gemm_workspace_bytes(CODE[dtype], M, N, K, a_k, b_k)
+        ws = torch.empty(max(nb, 256), dtype=torch.uint8, device="cuda")
+        lib.orbit_gemm(CODE[dtype], M, N, K, Adev, lda, a_k, Bdev, ldb, b_k, C, ldc, c_f32, 1.0, None, c_f32, ws)
+        torch.cuda.synchronize()
+        got = host(C)
+        assert np.isnan(got[:, N:]).all(), "columns past N were written"
+        tol = TOL[dtype] if dtype == "f32" else 1e-2
+        check(f"gemm strided {layout} {shape} c_f32={c_f32}", got[:, :N], A.astype(np.float64) @ B, tol)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("dh", [32, 64, 128])
 @pytest.mark.parametrize("L", [1, 37, 130])
