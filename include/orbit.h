@@ -273,7 +273,11 @@ orbit_status orbit_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const vo
  * (Sec. III-A). Row t = b*L + l of q holds head h at q[t*ldq + h*head_dim];
  * likewise k, v, o. lse [B, H, L] float32 receives the natural-log
  * normaliser of each softmax row (needed by the backward). o32 (may be NULL,
- * leading dimension ldo32) receives a float32 copy of O. */
+ * leading dimension ldo32) receives a float32 copy of O. Leading dimensions
+ * are at least H*head_dim and multiples of 8. In bf16 mode the kernels
+ * address one (sample, head) slice with 32-bit byte offsets: (L + 256) times
+ * the largest leading dimension times 4 must stay below 2^31 (and B*H*L
+ * below 2^31), else ORBIT_E_UNSUPPORTED; the backward has the same limits. */
 orbit_status orbit_attention_fwd(int32_t dtype, int32_t B, int32_t H, int32_t L, int32_t head_dim,
                                  const void* q, int64_t ldq, const void* k, int64_t ldk,
                                  const void* v, int64_t ldv, void* o, int64_t ldo, float* lse,
